@@ -1,0 +1,254 @@
+#!/usr/bin/env python3
+"""Throughput of the bit-packed LUT-network forward pass on one MI355X.
+
+One step = one whole forward (encode -> LUT layers -> GroupSum head + argmax)
+over one batch already resident in HBM, through the C-ABI entry point
+bitlogic_forward.  Default workload: the CIFAR-100-shaped wide network
+(2^18 samples x 3072 uint8 features, 7 uniform thresholds = 21504 wires,
+2 x 64000 nodes with k = 6, 100 classes x 640), synthetic seeded data.
+
+Prints ONE JSON line.  Besides the driver's fields it carries
+  roofline      the dominant kernel (the LUT layer, integer-VALU bound at
+                k = 6) against the chip's 32-bit VALU peak, from per-launch
+                HIP-event times over a staged copy of the timed loop;
+  cpu_baseline  the CPU oracle timed on a bounded sample of the same
+                workload on this host (and its agreement with the GPU there);
+  detail        per-stage times, algorithmic bytes/ops and roofline fractions.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# MI355X peaks (published): HBM3E bandwidth; 32-bit VALU lane-ops from
+# 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+PEAK_HBM_GBS = 8000.0
+PEAK_VALU_TOPS = 256 * 64 * 2.4e9 / 1e12      # 39.32 T lane-ops/s
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lut_layer_c4_traffic.json")
+LUT_SOURCE = os.path.join(ROOT, "paper_2602_07400_amd", "csrc", "lut_layer.hip")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="c4_cifar100_wide")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target CPU time of the oracle baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--stage-steps", type=int, default=None,
+                    help="steps of the per-kernel (staged) timing loop; default = --steps")
+    return ap.parse_args()
+
+
+def algorithmic(cfg, n):
+    """Compulsory bytes and algorithmic 32-bit lane-ops per stage of one forward."""
+    W = (n + 63) // 64
+    D0 = cfg.d * cfg.b
+    st = {"encode": {"bytes": n * cfg.d + D0 * W * 8, "ops": n * D0}}
+    w_in = D0
+    for l, w in enumerate(cfg.widths):
+        st[f"layer{l + 1}"] = {"bytes": (w_in + w) * W * 8,
+                               "ops": 2 * ((1 << cfg.k) - 1) * w * W}
+        w_in = w
+    st["head"] = {"bytes": w_in * W * 8 + 4 * n * cfg.n_classes + 4 * n,
+                  "ops": n * w_in // 32}
+    for v in st.values():
+        v["roof_ms"] = max(v["bytes"] / (PEAK_HBM_GBS * 1e9), v["ops"] / (PEAK_VALU_TOPS * 1e12)) * 1e3
+        v["bound"] = "hbm" if v["bytes"] / (PEAK_HBM_GBS * 1e9) >= v["ops"] / (PEAK_VALU_TOPS * 1e12) else "alu"
+    return st
+
+
+def traffic_for_current_kernel():
+    """HBM bytes per LUT-layer launch from the committed rocprofv3 counter
+    summary, or None when the kernel source changed since it was taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+        with open(LUT_SOURCE, "rb") as f:
+            h = hashlib.sha256(f.read()).hexdigest()
+    except (OSError, ValueError):
+        return None
+    if rec.get("lut_layer_sha256") != h:
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (the path shards by samples with no exchange; "
+              f"a multi-GPU run is not part of this build); got --gpus {args.gpus}",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2602_07400_amd import bitlogic as bl
+    from paper_2602_07400_amd.workloads import CONFIGS, make_workload
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    cfg = CONFIGS[args.config]
+    t0 = time.time()
+    wl = make_workload(cfg, seed=args.seed)
+    print(f"[bench] {cfg.name}: generated inputs in {time.time() - t0:.1f}s", file=sys.stderr,
+          flush=True)
+    n = wl.n
+    model = bl.BitlogicModel.from_numpy(wl.thresholds, wl.layers, wl.n_classes, device=dev)
+    x = torch.from_numpy(wl.x).to(dev)
+    ws = torch.empty(model.workspace_bytes(n), dtype=torch.uint8, device=dev)
+    scores = torch.empty((n, cfg.n_classes), dtype=torch.int32, device=dev)
+    argmax = torch.empty((n,), dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step():
+        bl.bitlogic_forward(x, model.thresholds, model.layers, model.n_classes,
+                            scores=scores, argmax=argmax, workspace=ws, stream=stream)
+
+    # ---- warmup, then exactly K timed steps
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    ms_per_step = elapsed / args.steps * 1e3
+    value = n * args.steps / elapsed / 1e6
+    print(f"[bench] timed {args.steps} steps: {ms_per_step:.3f} ms/step, {value:.2f} MSamples/s",
+          file=sys.stderr, flush=True)
+
+    # ---- per-kernel times: the same kernels launched stage by stage on the
+    # same stream, HIP events between the stages
+    D0 = cfg.d * cfg.b
+    W = (n + 63) // 64
+    enc = torch.empty((D0, W), dtype=torch.int64, device=dev)
+    acts = [torch.empty((w, W), dtype=torch.int64, device=dev) for w in cfg.widths]
+    hws = torch.empty(max(1, bl.bitlogic_groupsum_head_workspace_bytes(cfg.widths[-1], n,
+                                                                       cfg.n_classes)),
+                      dtype=torch.uint8, device=dev)
+    names = ["encode"] + [f"layer{l + 1}" for l in range(len(cfg.widths))] + ["head"]
+
+    def staged(events=None):
+        rec = (lambda i: events[i].record(stream)) if events else (lambda i: None)
+        rec(0)
+        bl.bitlogic_encode(x, model.thresholds, bits_out=enc, stream=stream)
+        rec(1)
+        cur = enc
+        for l, (conn, tab) in enumerate(model.layers):
+            bl.bitlogic_lut_layer(cur, conn, tab, bits_out=acts[l], stream=stream)
+            cur = acts[l]
+            rec(2 + l)
+        bl.bitlogic_groupsum_head(cur, n, cfg.n_classes, scores=scores, argmax=argmax,
+                                  workspace=hws, stream=stream)
+        rec(2 + len(model.layers))
+
+    for _ in range(3):
+        staged()
+    torch.cuda.synchronize()
+    ksteps = args.stage_steps or args.steps
+    sums = np.zeros(len(names))
+    for _ in range(ksteps):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
+        staged(ev)
+        torch.cuda.synchronize()
+        sums += [ev[i].elapsed_time(ev[i + 1]) for i in range(len(names))]
+    stage_ms = dict(zip(names, (sums / ksteps).tolist()))
+
+    alg = algorithmic(cfg, n)
+    roof_sum = sum(v["roof_ms"] for v in alg.values())
+    layer_names = [k for k in names if k.startswith("layer")]
+    layer_ms = float(np.mean([stage_ms[k] for k in layer_names]))
+    layer_ops = alg["layer1"]["ops"]                          # identical for every layer
+    layer_bound = "alu" if alg["layer1"]["bound"] == "alu" else "hbm"
+    if layer_bound == "alu":
+        achieved = layer_ops / (layer_ms * 1e-3) / 1e12
+        peak, unit = PEAK_VALU_TOPS, "TOP/s"
+    else:
+        achieved = float(np.mean([alg[k]["bytes"] for k in layer_names])) / (layer_ms * 1e-3) / 1e9
+        peak, unit = PEAK_HBM_GBS, "GB/s"
+    roofline = {"bound": layer_bound, "achieved": round(achieved, 3), "peak": round(peak, 3),
+                "unit": unit, "frac": round(achieved / peak, 4),
+                "traffic": traffic_for_current_kernel() if cfg.name == "c4_cifar100_wide" else None,
+                "kernel": "k_lut_layer (one LUT layer launch; mean of the layer launches)",
+                "per_launch": f"2*(2^k-1)*w*W = {layer_ops} int32 lane-ops"}
+
+    detail = {
+        "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
+        "stage_roofline_ms": {k: round(v["roof_ms"], 4) for k, v in alg.items()},
+        "stage_bound": {k: v["bound"] for k, v in alg.items()},
+        "stage_achieved_GBs": {k: round(alg[k]["bytes"] / (stage_ms[k] * 1e-3) / 1e9, 1)
+                               for k in names},
+        "stage_achieved_TOPs": {k: round(alg[k]["ops"] / (stage_ms[k] * 1e-3) / 1e12, 3)
+                                for k in names},
+        "forward_roofline_ms": round(roof_sum, 4),
+        "forward_roofline_frac": round(roof_sum / ms_per_step, 4),
+        "staged_sum_ms": round(sum(stage_ms.values()), 4),
+        "gpu": torch.cuda.get_device_name(dev),
+        "hip": torch.version.hip,
+    }
+
+    # ---- CPU oracle on a bounded sample of the same workload
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = oracle.max_threads()
+        probe = min(n, 64)
+        t0 = time.perf_counter()
+        oracle.forward(wl.x[:probe], wl.thresholds, wl.layers, wl.n_classes)
+        per = (time.perf_counter() - t0) / probe
+        m = int(min(n, max(probe, args.cpu_seconds / max(per, 1e-9))))
+        idx = np.random.default_rng(1).choice(n, size=m, replace=False)
+        idx.sort()
+        xs = np.ascontiguousarray(wl.x[idx])
+        t0 = time.perf_counter()
+        rs, rp = oracle.forward(xs, wl.thresholds, wl.layers, wl.n_classes)
+        cpu_s = time.perf_counter() - t0
+        agree = bool(np.array_equal(scores.cpu().numpy()[idx], rs) and
+                     np.array_equal(argmax.cpu().numpy()[idx], rp))
+        cpu = {"value": round(m / cpu_s / 1e6, 6), "unit": "MSamples/s", "cores": threads,
+               "kind": "oracle",
+               "sample": f"{m} random samples of the {n}-sample batch, whole forward, "
+                         f"{cpu_s:.1f} s on {threads} OpenMP threads",
+               "gpu_agrees_on_sample": agree}
+        print(f"[bench] oracle: {m} samples in {cpu_s:.1f}s on {threads} threads; "
+              f"GPU agrees: {agree}", file=sys.stderr, flush=True)
+
+    out = {
+        "metric": "MSamples/s end-to-end LUT-net inference at 1 GPU; % of HBM/int-VALU roofline",
+        "value": round(value, 3),
+        "unit": "MSamples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u64 (bitwise on packed 64-sample words; u8 pixels, i32 scores)",
+        "data": "synthetic",
+        "config": {"workload": cfg.description, "name": cfg.name, "n_samples": n,
+                   "features": cfg.d, "thresholds": cfg.b, "widths": list(cfg.widths),
+                   "k": cfg.k, "classes": cfg.n_classes, "seed": args.seed},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "detail": detail,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,166 @@
+/*
+ * bitlogic.h -- C ABI of the bit-packed LUT-network inference path for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The network is the paper's forward composition (Sec. 3, Eq. 1):
+ *
+ *     encoder E : R^d -> {0,1}^{d b}          (thermometer, Sec. 3 "Encoders
+ *                                               and heads")
+ *     D layers  : node j of a layer reads k wires through its connection map
+ *                 M_j and outputs entry a of its 2^k-entry truth table, where
+ *                 a = sum_i x_{M_j(i)} 2^i   (Sec. 3 "Nodes are
+ *                 parameterizations", "Connectivity is the main per-layer
+ *                 design choice"; App. C.1 "Bit-packed inference")
+ *     head H    : class i scores the number of 1s among its group of g = w/c
+ *                 final-layer nodes; argmax is the predicted class
+ *                 (Sec. 3 "Encoders and heads", Sec. 5 "Head"; App. C.2)
+ *
+ * evaluated on bit-packed activations: 64 samples per 64-bit word along the
+ * batch (App. C.1 "Bit-packed inference").
+ *
+ * ---------------------------------------------------------------- layouts
+ * N = n_samples, W = ceil(N / 64) words.
+ * Packed bit tensor  uint64 [rows][W], row-major (row stride W words).  Bit
+ *                    (s % 64) of word [r][s / 64] is the value of row r for
+ *                    sample s.  Bits of samples s >= N ("padding") are
+ *                    written as 0 by bitlogic_encode; LUT layers compute
+ *                    whatever their tables give there; the head ignores them.
+ * Pixels             uint8 [N][d], row-major.
+ * Thresholds         uint8 [d][b]; wire f*b + t of sample s is
+ *                    (x[s][f] > thresholds[f][t]) -- a strict comparison on
+ *                    the raw 0..255 pixel scale.
+ * Connections        int32 [w_out][k]; entry [j][i] is the wire feeding
+ *                    address bit i of node j; 0 <= conn < w_in, repeats
+ *                    allowed.
+ * Truth tables       uint64 [w_out]; entry a of node j is bit a of
+ *                    tables[j]; bits >= 2^k are ignored.
+ * Scores             int32 [N][c], row-major; class i of sample s.
+ * Argmax             int32 [N]; lowest class index among the maxima.
+ *
+ * ------------------------------------------------------------ conventions
+ * - Every array argument is a DEVICE pointer (memory the GPU can read or
+ *   write), except the bitlogic_layer descriptor array of bitlogic_forward,
+ *   which is a HOST array (its members are device pointers).
+ * - The caller owns every buffer.  No entry point allocates or frees device
+ *   memory; scratch comes from a caller-supplied workspace of at least the
+ *   size the matching *_workspace_bytes query returns.
+ * - Calls are asynchronous: work is enqueued on `stream` (a hipStream_t
+ *   passed as void*; NULL is the null stream) and BITLOGIC_OK means "validated
+ *   and enqueued".  Inputs must stay valid until the stream has run the work.
+ * - Arguments are checked on the host before anything is enqueued; a failed
+ *   check returns an error code, launches nothing and touches no memory.
+ *   Connection indices are device data and are NOT range-checked: an index
+ *   outside [0, w_in) is undefined behaviour.  The Python binding checks
+ *   them on the host when it builds a model.
+ * - Packed bit buffers (bits_in, bits_out, bits) must be 8-byte aligned
+ *   (16-byte alignment together with an even word count W lets the kernels
+ *   use 16-byte accesses); the workspace must be 256-byte aligned.  Pixels,
+ *   thresholds, connections, tables, scores and argmax need only their
+ *   natural alignment.
+ * - Buffers written by a call must not overlap any buffer it reads.
+ * - A HIP launch failure returns BITLOGIC_ERR_HIP; bitlogic_last_error()
+ *   then names the runtime's error.
+ * - Limits: 1 <= k <= 6; n_samples >= 0 (0 enqueues nothing);
+ *   1 <= n_thresholds <= 64; every row count fits in int32; the head needs
+ *   w % n_classes == 0 and g = w / n_classes <= 65535.
+ * - Entry points are thread-safe; calls on one stream run in order.
+ */
+#ifndef BITLOGIC_H
+#define BITLOGIC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum bitlogic_status {
+    BITLOGIC_OK = 0,
+    BITLOGIC_ERR_NULL = 1,         /* a required pointer is NULL */
+    BITLOGIC_ERR_SHAPE = 2,        /* a size is out of range or inconsistent */
+    BITLOGIC_ERR_ALIGN = 3,        /* a buffer is not aligned as required */
+    BITLOGIC_ERR_UNSUPPORTED = 4,  /* e.g. k outside 1..6 */
+    BITLOGIC_ERR_HIP = 5,          /* the HIP runtime reported an error */
+    BITLOGIC_ERR_WORKSPACE = 6     /* workspace smaller than required */
+} bitlogic_status;
+
+/* Thermometer encoder and bit-pack (Sec. 3 "Encoders and heads"; App. A
+ * "Initialization": linear or quantile threshold ladders; App. C.1: 64
+ * samples per 64-bit word).
+ *   x           uint8 [n_samples][n_features]
+ *   thresholds  uint8 [n_features][n_thresholds]
+ *   bits_out    uint64 [n_features * n_thresholds][W]; padding bits are 0.
+ * Any threshold values are accepted (they need not be sorted). */
+int bitlogic_encode(const uint8_t *x, int64_t n_samples, int32_t n_features,
+                    const uint8_t *thresholds, int32_t n_thresholds,
+                    uint64_t *bits_out, void *stream);
+
+/* One LUT layer on packed bits (Sec. 3: connection map M_j, fan-in n = k,
+ * 2^k-entry truth table; App. C.1: bitwise evaluation of 64 samples per op).
+ *   bits_in   uint64 [w_in][n_words]
+ *   conn      int32  [w_out][k]
+ *   tables    uint64 [w_out]
+ *   bits_out  uint64 [w_out][n_words]
+ * Bit s of bits_out[j][.] = (tables[j] >> a) & 1 with
+ * a = sum_i bit_s(bits_in[conn[j][i]][.]) << i. */
+int bitlogic_lut_layer(const uint64_t *bits_in, int32_t w_in, int64_t n_words,
+                       const int32_t *conn, const uint64_t *tables,
+                       int32_t w_out, int32_t k, uint64_t *bits_out,
+                       void *stream);
+
+/* Scratch bytes bitlogic_groupsum_head needs for these sizes. */
+size_t bitlogic_groupsum_head_workspace_bytes(int32_t w, int64_t n_samples,
+                                              int32_t n_classes);
+
+/* GroupSum popcount head and argmax (Sec. 3 "Encoders and heads"; Sec. 5
+ * "Head"; App. C.2: the deployed design outputs the class index).
+ *   bits     uint64 [w][W], the last layer's output
+ *   scores   int32 [n_samples][n_classes], or NULL to skip
+ *   argmax   int32 [n_samples], or NULL to skip (not both NULL)
+ * Class i owns nodes [i*g, (i+1)*g), g = w / n_classes. */
+int bitlogic_groupsum_head(const uint64_t *bits, int32_t w, int64_t n_samples,
+                           int32_t n_classes, int32_t *scores, int32_t *argmax,
+                           void *workspace, size_t workspace_bytes,
+                           void *stream);
+
+/* One layer of a network: device pointers plus its shape. */
+typedef struct bitlogic_layer {
+    const int32_t *conn;      /* int32 [w_out][k] */
+    const uint64_t *tables;   /* uint64 [w_out] */
+    int32_t w_out;
+    int32_t k;
+} bitlogic_layer;
+
+/* Scratch bytes bitlogic_forward needs for these sizes (0 on bad shapes). */
+size_t bitlogic_forward_workspace_bytes(int64_t n_samples, int32_t n_features,
+                                        int32_t n_thresholds,
+                                        const bitlogic_layer *layers,
+                                        int32_t n_layers, int32_t n_classes);
+
+/* Whole forward pass, encoder -> n_layers LUT layers -> head (Sec. 3,
+ * Eq. 1; App. C.1): pixels in device memory to scores and argmax in
+ * device memory.  Layer 0 reads the n_features * n_thresholds encoder wires
+ * and layer l > 0 reads layer l-1, so w_in(l) = layers[l-1].w_out.
+ * `layers` is a host array of n_layers >= 1 descriptors.  The encoded and
+ * intermediate bit tensors live in the workspace. */
+int bitlogic_forward(const uint8_t *x, int64_t n_samples, int32_t n_features,
+                     const uint8_t *thresholds, int32_t n_thresholds,
+                     const bitlogic_layer *layers, int32_t n_layers,
+                     int32_t n_classes, int32_t *scores, int32_t *argmax,
+                     void *workspace, size_t workspace_bytes, void *stream);
+
+/* Static description of a status code. */
+const char *bitlogic_status_string(int status);
+
+/* Detail of the last failing call on this host thread ("" if none). */
+const char *bitlogic_last_error(void);
+
+/* Library version, major * 10000 + minor * 100 + patch. */
+int bitlogic_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BITLOGIC_H */

@@ -1,0 +1,270 @@
+"""Python binding of libbitlogic (C ABI in include/bitlogic.h).
+
+Argument marshalling only: every step of the forward pass runs in the HIP
+kernels of ``libbitlogic.so``.  Tensors are torch tensors on the GPU; their
+``data_ptr()`` is handed to the C ABI together with the current HIP stream.
+Packed bit tensors are ``torch.int64`` (the same 64 bits the C side reads as
+``uint64``); ``torch.uint64`` tensors are accepted too.
+
+If the shared library has not been built, every call raises: there is no
+fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import List, Optional, Sequence, Tuple
+
+import numpy as np
+import torch
+
+__all__ = [
+    "BitlogicError", "bitlogic_encode", "bitlogic_lut_layer", "bitlogic_groupsum_head",
+    "bitlogic_forward", "bitlogic_forward_workspace_bytes",
+    "bitlogic_groupsum_head_workspace_bytes", "bitlogic_status_string", "bitlogic_version",
+    "BitlogicModel", "library_path", "load_library", "words",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libbitlogic.so")
+
+OK = 0
+_lib = None
+
+
+class BitlogicError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        self.status = status
+        super().__init__(f"bitlogic status {status} ({bitlogic_status_string(status)}): {detail}")
+
+
+class _Layer(ctypes.Structure):
+    _fields_ = [("conn", ctypes.c_void_p), ("tables", ctypes.c_void_p),
+                ("w_out", ctypes.c_int32), ("k", ctypes.c_int32)]
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load_library():
+    """Load libbitlogic.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError(
+            f"{_LIB_PATH} is missing: build it with __graft_entry__.build() "
+            "(hipcc --offload-arch=gfx950); there is no fallback path")
+    lib = ctypes.CDLL(_LIB_PATH)
+    P, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    sig = {
+        "bitlogic_encode": ([P, i64, i32, P, i32, P, P], ctypes.c_int),
+        "bitlogic_lut_layer": ([P, i32, i64, P, P, i32, i32, P, P], ctypes.c_int),
+        "bitlogic_groupsum_head_workspace_bytes": ([i32, i64, i32], sz),
+        "bitlogic_groupsum_head": ([P, i32, i64, i32, P, P, P, sz, P], ctypes.c_int),
+        "bitlogic_forward_workspace_bytes": ([i64, i32, i32, P, i32, i32], sz),
+        "bitlogic_forward": ([P, i64, i32, P, i32, P, i32, i32, P, P, P, sz, P], ctypes.c_int),
+        "bitlogic_status_string": ([ctypes.c_int], ctypes.c_char_p),
+        "bitlogic_last_error": ([], ctypes.c_char_p),
+        "bitlogic_version": ([], ctypes.c_int),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = res
+    _lib = lib
+    return lib
+
+
+def bitlogic_status_string(status: int) -> str:
+    return load_library().bitlogic_status_string(int(status)).decode()
+
+
+def bitlogic_version() -> int:
+    return int(load_library().bitlogic_version())
+
+
+def _check(rc: int) -> None:
+    if rc != OK:
+        raise BitlogicError(rc, load_library().bitlogic_last_error().decode())
+
+
+def words(n_samples: int) -> int:
+    return (int(n_samples) + 63) // 64
+
+
+def _stream(stream, device) -> int:
+    if stream is None:
+        return torch.cuda.current_stream(device).cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _dev(t: torch.Tensor, name: str, dtypes) -> int:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on the GPU")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+_U8 = (torch.uint8,)
+_I32 = (torch.int32,)
+_U64 = (torch.int64, torch.uint64)
+
+
+def bitlogic_encode(x: torch.Tensor, thresholds: torch.Tensor,
+                    bits_out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """x uint8 [N][d], thresholds uint8 [d][b] -> packed wires int64 [d*b][ceil(N/64)]."""
+    n, d = x.shape
+    b = thresholds.shape[1]
+    if bits_out is None:
+        bits_out = torch.empty((d * b, words(n)), dtype=torch.int64, device=x.device)
+    _check(load_library().bitlogic_encode(
+        _dev(x, "x", _U8), n, d, _dev(thresholds, "thresholds", _U8), b,
+        _dev(bits_out, "bits_out", _U64), _stream(stream, x.device)))
+    return bits_out
+
+
+def bitlogic_lut_layer(bits_in: torch.Tensor, conn: torch.Tensor, tables: torch.Tensor,
+                       bits_out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """bits_in [w_in][W], conn int32 [w][k], tables [w] -> bits_out [w][W]."""
+    w_in, n_words = bits_in.shape
+    w, k = conn.shape
+    if bits_out is None:
+        bits_out = torch.empty((w, n_words), dtype=torch.int64, device=bits_in.device)
+    _check(load_library().bitlogic_lut_layer(
+        _dev(bits_in, "bits_in", _U64), w_in, n_words, _dev(conn, "conn", _I32),
+        _dev(tables, "tables", _U64), w, k, _dev(bits_out, "bits_out", _U64),
+        _stream(stream, bits_in.device)))
+    return bits_out
+
+
+def bitlogic_groupsum_head_workspace_bytes(w: int, n_samples: int, n_classes: int) -> int:
+    return int(load_library().bitlogic_groupsum_head_workspace_bytes(w, n_samples, n_classes))
+
+
+def _workspace(nbytes: int, device, given: Optional[torch.Tensor]) -> Tuple[int, int]:
+    if given is not None:
+        return _dev(given, "workspace", (torch.uint8,)), given.numel()
+    if nbytes == 0:
+        return 0, 0
+    buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    _workspace.keep = buf        # kept alive until the next call allocates one
+    return buf.data_ptr(), nbytes
+
+
+def bitlogic_groupsum_head(bits: torch.Tensor, n_samples: int, n_classes: int,
+                           scores: Optional[torch.Tensor] = None,
+                           argmax: Optional[torch.Tensor] = None,
+                           workspace: Optional[torch.Tensor] = None, stream=None,
+                           want_scores: bool = True):
+    """bits [w][W] -> (scores int32 [N][c] or None, argmax int32 [N])."""
+    w = bits.shape[0]
+    dev = bits.device
+    if scores is None and want_scores:
+        scores = torch.empty((n_samples, n_classes), dtype=torch.int32, device=dev)
+    if argmax is None:
+        argmax = torch.empty((n_samples,), dtype=torch.int32, device=dev)
+    ws_ptr, ws_bytes = _workspace(bitlogic_groupsum_head_workspace_bytes(w, n_samples, n_classes),
+                                  dev, workspace)
+    _check(load_library().bitlogic_groupsum_head(
+        _dev(bits, "bits", _U64), w, n_samples, n_classes,
+        _dev(scores, "scores", _I32) if scores is not None else None,
+        _dev(argmax, "argmax", _I32), ws_ptr, ws_bytes, _stream(stream, dev)))
+    return scores, argmax
+
+
+def _layer_array(layers: Sequence[Tuple[torch.Tensor, torch.Tensor]]):
+    arr = (_Layer * len(layers))()
+    for l, (conn, tables) in enumerate(layers):
+        arr[l].conn = _dev(conn, f"conn[{l}]", _I32)
+        arr[l].tables = _dev(tables, f"tables[{l}]", _U64)
+        arr[l].w_out = conn.shape[0]
+        arr[l].k = conn.shape[1]
+    return arr
+
+
+def bitlogic_forward_workspace_bytes(n_samples: int, n_features: int, n_thresholds: int,
+                                     layers, n_classes: int) -> int:
+    arr = _layer_array(layers)
+    return int(load_library().bitlogic_forward_workspace_bytes(
+        n_samples, n_features, n_thresholds, ctypes.cast(arr, ctypes.c_void_p), len(layers),
+        n_classes))
+
+
+def bitlogic_forward(x: torch.Tensor, thresholds: torch.Tensor,
+                     layers: Sequence[Tuple[torch.Tensor, torch.Tensor]], n_classes: int,
+                     scores: Optional[torch.Tensor] = None,
+                     argmax: Optional[torch.Tensor] = None,
+                     workspace: Optional[torch.Tensor] = None, stream=None,
+                     want_scores: bool = True):
+    """Whole forward: pixels uint8 [N][d] -> (scores int32 [N][c], argmax int32 [N])."""
+    n, d = x.shape
+    b = thresholds.shape[1]
+    dev = x.device
+    arr = _layer_array(layers)
+    lib = load_library()
+    need = int(lib.bitlogic_forward_workspace_bytes(
+        n, d, b, ctypes.cast(arr, ctypes.c_void_p), len(arr), n_classes))
+    if need == 0:
+        _check(lib.bitlogic_forward(_dev(x, "x", _U8), n, d, _dev(thresholds, "thresholds", _U8),
+                                    b, ctypes.cast(arr, ctypes.c_void_p), len(arr), n_classes,
+                                    None, None, None, 0, _stream(stream, dev)))
+    if scores is None and want_scores:
+        scores = torch.empty((n, n_classes), dtype=torch.int32, device=dev)
+    if argmax is None:
+        argmax = torch.empty((n,), dtype=torch.int32, device=dev)
+    ws_ptr, ws_bytes = _workspace(need, dev, workspace)
+    _check(lib.bitlogic_forward(
+        _dev(x, "x", _U8), n, d, _dev(thresholds, "thresholds", _U8), b,
+        ctypes.cast(arr, ctypes.c_void_p), len(arr), n_classes,
+        _dev(scores, "scores", _I32) if scores is not None else None,
+        _dev(argmax, "argmax", _I32), ws_ptr, ws_bytes, _stream(stream, dev)))
+    return scores, argmax
+
+
+@dataclass
+class BitlogicModel:
+    """A network resident in device memory: thresholds, per-layer conn/tables."""
+    thresholds: torch.Tensor
+    layers: List[Tuple[torch.Tensor, torch.Tensor]]
+    n_classes: int
+
+    @classmethod
+    def from_numpy(cls, thresholds: np.ndarray, layers, n_classes: int,
+                   device="cuda") -> "BitlogicModel":
+        """Copy a host model to the GPU, checking every connection index."""
+        th = np.ascontiguousarray(thresholds, dtype=np.uint8)
+        if th.ndim != 2:
+            raise ValueError("thresholds must be [d][b]")
+        w_in = th.shape[0] * th.shape[1]
+        dev_layers = []
+        for l, (conn, tables) in enumerate(layers):
+            conn = np.ascontiguousarray(conn, dtype=np.int32)
+            tables = np.ascontiguousarray(tables, dtype=np.uint64)
+            if conn.ndim != 2 or tables.shape != (conn.shape[0],):
+                raise ValueError(f"layer {l}: conn [w][k] and tables [w] expected")
+            if conn.size and (conn.min() < 0 or conn.max() >= w_in):
+                raise ValueError(f"layer {l}: connection index outside [0, {w_in})")
+            dev_layers.append((torch.from_numpy(conn).to(device),
+                               torch.from_numpy(tables.view(np.int64)).to(device)))
+            w_in = conn.shape[0]
+        if w_in % n_classes != 0:
+            raise ValueError("last width must be a multiple of n_classes")
+        return cls(torch.from_numpy(th).to(device), dev_layers, int(n_classes))
+
+    def workspace_bytes(self, n_samples: int) -> int:
+        return bitlogic_forward_workspace_bytes(n_samples, self.thresholds.shape[0],
+                                                self.thresholds.shape[1], self.layers,
+                                                self.n_classes)
+
+    def forward(self, x: torch.Tensor, **kw):
+        return bitlogic_forward(x, self.thresholds, self.layers, self.n_classes, **kw)

@@ -1,0 +1,288 @@
+// C-ABI front end of libbitlogic: argument checks on the host, workspace
+// carving, launches.  Every check runs before any HIP runtime call, so a
+// rejected call enqueues nothing (and needs no GPU to be rejected).
+#include <stdarg.h>
+#include <stdio.h>
+
+#include "../../include/bitlogic.h"
+#include "bl_internal.h"
+
+namespace {
+
+thread_local char g_last_error[256] = "";
+
+int fail(int status, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+    va_end(ap);
+    return status;
+}
+
+int ok()
+{
+    g_last_error[0] = '\0';
+    return BITLOGIC_OK;
+}
+
+int hip_status(hipError_t e, const char *what)
+{
+    if (e != hipSuccess)
+        return fail(BITLOGIC_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    return ok();
+}
+
+bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p % a) == 0; }
+
+constexpr int64_t kMaxRows = 0x7fffffff;
+constexpr size_t kWsAlign = 256;
+
+size_t round_up(size_t v) { return (v + kWsAlign - 1) / kWsAlign * kWsAlign; }
+
+int64_t words_of(int64_t n) { return (n + 63) / 64; }
+
+int check_encode(const uint8_t *x, int64_t n, int32_t d, const uint8_t *th, int32_t b,
+                 const uint64_t *out)
+{
+    if (!x || !th || !out)
+        return fail(BITLOGIC_ERR_NULL, "encode: NULL pointer");
+    if (n < 0 || d <= 0 || b <= 0 || b > 64)
+        return fail(BITLOGIC_ERR_SHAPE, "encode: need n >= 0, d > 0, 1 <= b <= 64");
+    if ((int64_t)d * b > kMaxRows)
+        return fail(BITLOGIC_ERR_SHAPE, "encode: d * b exceeds int32");
+    if (!aligned(out, 8))
+        return fail(BITLOGIC_ERR_ALIGN, "encode: bits_out not 8-byte aligned");
+    return BITLOGIC_OK;
+}
+
+int check_layer(const uint64_t *in, int32_t w_in, int64_t n_words, const int32_t *conn,
+                const uint64_t *tables, int32_t w_out, int32_t k, const uint64_t *out,
+                const char *who)
+{
+    if (!in || !conn || !tables || !out)
+        return fail(BITLOGIC_ERR_NULL, "%s: NULL pointer", who);
+    if (k < 1 || k > 6)
+        return fail(BITLOGIC_ERR_UNSUPPORTED, "%s: fan-in k=%d outside 1..6", who, k);
+    if (w_in <= 0 || w_out <= 0 || n_words < 0)
+        return fail(BITLOGIC_ERR_SHAPE, "%s: need w_in > 0, w_out > 0, n_words >= 0", who);
+    if (n_words > ((int64_t)1 << 40))
+        return fail(BITLOGIC_ERR_SHAPE, "%s: n_words too large", who);
+    if (!aligned(in, 8) || !aligned(out, 8))
+        return fail(BITLOGIC_ERR_ALIGN, "%s: bit buffers must be 8-byte aligned", who);
+    if (!aligned(conn, 4) || !aligned(tables, 8))
+        return fail(BITLOGIC_ERR_ALIGN, "%s: conn/tables misaligned", who);
+    return BITLOGIC_OK;
+}
+
+int check_head(const uint64_t *bits, int32_t w, int64_t n, int32_t c, const int32_t *scores,
+               const int32_t *argmax)
+{
+    if (!bits || (!scores && !argmax))
+        return fail(BITLOGIC_ERR_NULL, "head: NULL bits, or both outputs NULL");
+    if (w <= 0 || c <= 0 || n < 0)
+        return fail(BITLOGIC_ERR_SHAPE, "head: need w > 0, c > 0, n >= 0");
+    if (w % c != 0)
+        return fail(BITLOGIC_ERR_SHAPE, "head: w=%d not a multiple of n_classes=%d", w, c);
+    if (w / c > 65535)
+        return fail(BITLOGIC_ERR_SHAPE, "head: group size %d > 65535", w / c);
+    if (n > ((int64_t)1 << 40))
+        return fail(BITLOGIC_ERR_SHAPE, "head: n_samples too large");
+    if (!aligned(bits, 8) || (scores && !aligned(scores, 4)) || (argmax && !aligned(argmax, 4)))
+        return fail(BITLOGIC_ERR_ALIGN, "head: misaligned buffer");
+    return BITLOGIC_OK;
+}
+
+struct ForwardPlan {
+    int64_t W;
+    int32_t widest;
+    size_t off_enc, off_a, off_b, off_head, total;
+    bl::HeadPlan head;
+};
+
+int plan_forward(int64_t n, int32_t d, int32_t b, const bitlogic_layer *layers, int32_t L,
+                 int32_t c, ForwardPlan *fp)
+{
+    if (!layers)
+        return fail(BITLOGIC_ERR_NULL, "forward: NULL layer array");
+    if (L < 1)
+        return fail(BITLOGIC_ERR_SHAPE, "forward: need n_layers >= 1");
+    if (n < 0 || d <= 0 || b <= 0 || b > 64 || c <= 0)
+        return fail(BITLOGIC_ERR_SHAPE, "forward: need n >= 0, d > 0, 1 <= b <= 64, c > 0");
+    if ((int64_t)d * b > kMaxRows)
+        return fail(BITLOGIC_ERR_SHAPE, "forward: d * b exceeds int32");
+    if (n > ((int64_t)1 << 40))
+        return fail(BITLOGIC_ERR_SHAPE, "forward: n_samples too large");
+    int32_t widest = 0;
+    for (int32_t l = 0; l < L; ++l) {
+        if (!layers[l].conn || !layers[l].tables)
+            return fail(BITLOGIC_ERR_NULL, "forward: layer %d has a NULL pointer", l);
+        if (layers[l].k < 1 || layers[l].k > 6)
+            return fail(BITLOGIC_ERR_UNSUPPORTED, "forward: layer %d fan-in %d outside 1..6",
+                        l, layers[l].k);
+        if (layers[l].w_out <= 0)
+            return fail(BITLOGIC_ERR_SHAPE, "forward: layer %d width %d", l, layers[l].w_out);
+        if (!aligned(layers[l].conn, 4) || !aligned(layers[l].tables, 8))
+            return fail(BITLOGIC_ERR_ALIGN, "forward: layer %d conn/tables misaligned", l);
+        if (layers[l].w_out > widest)
+            widest = layers[l].w_out;
+    }
+    const int32_t w_last = layers[L - 1].w_out;
+    if (w_last % c != 0)
+        return fail(BITLOGIC_ERR_SHAPE, "forward: last width %d not a multiple of %d classes",
+                    w_last, c);
+    if (w_last / c > 65535)
+        return fail(BITLOGIC_ERR_SHAPE, "forward: group size %d > 65535", w_last / c);
+    fp->W = words_of(n);
+    fp->widest = widest;
+    const size_t enc = (size_t)d * b * fp->W * sizeof(uint64_t);
+    const size_t act = (size_t)widest * fp->W * sizeof(uint64_t);
+    fp->head = bl::plan_head(w_last, n, c);
+    fp->off_enc = 0;
+    fp->off_a = round_up(enc);
+    fp->off_b = fp->off_a + round_up(act);
+    fp->off_head = fp->off_b + (L > 1 ? round_up(act) : 0);
+    fp->total = fp->off_head + round_up(fp->head.ws_bytes);
+    return BITLOGIC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int bitlogic_encode(const uint8_t *x, int64_t n_samples, int32_t n_features,
+                    const uint8_t *thresholds, int32_t n_thresholds, uint64_t *bits_out,
+                    void *stream)
+{
+    int st = check_encode(x, n_samples, n_features, thresholds, n_thresholds, bits_out);
+    if (st != BITLOGIC_OK)
+        return st;
+    if (n_samples == 0)
+        return ok();
+    return hip_status(bl::launch_encode(x, n_samples, n_features, thresholds, n_thresholds,
+                                        bits_out, (hipStream_t)stream),
+                      "encode launch");
+}
+
+int bitlogic_lut_layer(const uint64_t *bits_in, int32_t w_in, int64_t n_words,
+                       const int32_t *conn, const uint64_t *tables, int32_t w_out, int32_t k,
+                       uint64_t *bits_out, void *stream)
+{
+    int st = check_layer(bits_in, w_in, n_words, conn, tables, w_out, k, bits_out, "lut_layer");
+    if (st != BITLOGIC_OK)
+        return st;
+    if (n_words == 0)
+        return ok();
+    return hip_status(bl::launch_lut_layer(bits_in, w_in, n_words, conn, tables, w_out, k,
+                                           bits_out, (hipStream_t)stream),
+                      "lut_layer launch");
+}
+
+size_t bitlogic_groupsum_head_workspace_bytes(int32_t w, int64_t n_samples, int32_t n_classes)
+{
+    if (w <= 0 || n_classes <= 0 || n_samples < 0 || w % n_classes != 0 ||
+        w / n_classes > 65535 || n_samples > ((int64_t)1 << 40))
+        return 0;
+    return bl::plan_head(w, n_samples, n_classes).ws_bytes;
+}
+
+int bitlogic_groupsum_head(const uint64_t *bits, int32_t w, int64_t n_samples,
+                           int32_t n_classes, int32_t *scores, int32_t *argmax,
+                           void *workspace, size_t workspace_bytes, void *stream)
+{
+    int st = check_head(bits, w, n_samples, n_classes, scores, argmax);
+    if (st != BITLOGIC_OK)
+        return st;
+    const bl::HeadPlan plan = bl::plan_head(w, n_samples, n_classes);
+    if (plan.ws_bytes > 0 && !workspace)
+        return fail(BITLOGIC_ERR_NULL, "head: NULL workspace");
+    if (workspace_bytes < plan.ws_bytes)
+        return fail(BITLOGIC_ERR_WORKSPACE, "head: workspace %zu < %zu bytes", workspace_bytes,
+                    plan.ws_bytes);
+    if (workspace && !aligned(workspace, kWsAlign))
+        return fail(BITLOGIC_ERR_ALIGN, "head: workspace not 256-byte aligned");
+    if (n_samples == 0)
+        return ok();
+    return hip_status(bl::launch_head(bits, w, n_samples, n_classes, scores, argmax, workspace,
+                                      plan, (hipStream_t)stream),
+                      "head launch");
+}
+
+size_t bitlogic_forward_workspace_bytes(int64_t n_samples, int32_t n_features,
+                                        int32_t n_thresholds, const bitlogic_layer *layers,
+                                        int32_t n_layers, int32_t n_classes)
+{
+    ForwardPlan fp;
+    if (plan_forward(n_samples, n_features, n_thresholds, layers, n_layers, n_classes, &fp) !=
+        BITLOGIC_OK)
+        return 0;
+    return fp.total;
+}
+
+int bitlogic_forward(const uint8_t *x, int64_t n_samples, int32_t n_features,
+                     const uint8_t *thresholds, int32_t n_thresholds,
+                     const bitlogic_layer *layers, int32_t n_layers, int32_t n_classes,
+                     int32_t *scores, int32_t *argmax, void *workspace, size_t workspace_bytes,
+                     void *stream)
+{
+    if (!x || !thresholds || (!scores && !argmax))
+        return fail(BITLOGIC_ERR_NULL, "forward: NULL pixels/thresholds or both outputs NULL");
+    ForwardPlan fp;
+    int st = plan_forward(n_samples, n_features, n_thresholds, layers, n_layers, n_classes, &fp);
+    if (st != BITLOGIC_OK)
+        return st;
+    if (!workspace)
+        return fail(BITLOGIC_ERR_NULL, "forward: NULL workspace");
+    if (workspace_bytes < fp.total)
+        return fail(BITLOGIC_ERR_WORKSPACE, "forward: workspace %zu < %zu bytes",
+                    workspace_bytes, fp.total);
+    if (!aligned(workspace, kWsAlign))
+        return fail(BITLOGIC_ERR_ALIGN, "forward: workspace not 256-byte aligned");
+    if ((scores && !aligned(scores, 4)) || (argmax && !aligned(argmax, 4)))
+        return fail(BITLOGIC_ERR_ALIGN, "forward: misaligned output");
+    if (n_samples == 0)
+        return ok();
+
+    hipStream_t s = (hipStream_t)stream;
+    char *ws = static_cast<char *>(workspace);
+    uint64_t *enc = reinterpret_cast<uint64_t *>(ws + fp.off_enc);
+    uint64_t *act[2] = {reinterpret_cast<uint64_t *>(ws + fp.off_a),
+                        reinterpret_cast<uint64_t *>(ws + fp.off_b)};
+    hipError_t e = bl::launch_encode(x, n_samples, n_features, thresholds, n_thresholds, enc, s);
+    if (e != hipSuccess)
+        return hip_status(e, "forward: encode launch");
+    const uint64_t *cur = enc;
+    int32_t w_in = n_features * n_thresholds;
+    for (int32_t l = 0; l < n_layers; ++l) {
+        uint64_t *dst = act[l & 1];
+        e = bl::launch_lut_layer(cur, w_in, fp.W, layers[l].conn, layers[l].tables,
+                                 layers[l].w_out, layers[l].k, dst, s);
+        if (e != hipSuccess)
+            return fail(BITLOGIC_ERR_HIP, "forward: layer %d launch: %s", l, hipGetErrorString(e));
+        cur = dst;
+        w_in = layers[l].w_out;
+    }
+    e = bl::launch_head(cur, w_in, n_samples, n_classes, scores, argmax, ws + fp.off_head,
+                        fp.head, s);
+    return hip_status(e, "forward: head launch");
+}
+
+const char *bitlogic_status_string(int status)
+{
+    switch (status) {
+    case BITLOGIC_OK: return "ok";
+    case BITLOGIC_ERR_NULL: return "a required pointer is NULL";
+    case BITLOGIC_ERR_SHAPE: return "a size is out of range or inconsistent";
+    case BITLOGIC_ERR_ALIGN: return "a buffer is not aligned as required";
+    case BITLOGIC_ERR_UNSUPPORTED: return "unsupported parameter";
+    case BITLOGIC_ERR_HIP: return "HIP runtime error";
+    case BITLOGIC_ERR_WORKSPACE: return "workspace too small";
+    default: return "unknown status";
+    }
+}
+
+const char *bitlogic_last_error(void) { return g_last_error; }
+
+int bitlogic_version(void) { return 100; }
+
+}  // extern "C"

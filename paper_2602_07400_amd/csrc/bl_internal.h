@@ -1,0 +1,42 @@
+// Library-internal declarations shared by the kernel translation units and
+// the C-ABI front end.  Nothing here is part of the public interface.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace bl {
+
+constexpr int kWave = 64;       // CDNA wavefront width
+constexpr int kXcds = 8;        // MI355X: 8 accelerator dies, each with its own L2
+
+// Workgroups are dealt to the XCDs round-robin by workgroup id.  These helpers
+// turn a linear id into (xcd, index within that xcd).
+__device__ __forceinline__ int xcd_of(int bid) { return bid % kXcds; }
+__device__ __forceinline__ int local_of(int bid) { return bid / kXcds; }
+
+// ---- launchers (each returns the hipError_t of its launch) ----
+
+hipError_t launch_encode(const uint8_t *x, int64_t n, int32_t d,
+                         const uint8_t *thresholds, int32_t b, uint64_t *out,
+                         hipStream_t stream);
+
+hipError_t launch_lut_layer(const uint64_t *in, int32_t w_in, int64_t n_words,
+                            const int32_t *conn, const uint64_t *tables,
+                            int32_t w_out, int32_t k, uint64_t *out,
+                            hipStream_t stream);
+
+struct HeadPlan {
+    int32_t splits;        // row splits per class group
+    int32_t planes;        // bit planes per split counter
+    int32_t rows_per_split;
+    size_t ws_bytes;       // scratch bytes
+};
+HeadPlan plan_head(int32_t w, int64_t n, int32_t c);
+
+hipError_t launch_head(const uint64_t *bits, int32_t w, int64_t n, int32_t c,
+                       int32_t *scores, int32_t *argmax, void *ws,
+                       const HeadPlan &plan, hipStream_t stream);
+
+}  // namespace bl

@@ -1,0 +1,213 @@
+// GroupSum popcount head + argmax on gfx950.
+//
+// score[s][i] = number of 1s among nodes [i*g, (i+1)*g) for sample s, and
+// argmax[s] = lowest i with the largest score (Sec. 3 "Encoders and heads";
+// Sec. 5 "Head"; App. C.2, where the deployed design outputs the class index).
+//
+// Packed words count *across* samples, but a score counts one sample
+// *across* nodes: a positional ("vertical") popcount.  Stage 1 keeps, per
+// 64-sample column, a bit-sliced counter (plane p holds bit p of 64 counts)
+// and adds the group's words into it with a Harley-Seal carry-save tree
+// (v_bitop3 full adders, ~2 ops per word per 32 samples), one lane per column
+// so every row load is a coalesced 512-byte segment.  Long groups are split
+// into row ranges so the launch fills the chip.  Stage 2 runs one lane per
+// sample: it reads the planes of its column (wave-uniform scalar loads),
+// assembles each class score bit by bit, sums the splits and tracks the
+// running argmax.
+#include "bl_internal.h"
+
+namespace bl {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / kWave;
+constexpr int kMaxPlanes = 16;
+
+__device__ __forceinline__ void csa(uint64_t &h, uint64_t &l, uint64_t a, uint64_t b,
+                                    uint64_t c)
+{
+    const uint64_t u = a ^ b;
+    h = (a & b) | (u & c);
+    l = u ^ c;
+}
+
+template <int P>
+__device__ __forceinline__ void ripple_add(uint64_t (&cnt)[P], uint64_t carry, int from)
+{
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+        if (p < from)
+            continue;
+        const uint64_t t = cnt[p] & carry;
+        cnt[p] ^= carry;
+        carry = t;
+    }
+}
+
+template <int P>
+__global__ __launch_bounds__(kThreads) void k_head_planes(
+    const uint64_t *__restrict__ bits, int64_t W, int32_t g, int32_t S, int32_t rps,
+    int32_t c, uint64_t *__restrict__ planes, int64_t n_cb)
+{
+    const int lane = threadIdx.x % kWave;
+    const int64_t task = (int64_t)blockIdx.x * kWaves + threadIdx.x / kWave;
+    const int64_t cb = task % n_cb;
+    const int64_t rest = task / n_cb;
+    const int q = (int)(rest % S);
+    const int i = (int)(rest / S);
+    if (i >= c)
+        return;
+    const int64_t col = cb * kWave + lane;
+    const int64_t colc = min(col, W - 1);
+    const int64_t r0 = (int64_t)i * g + (int64_t)q * rps;
+    const int64_t r1 = min(r0 + rps, (int64_t)(i + 1) * g);
+
+    uint64_t cnt[P];
+#pragma unroll
+    for (int p = 0; p < P; ++p)
+        cnt[p] = 0;
+    const uint64_t *src = bits + colc;
+    int64_t r = r0;
+    if constexpr (P >= 4) {
+        for (; r + 8 <= r1; r += 8) {
+            uint64_t d[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                d[u] = src[(r + u) * W];
+            uint64_t twosA, twosB, foursA, foursB, eights;
+            csa(twosA, cnt[0], cnt[0], d[0], d[1]);
+            csa(twosB, cnt[0], cnt[0], d[2], d[3]);
+            csa(foursA, cnt[1], cnt[1], twosA, twosB);
+            csa(twosA, cnt[0], cnt[0], d[4], d[5]);
+            csa(twosB, cnt[0], cnt[0], d[6], d[7]);
+            csa(foursB, cnt[1], cnt[1], twosA, twosB);
+            csa(eights, cnt[2], cnt[2], foursA, foursB);
+            ripple_add<P>(cnt, eights, 3);
+        }
+    }
+    for (; r < r1; ++r)
+        ripple_add<P>(cnt, src[r * W], 0);
+
+    if (col < W) {
+        uint64_t *dst = planes + ((int64_t)(i * S + q) * P) * W + col;
+#pragma unroll
+        for (int p = 0; p < P; ++p)
+            dst[(int64_t)p * W] = cnt[p];
+    }
+}
+
+template <int P>
+__global__ __launch_bounds__(kThreads) void k_head_finish(
+    const uint64_t *__restrict__ planes, int64_t W, int64_t n, int32_t c, int32_t S,
+    int32_t *__restrict__ scores, int32_t *__restrict__ argmax)
+{
+    const int lane = threadIdx.x % kWave;
+    const int64_t col = (int64_t)blockIdx.x * kWaves +
+                        __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    if (col >= W)
+        return;
+    const int64_t s = col * kWave + lane;
+    int32_t best = -1, besti = 0;
+    for (int i = 0; i < c; ++i) {
+        int32_t cnt = 0;
+        for (int q = 0; q < S; ++q) {
+            const uint64_t *pl = planes + ((int64_t)(i * S + q) * P) * W + col;
+            int32_t part = 0;
+#pragma unroll
+            for (int p = 0; p < P; ++p)
+                part |= (int32_t)((pl[(int64_t)p * W] >> lane) & 1u) << p;
+            cnt += part;
+        }
+        if (scores && s < n)
+            scores[s * c + i] = cnt;
+        if (cnt > best) {
+            best = cnt;
+            besti = i;
+        }
+    }
+    if (argmax && s < n)
+        argmax[s] = besti;
+}
+
+template <int P>
+hipError_t launch_p(const uint64_t *bits, int32_t w, int64_t n, int32_t c,
+                    int32_t *scores, int32_t *argmax, uint64_t *planes,
+                    const HeadPlan &plan, hipStream_t stream)
+{
+    const int64_t W = (n + 63) / 64;
+    const int64_t n_cb = (W + kWave - 1) / kWave;
+    const int64_t tasks = n_cb * plan.splits * c;
+    const int64_t blocks1 = (tasks + kWaves - 1) / kWaves;
+    const int64_t blocks2 = (W + kWaves - 1) / kWaves;
+    if (blocks1 > 0x7fffffff || blocks2 > 0x7fffffff)
+        return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(k_head_planes<P>, dim3((unsigned)blocks1), dim3(kThreads), 0, stream,
+                       bits, W, w / c, plan.splits, plan.rows_per_split, c, planes, n_cb);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(k_head_finish<P>, dim3((unsigned)blocks2), dim3(kThreads), 0, stream,
+                       planes, W, n, c, plan.splits, scores, argmax);
+    return hipGetLastError();
+}
+
+int bit_length(int64_t v)
+{
+    int b = 0;
+    while (v > 0) {
+        ++b;
+        v >>= 1;
+    }
+    return b;
+}
+
+}  // namespace
+
+HeadPlan plan_head(int32_t w, int64_t n, int32_t c)
+{
+    HeadPlan p{};
+    const int64_t W = (n + 63) / 64;
+    const int64_t n_cb = (W + kWave - 1) / kWave;
+    const int32_t g = w / c;
+    if (W == 0 || g == 0) {          // nothing to count
+        p.splits = 1;
+        p.rows_per_split = g;
+        p.planes = bit_length(g);
+        p.ws_bytes = 0;
+        return p;
+    }
+    // enough (class, split, column block) waves to fill 256 CUs several
+    // times, but keep at least 32 rows per split
+    const int64_t want = (4096 + (int64_t)c * n_cb - 1) / ((int64_t)c * n_cb);
+    int64_t S = want < 1 ? 1 : want;
+    const int64_t max_s = (g + 31) / 32;
+    if (S > max_s)
+        S = max_s < 1 ? 1 : max_s;
+    int64_t rps = (g + S - 1) / S;
+    S = (g + rps - 1) / rps;
+    p.splits = (int32_t)S;
+    p.rows_per_split = (int32_t)rps;
+    p.planes = bit_length(rps);
+    p.ws_bytes = (size_t)c * S * p.planes * W * sizeof(uint64_t);
+    return p;
+}
+
+hipError_t launch_head(const uint64_t *bits, int32_t w, int64_t n, int32_t c,
+                       int32_t *scores, int32_t *argmax, void *ws, const HeadPlan &plan,
+                       hipStream_t stream)
+{
+    uint64_t *planes = static_cast<uint64_t *>(ws);
+    switch (plan.planes) {
+#define BL_CASE(P) \
+    case P: return launch_p<P>(bits, w, n, c, scores, argmax, planes, plan, stream);
+    BL_CASE(1) BL_CASE(2) BL_CASE(3) BL_CASE(4) BL_CASE(5) BL_CASE(6) BL_CASE(7) BL_CASE(8)
+    BL_CASE(9) BL_CASE(10) BL_CASE(11) BL_CASE(12) BL_CASE(13) BL_CASE(14) BL_CASE(15)
+    BL_CASE(16)
+#undef BL_CASE
+    default: return hipErrorInvalidValue;
+    }
+}
+
+static_assert(kMaxPlanes == 16, "plane count switch covers 1..16");
+
+}  // namespace bl

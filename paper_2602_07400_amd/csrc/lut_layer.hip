@@ -1,0 +1,232 @@
+// One LUT layer on packed bits, gfx950.
+//
+// Node j outputs, for every sample s, entry a of its truth table with
+// a = sum_i bit_s(in[conn[j][i]]) << i (Sec. 3 "Nodes are
+// parameterizations", "Connectivity is the main per-layer design choice";
+// App. C.1 "Bit-packed inference").  On packed words this is a Shannon
+// expansion: the 2^k table entries become all-0 / all-1 masks and k levels
+// of bitwise multiplexers, level i selected by input word i, fold them to
+// one word -- 2^k - 1 v_bfi_b32 per 32 samples, no per-sample work.
+//
+// Mapping (K = fan-in, LPN lanes per node, R words per lane):
+//  * a wave holds 64/LPN nodes; the LPN lanes of a node cover a window of
+//    LPN*R consecutive words (LPN*R*8 bytes of each input row);
+//  * each lane evaluates R words of its node, so the 2^K masks it derives
+//    from the node's table with v_bfe_i32 are reused 2R times (two 32-bit
+//    halves per word);
+//  * connection indices and tables of the block's NB nodes are staged in
+//    LDS with coalesced loads; lanes read their node's entries from LDS.
+//
+// Locality: input rows are gathered at random (fixed random routing has no
+// spatial locality), so the cache working set of one window is w_in rows x
+// window bytes.  Windows are dealt to the 8 XCDs round-robin and each XCD
+// walks all node blocks of one window before the next, so that slab stays in
+// that XCD's L2 while every node reading it runs.
+#include "bl_internal.h"
+
+namespace bl {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWavesPerBlock = kThreads / kWave;
+
+__device__ __forceinline__ uint32_t bfi(uint32_t sel, uint32_t one, uint32_t zero)
+{
+    return (sel & one) | (~sel & zero);
+}
+
+// Fold 2^K masks with K select words: level i pairs entries that differ in
+// address bit i, so the address bit order is slot 0 = least significant.
+template <int K>
+__device__ __forceinline__ uint32_t mux_tree(const uint32_t (&sel)[K],
+                                             const uint32_t (&m)[1 << K])
+{
+    uint32_t v[1 << (K - 1)];
+#pragma unroll
+    for (int a = 0; a < (1 << (K - 1)); ++a)
+        v[a] = bfi(sel[0], m[2 * a + 1], m[2 * a]);
+#pragma unroll
+    for (int i = 1; i < K; ++i) {
+#pragma unroll
+        for (int a = 0; a < (1 << (K - 1 - i)); ++a)
+            v[a] = bfi(sel[i], v[2 * a + 1], v[2 * a]);
+    }
+    return v[0];
+}
+
+// Access modes: whole windows with 16-byte or 8-byte accesses, or the one
+// ragged last window with per-word guards.  Separate instantiations keep the
+// guards out of the hot loop.
+enum Mode { kFull16 = 0, kFull8 = 1, kTail = 2 };
+
+template <int K, int LPN, int R, int NB, int MODE>
+__global__ __launch_bounds__(kThreads) void k_lut_layer(
+    const uint64_t *__restrict__ in, int64_t W, const int32_t *__restrict__ conn,
+    const uint64_t *__restrict__ tables, int32_t w_out, uint64_t *__restrict__ out,
+    int32_t n_nblk, int32_t n_win, int32_t win_base)
+{
+    constexpr int kGroups = kWave / LPN;                  // nodes per wave per pass
+    constexpr int kPassNodes = kGroups * kWavesPerBlock;  // nodes per block per pass
+    constexpr int kWin = LPN * R;                         // words per window
+    static_assert(NB % kPassNodes == 0, "node block must be whole passes");
+    static_assert(MODE != kFull16 || R % 2 == 0, "16-byte path needs an even R");
+
+    __shared__ int32_t s_conn[NB * K];
+    __shared__ uint64_t s_tab[NB];
+
+    const int bid = blockIdx.x;
+    const int loc = local_of(bid);
+    const int win = win_base + (loc / n_nblk) * kXcds + xcd_of(bid);
+    const int nblk = loc % n_nblk;
+    if (win >= n_win)
+        return;
+    const int node0 = nblk * NB;
+    const int nodes = min(NB, w_out - node0);
+
+    for (int q = threadIdx.x; q < NB * K; q += kThreads)
+        s_conn[q] = (q < nodes * K) ? conn[(int64_t)node0 * K + q] : 0;
+    for (int q = threadIdx.x; q < NB; q += kThreads)
+        s_tab[q] = (q < nodes) ? tables[node0 + q] : 0;
+    __syncthreads();
+
+    const int lane = threadIdx.x % kWave;
+    const int wave = threadIdx.x / kWave;
+    const int grp = lane / LPN;
+    const int sub = lane % LPN;
+    const int64_t wb0 = (int64_t)win * kWin + (int64_t)sub * R;
+
+#pragma unroll 1
+    for (int pass = 0; pass < NB / kPassNodes; ++pass) {
+        if (pass * kPassNodes >= nodes)
+            break;
+        const int jl = pass * kPassNodes + wave * kGroups + grp;
+
+        // gather the K input words of each of this lane's R words
+        uint32_t xv[2 * R][K];
+#pragma unroll
+        for (int i = 0; i < K; ++i) {
+            const uint64_t *src = in + (int64_t)s_conn[jl * K + i] * W + wb0;
+            if constexpr (MODE == kFull16) {
+#pragma unroll
+                for (int r = 0; r < R; r += 2) {
+                    const uint4 v = reinterpret_cast<const uint4 *>(src)[r / 2];
+                    xv[2 * r + 0][i] = v.x;
+                    xv[2 * r + 1][i] = v.y;
+                    xv[2 * r + 2][i] = v.z;
+                    xv[2 * r + 3][i] = v.w;
+                }
+            } else if constexpr (MODE == kFull8) {
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    const uint2 v = reinterpret_cast<const uint2 *>(src)[r];
+                    xv[2 * r + 0][i] = v.x;
+                    xv[2 * r + 1][i] = v.y;
+                }
+            } else {
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    // words past the end read the row's last word (discarded)
+                    const int64_t idx = min(wb0 + r, W - 1) - wb0;
+                    const uint2 v = reinterpret_cast<const uint2 *>(src)[idx];
+                    xv[2 * r + 0][i] = v.x;
+                    xv[2 * r + 1][i] = v.y;
+                }
+            }
+        }
+
+        // table entries -> full-word masks (one v_bfe_i32 each)
+        const uint64_t T = s_tab[jl];
+        const uint32_t t_lo = (uint32_t)T, t_hi = (uint32_t)(T >> 32);
+        uint32_t m[1 << K];
+#pragma unroll
+        for (int a = 0; a < (1 << K); ++a)
+            m[a] = 0u - (((a < 32 ? t_lo : t_hi) >> (a & 31)) & 1u);
+
+        uint32_t o[2 * R];
+#pragma unroll
+        for (int h = 0; h < 2 * R; ++h)
+            o[h] = mux_tree<K>(xv[h], m);
+
+        if (jl < nodes) {
+            uint64_t *dst = out + (int64_t)(node0 + jl) * W + wb0;
+            if constexpr (MODE == kFull16) {
+#pragma unroll
+                for (int r = 0; r < R; r += 2)
+                    reinterpret_cast<uint4 *>(dst)[r / 2] =
+                        make_uint4(o[2 * r], o[2 * r + 1], o[2 * r + 2], o[2 * r + 3]);
+            } else if constexpr (MODE == kFull8) {
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+                    reinterpret_cast<uint2 *>(dst)[r] = make_uint2(o[2 * r], o[2 * r + 1]);
+            } else {
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+                    if (wb0 + r < W)
+                        reinterpret_cast<uint2 *>(dst)[r] = make_uint2(o[2 * r], o[2 * r + 1]);
+            }
+        }
+    }
+}
+
+constexpr int kLPN = 4;
+constexpr int kR = 4;
+constexpr int kNB = 256;
+
+template <int K, int MODE>
+hipError_t launch_mode(const uint64_t *in, int64_t W, const int32_t *conn,
+                       const uint64_t *tables, int32_t w_out, uint64_t *out,
+                       int64_t win_base, int64_t n_win, hipStream_t stream)
+{
+    const int32_t n_nblk = (w_out + kNB - 1) / kNB;
+    const int64_t span = n_win - win_base;
+    const int64_t span_pad = (span + kXcds - 1) / kXcds * kXcds;
+    const int64_t blocks = span_pad * n_nblk;
+    if (blocks > 0x7fffffff || n_win > 0x7fffffff)
+        return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((k_lut_layer<K, kLPN, kR, kNB, MODE>), dim3((unsigned)blocks),
+                       dim3(kThreads), 0, stream, in, W, conn, tables, w_out, out, n_nblk,
+                       (int32_t)n_win, (int32_t)win_base);
+    return hipGetLastError();
+}
+
+template <int K>
+hipError_t launch_k(const uint64_t *in, int64_t W, const int32_t *conn,
+                    const uint64_t *tables, int32_t w_out, uint64_t *out,
+                    hipStream_t stream)
+{
+    constexpr int kWin = kLPN * kR;
+    const int64_t n_full = W / kWin;
+    hipError_t e = hipSuccess;
+    if (n_full > 0) {
+        const bool vec16 = (W % 2 == 0) && ((uintptr_t)in % 16 == 0) &&
+                           ((uintptr_t)out % 16 == 0);
+        e = vec16 ? launch_mode<K, kFull16>(in, W, conn, tables, w_out, out, 0, n_full, stream)
+                  : launch_mode<K, kFull8>(in, W, conn, tables, w_out, out, 0, n_full, stream);
+        if (e != hipSuccess)
+            return e;
+    }
+    if (W % kWin != 0)
+        e = launch_mode<K, kTail>(in, W, conn, tables, w_out, out, n_full, n_full + 1, stream);
+    return e;
+}
+
+}  // namespace
+
+hipError_t launch_lut_layer(const uint64_t *in, int32_t w_in, int64_t n_words,
+                            const int32_t *conn, const uint64_t *tables,
+                            int32_t w_out, int32_t k, uint64_t *out,
+                            hipStream_t stream)
+{
+    (void)w_in;
+    switch (k) {
+    case 1: return launch_k<1>(in, n_words, conn, tables, w_out, out, stream);
+    case 2: return launch_k<2>(in, n_words, conn, tables, w_out, out, stream);
+    case 3: return launch_k<3>(in, n_words, conn, tables, w_out, out, stream);
+    case 4: return launch_k<4>(in, n_words, conn, tables, w_out, out, stream);
+    case 5: return launch_k<5>(in, n_words, conn, tables, w_out, out, stream);
+    case 6: return launch_k<6>(in, n_words, conn, tables, w_out, out, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace bl

@@ -28,6 +28,8 @@ from __future__ import annotations
 from dataclasses import dataclass, field
 from typing import List, Optional, Tuple
 
+import concurrent.futures as cf
+import os
 import zlib
 
 import numpy as np
@@ -122,8 +124,7 @@ class Workload:
 
 def _streams(seed: int, name: str, n_layers: int):
     root = np.random.SeedSequence([seed, zlib.crc32(name.encode())])
-    kids = root.spawn(_S_LAYERS + 2 * n_layers)
-    return [np.random.default_rng(s) for s in kids]
+    return root.spawn(_S_LAYERS + 2 * n_layers)
 
 
 def uniform_thresholds(d: int, b: int) -> np.ndarray:
@@ -144,22 +145,47 @@ def _quantile_thresholds(train: np.ndarray, b: int, channels: int) -> np.ndarray
     return th
 
 
-def _pixels(cfg: Config, n: int, rng: np.random.Generator, proto_rng: np.random.Generator):
+_CHUNK = 1 << 14           # pixel rows per independently seeded chunk
+
+
+def _pixel_chunks(n: int, d: int, ss: np.random.SeedSequence, fill) -> np.ndarray:
+    """Fill x [n][d] chunk by chunk; chunk i draws from child i of ``ss``, so
+    the bytes do not depend on how many threads run the chunks."""
+    x = np.empty((n, d), dtype=np.uint8)
+    n_chunks = (n + _CHUNK - 1) // _CHUNK
+    kids = ss.spawn(n_chunks)
+
+    def run(i):
+        s0, s1 = i * _CHUNK, min(n, (i + 1) * _CHUNK)
+        fill(np.random.default_rng(kids[i]), x[s0:s1], s0, s1)
+
+    workers = max(1, min(16, os.cpu_count() or 1, n_chunks))
+    if workers == 1:
+        for i in range(n_chunks):
+            run(i)
+    else:
+        with cf.ThreadPoolExecutor(workers) as ex:
+            list(ex.map(run, range(n_chunks)))
+    return x
+
+
+def _pixels(cfg: Config, n: int, ss: np.random.SeedSequence, proto_rng: np.random.Generator):
     if cfg.pixels == "uniform":
-        return rng.integers(0, 256, size=(n, cfg.d), dtype=np.uint8), None
+        def fill(rng, out, s0, s1):
+            out[...] = np.frombuffer(rng.bytes(out.size), dtype=np.uint8).reshape(out.shape)
+        return _pixel_chunks(n, cfg.d, ss, fill), None
     # Gaussian mixture of class prototypes, clipped to the pixel range
     protos = proto_rng.uniform(0.0, 255.0, size=(cfg.n_classes, cfg.d)).astype(np.float32)
     labels = proto_rng.integers(0, cfg.n_classes, size=n).astype(np.int32)
-    x = np.empty((n, cfg.d), dtype=np.uint8)
-    chunk = 1 << 15
-    for s0 in range(0, n, chunk):
-        s1 = min(n, s0 + chunk)
-        z = rng.standard_normal(size=(s1 - s0, cfg.d), dtype=np.float32)
-        v = protos[labels[s0:s1]] + np.float32(_GM_SIGMA) * z
-        np.rint(v, out=v)
-        np.clip(v, 0.0, 255.0, out=v)
-        x[s0:s1] = v.astype(np.uint8)
-    return x, labels
+
+    def fill(rng, out, s0, s1):
+        z = rng.standard_normal(size=out.shape, dtype=np.float32)
+        z *= np.float32(_GM_SIGMA)
+        z += protos[labels[s0:s1]]
+        np.rint(z, out=z)
+        np.clip(z, 0.0, 255.0, out=z)
+        out[...] = z.astype(np.uint8)
+    return _pixel_chunks(n, cfg.d, ss, fill), labels
 
 
 def draw_connectivity(rng: np.random.Generator, w: int, k: int, w_in: int) -> np.ndarray:
@@ -193,14 +219,15 @@ def make_workload(name_or_cfg, seed: int = 0, n: Optional[int] = None) -> Worklo
     cfg = CONFIGS[name_or_cfg] if isinstance(name_or_cfg, str) else name_or_cfg
     n = cfg.n if n is None else int(n)
     L = len(cfg.widths)
-    rngs = _streams(seed, cfg.seed_key, L)
-    x, labels = _pixels(cfg, n, rngs[_S_PIXELS], rngs[_S_PROTO])
+    ss = _streams(seed, cfg.seed_key, L)
+    rngs = [np.random.default_rng(q) for q in ss]
+    x, labels = _pixels(cfg, n, ss[_S_PIXELS], rngs[_S_PROTO])
     if cfg.thresholds == "fixed128":
         th = np.full((cfg.d, cfg.b), 128, dtype=np.uint8)
     elif cfg.thresholds == "uniform":
         th = uniform_thresholds(cfg.d, cfg.b)
     elif cfg.thresholds == "quantile":
-        train, _ = _pixels(cfg, _TRAIN_SPLIT, rngs[_S_TRAIN], np.random.default_rng(seed))
+        train, _ = _pixels(cfg, _TRAIN_SPLIT, ss[_S_TRAIN], np.random.default_rng(seed))
         th = _quantile_thresholds(train, cfg.b, cfg.channels)
     else:
         raise ValueError(cfg.thresholds)

@@ -1,0 +1,152 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/bitlogic.h declares, and rejects bad arguments on the host before any
+HIP call (so fake, never-dereferenced pointers are safe here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2602_07400_amd import bitlogic as bl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bitlogic.h")
+
+# a non-NULL address that is never dereferenced (every call below fails its
+# host-side checks first)
+FAKE = 0x10000
+OK, ENULL, ESHAPE, EALIGN, EUNSUP, EHIP, EWS = range(7)
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(bitlogic_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return bl.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared()
+    assert {"bitlogic_encode", "bitlogic_lut_layer", "bitlogic_groupsum_head",
+            "bitlogic_forward"} <= set(names)
+    raw = ctypes.CDLL(bl.library_path())
+    for name in names:
+        assert hasattr(raw, name), name
+
+
+def test_status_strings(lib):
+    for s in range(7):
+        assert bl.bitlogic_status_string(s) and bl.bitlogic_status_string(s) != "unknown status"
+    assert bl.bitlogic_status_string(99) == "unknown status"
+    assert bl.bitlogic_version() >= 100
+
+
+def _err(lib):
+    return lib.bitlogic_last_error().decode()
+
+
+def test_encode_validation(lib):
+    assert lib.bitlogic_encode(None, 64, 4, FAKE, 1, FAKE, None) == ENULL
+    assert lib.bitlogic_encode(FAKE, -1, 4, FAKE, 1, FAKE, None) == ESHAPE
+    assert lib.bitlogic_encode(FAKE, 64, 0, FAKE, 1, FAKE, None) == ESHAPE
+    assert lib.bitlogic_encode(FAKE, 64, 4, FAKE, 0, FAKE, None) == ESHAPE
+    assert lib.bitlogic_encode(FAKE, 64, 4, FAKE, 65, FAKE, None) == ESHAPE
+    assert "b <= 64" in _err(lib)
+    assert lib.bitlogic_encode(FAKE, 64, 4, FAKE, 1, FAKE + 4, None) == EALIGN
+    # n = 0 is valid and enqueues nothing
+    assert lib.bitlogic_encode(FAKE, 0, 4, FAKE, 1, FAKE, None) == OK
+    assert _err(lib) == ""
+
+
+@pytest.mark.parametrize("k", [0, 7, -1])
+def test_layer_rejects_fan_in(lib, k):
+    assert lib.bitlogic_lut_layer(FAKE, 10, 4, FAKE, FAKE, 10, k, FAKE, None) == EUNSUP
+
+
+def test_layer_validation(lib):
+    assert lib.bitlogic_lut_layer(None, 10, 4, FAKE, FAKE, 10, 6, FAKE, None) == ENULL
+    assert lib.bitlogic_lut_layer(FAKE, 10, 4, None, FAKE, 10, 6, FAKE, None) == ENULL
+    assert lib.bitlogic_lut_layer(FAKE, 0, 4, FAKE, FAKE, 10, 6, FAKE, None) == ESHAPE
+    assert lib.bitlogic_lut_layer(FAKE, 10, -4, FAKE, FAKE, 10, 6, FAKE, None) == ESHAPE
+    assert lib.bitlogic_lut_layer(FAKE, 10, 4, FAKE, FAKE, 0, 6, FAKE, None) == ESHAPE
+    assert lib.bitlogic_lut_layer(FAKE + 2, 10, 4, FAKE, FAKE, 10, 6, FAKE, None) == EALIGN
+    assert lib.bitlogic_lut_layer(FAKE, 10, 4, FAKE + 1, FAKE, 10, 6, FAKE, None) == EALIGN
+    assert lib.bitlogic_lut_layer(FAKE, 10, 0, FAKE, FAKE, 10, 6, FAKE, None) == OK
+
+
+def test_head_validation(lib):
+    ws = lib.bitlogic_groupsum_head_workspace_bytes(100, 4096, 10)
+    assert ws > 0 and ws % 8 == 0
+    assert lib.bitlogic_groupsum_head_workspace_bytes(101, 4096, 10) == 0
+    assert lib.bitlogic_groupsum_head(None, 100, 4096, 10, FAKE, FAKE, FAKE, ws, None) == ENULL
+    assert lib.bitlogic_groupsum_head(FAKE, 100, 4096, 10, None, None, FAKE, ws, None) == ENULL
+    assert lib.bitlogic_groupsum_head(FAKE, 101, 4096, 10, FAKE, FAKE, FAKE, ws, None) == ESHAPE
+    assert lib.bitlogic_groupsum_head(FAKE, 100, 4096, 0, FAKE, FAKE, FAKE, ws, None) == ESHAPE
+    assert lib.bitlogic_groupsum_head(FAKE, 70000 * 2, 64, 2, FAKE, FAKE, FAKE, 1 << 30,
+                                      None) == ESHAPE
+    assert lib.bitlogic_groupsum_head(FAKE, 100, 4096, 10, FAKE, FAKE, FAKE, ws - 1,
+                                      None) == EWS
+    assert lib.bitlogic_groupsum_head(FAKE, 100, 4096, 10, FAKE, FAKE, None, ws, None) == ENULL
+    assert lib.bitlogic_groupsum_head(FAKE, 100, 4096, 10, FAKE, FAKE, FAKE + 8, ws,
+                                      None) == EALIGN
+    assert lib.bitlogic_groupsum_head(FAKE, 100, 0, 10, FAKE, FAKE, FAKE, ws, None) == OK
+
+
+def _layers(specs):
+    arr = (bl._Layer * len(specs))()
+    for i, (w, k) in enumerate(specs):
+        arr[i].conn, arr[i].tables, arr[i].w_out, arr[i].k = FAKE, FAKE, w, k
+    return ctypes.cast(arr, ctypes.c_void_p), arr
+
+
+def test_forward_workspace_formula(lib):
+    p, keep = _layers([(1000, 6), (1000, 6)])
+    n, d, b, c = 4096, 784, 1, 10
+    need = lib.bitlogic_forward_workspace_bytes(n, d, b, p, 2, c)
+    W = 64
+    rnd = lambda v: (v + 255) // 256 * 256
+    head = lib.bitlogic_groupsum_head_workspace_bytes(1000, n, c)
+    assert need == rnd(d * b * W * 8) + 2 * rnd(1000 * W * 8) + rnd(head)
+    # bad shapes give 0
+    assert lib.bitlogic_forward_workspace_bytes(n, d, b, p, 2, 7) == 0
+    assert lib.bitlogic_forward_workspace_bytes(n, d, b, p, 0, c) == 0
+    p7, keep7 = _layers([(1000, 7)])
+    assert lib.bitlogic_forward_workspace_bytes(n, d, b, p7, 1, c) == 0
+
+
+def test_forward_validation(lib):
+    p, keep = _layers([(1000, 6), (1000, 6)])
+    need = lib.bitlogic_forward_workspace_bytes(4096, 784, 1, p, 2, 10)
+    args = lambda **o: [o.get("x", FAKE), o.get("n", 4096), 784, FAKE, 1, o.get("layers", p),
+                        o.get("L", 2), o.get("c", 10), FAKE, FAKE, o.get("ws", FAKE * 16),
+                        o.get("wsb", need), None]
+    assert lib.bitlogic_forward(*args(x=None)) == ENULL
+    assert lib.bitlogic_forward(*args(layers=None)) == ENULL
+    assert lib.bitlogic_forward(*args(L=0)) == ESHAPE
+    assert lib.bitlogic_forward(*args(c=7)) == ESHAPE
+    assert lib.bitlogic_forward(*args(ws=None)) == ENULL
+    assert lib.bitlogic_forward(*args(wsb=need - 1)) == EWS
+    assert lib.bitlogic_forward(*args(ws=FAKE * 16 + 64)) == EALIGN
+    assert lib.bitlogic_forward(*args(n=0)) == OK
+    pk, keepk = _layers([(1000, 6), (1000, 0)])
+    assert lib.bitlogic_forward(*args(layers=pk)) == EUNSUP
+
+
+def test_python_binding_refuses_cpu_tensors():
+    import torch
+    x = torch.zeros((64, 4), dtype=torch.uint8)
+    th = torch.zeros((4, 1), dtype=torch.uint8)
+    with pytest.raises(ValueError, match="GPU"):
+        bl.bitlogic_encode(x, th, bits_out=torch.zeros((4, 1), dtype=torch.int64))
+
+
+def test_model_checks_connection_range():
+    import numpy as np
+    th = np.zeros((4, 2), np.uint8)
+    conn = np.array([[0, 8]], np.int32)          # 8 >= w_in = 8
+    with pytest.raises(ValueError, match="outside"):
+        bl.BitlogicModel.from_numpy(th, [(conn, np.zeros(1, np.uint64))], 1, device="cpu")

@@ -1,0 +1,301 @@
+"""Bit-exact parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Per-kernel cases cover every fan-in, ragged word counts (the tail window),
+odd word counts and 8-byte-only alignment (the 8-byte access path), node
+counts that are not whole node blocks, repeated connection indices, junk
+table bits above 2^k, threshold edge values, unaligned pixel rows, and head
+groups from 1 node to thousands (split counters).  Whole-network cases run
+every configuration at a reduced batch (several windows plus a ragged tail)
+and at its full batch, where the oracle checks a sample of rows.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2602_07400_amd import bitlogic as bl
+from paper_2602_07400_amd.workloads import CONFIG_ORDER, CONFIGS, make_workload
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0")
+
+
+def unpack(bits: torch.Tensor, n: int) -> np.ndarray:
+    """int64 [rows][W] packed bits -> uint8 [n][rows] (bit s%64 of word s/64)."""
+    b = bits.cpu().numpy().view(np.uint8)                  # [rows][W*8], little-endian
+    v = np.unpackbits(b, axis=1, bitorder="little")        # [rows][W*64]
+    return np.ascontiguousarray(v[:, :n].T)
+
+
+def pack(v: np.ndarray) -> torch.Tensor:
+    """uint8 [n][rows] (0/1) -> int64 [rows][ceil(n/64)] on the GPU."""
+    n, rows = v.shape
+    W = (n + 63) // 64
+    buf = np.zeros((rows, W * 8), dtype=np.uint8)
+    p = np.packbits(v.T, axis=1, bitorder="little")
+    buf[:, :p.shape[1]] = p
+    return torch.from_numpy(buf.view(np.int64).copy()).to(DEV)
+
+
+def to_dev(a: np.ndarray) -> torch.Tensor:
+    if a.dtype == np.uint64:
+        a = a.view(np.int64)
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def _report(name, got, ref):
+    bad = np.argwhere(got != ref)
+    return f"{name}: {len(bad)} mismatches, first {bad[:5].tolist()}"
+
+
+# ------------------------------------------------------------------ encoder
+
+ENC_CASES = [
+    # n, d, b, threshold kind
+    (64, 4, 1, "random"),
+    (64 * 3 + 5, 37, 3, "random"),          # ragged samples, d % 4 != 0 (byte path)
+    (4096 + 17, 784, 1, "128"),
+    (1000, 100, 7, "edges"),                 # 0 / 255 / duplicates / unsorted
+    (2048, 3072, 3, "random"),
+    (777, 33, 64, "random"),                 # b at its maximum
+    (64 * 16 * 2, 64, 8, "zero"),            # the quantile collapse: all thresholds 0
+]
+
+
+@pytest.mark.parametrize("n,d,b,kind", ENC_CASES)
+def test_encode_parity(n, d, b, kind):
+    rng = np.random.default_rng(n * 131 + d * 7 + b)
+    x = rng.integers(0, 256, size=(n, d), dtype=np.uint8)
+    x[: min(n, 5)] = 0
+    x[min(n, 5): min(n, 9)] = 255
+    if kind == "128":
+        th = np.full((d, b), 128, np.uint8)
+    elif kind == "edges":
+        th = rng.choice(np.array([0, 255, 128, 128, 1, 254], np.uint8), size=(d, b))
+    elif kind == "zero":
+        th = np.zeros((d, b), np.uint8)
+    else:
+        th = rng.integers(0, 256, size=(d, b), dtype=np.uint8)
+    bits = bl.bitlogic_encode(to_dev(x), to_dev(th))
+    torch.cuda.synchronize()
+    got = unpack(bits, bits.shape[1] * 64)
+    ref = oracle.encode(x, th)
+    assert np.array_equal(got[:n], ref), _report("encode", got[:n], ref)
+    assert not got[n:].any(), "padding bits must be 0"
+
+
+def test_encode_unaligned_rows():
+    """Pixels whose base address is not 4-byte aligned take the byte path."""
+    rng = np.random.default_rng(5)
+    n, d, b = 300, 40, 3
+    big = rng.integers(0, 256, size=(n + 1) * d + 1, dtype=np.uint8)
+    xt = to_dev(big)[1:1 + n * d].view(n, d)
+    assert xt.data_ptr() % 4 != 0
+    th = rng.integers(0, 256, size=(d, b), dtype=np.uint8)
+    bits = bl.bitlogic_encode(xt, to_dev(th))
+    ref = oracle.encode(big[1:1 + n * d].reshape(n, d), th)
+    assert np.array_equal(unpack(bits, n), ref)
+
+
+# ---------------------------------------------------------------- LUT layer
+
+LAYER_CASES = [
+    # n_words, w_in, w_out, k, repeats
+    (1, 6, 1, 6, False),
+    (4, 7, 5, 3, True),              # tail window only
+    (16, 100, 256, 6, False),        # exactly one window, one node block
+    (16 * 3 + 5, 1000, 300, 6, False),   # full windows + tail; partial node block
+    (33, 64, 70, 4, True),           # odd word count: 8-byte path
+    (64, 300, 513, 5, False),
+    (40, 50, 64, 1, True),
+    (40, 50, 64, 2, False),
+    (128, 21504, 1000, 6, False),    # C4-shaped input width
+]
+
+
+@pytest.mark.parametrize("n_words,w_in,w_out,k,repeats", LAYER_CASES)
+def test_lut_layer_parity(n_words, w_in, w_out, k, repeats):
+    rng = np.random.default_rng(n_words * 1009 + w_in + k)
+    n = n_words * 64
+    v = rng.integers(0, 2, size=(n, w_in), dtype=np.uint8)
+    if repeats:
+        conn = rng.integers(0, w_in, size=(w_out, k)).astype(np.int32)
+        conn[: w_out // 2, :min(k, 2)] = conn[: w_out // 2, :1]
+    else:
+        conn = np.stack([rng.choice(w_in, size=k, replace=False) for _ in range(w_out)]
+                        ).astype(np.int32)
+    tables = rng.integers(0, np.iinfo(np.uint64).max, size=w_out, dtype=np.uint64,
+                          endpoint=True)   # junk above 2^k for k < 6 must be ignored
+    out = bl.bitlogic_lut_layer(pack(v), to_dev(conn), to_dev(tables))
+    ref = oracle.lut_layer(v, conn, tables)
+    got = unpack(out, n)
+    assert np.array_equal(got, ref), _report("lut_layer", got, ref)
+
+
+def test_lut_layer_8byte_alignment_path():
+    """Buffers that are 8- but not 16-byte aligned use 8-byte accesses."""
+    rng = np.random.default_rng(17)
+    n_words, w_in, w_out, k = 48, 90, 130, 6
+    n = n_words * 64
+    v = rng.integers(0, 2, size=(n, w_in), dtype=np.uint8)
+    packed = pack(v)
+    big_in = torch.zeros(w_in * n_words + 1, dtype=torch.int64, device=DEV)
+    big_in[1:] = packed.reshape(-1)
+    bits_in = big_in[1:].view(w_in, n_words)
+    big_out = torch.zeros(w_out * n_words + 1, dtype=torch.int64, device=DEV)
+    bits_out = big_out[1:].view(w_out, n_words)
+    assert bits_in.data_ptr() % 16 == 8
+    conn = np.stack([rng.choice(w_in, size=k, replace=False) for _ in range(w_out)]).astype(np.int32)
+    tables = rng.integers(0, 1 << 63, size=w_out).astype(np.uint64)
+    bl.bitlogic_lut_layer(bits_in, to_dev(conn), to_dev(tables), bits_out=bits_out)
+    assert np.array_equal(unpack(bits_out, n), oracle.lut_layer(v, conn, tables))
+    assert big_out[0].item() == 0
+
+
+def test_lut_layer_projection_tables():
+    """Closed-form projection tables reproduce their input wires on the GPU."""
+    rng = np.random.default_rng(3)
+    n_words, w_in = 20, 64
+    v = rng.integers(0, 2, size=(n_words * 64, w_in), dtype=np.uint8)
+    bits_in = pack(v)
+    proj = [0xAAAAAAAAAAAAAAAA, 0xCCCCCCCCCCCCCCCC, 0xF0F0F0F0F0F0F0F0,
+            0xFF00FF00FF00FF00, 0xFFFF0000FFFF0000, 0xFFFFFFFF00000000]
+    conn = np.stack([rng.choice(w_in, size=6, replace=False) for _ in range(6)]).astype(np.int32)
+    tables = np.array(proj, dtype=np.uint64)
+    out = bl.bitlogic_lut_layer(bits_in, to_dev(conn), to_dev(tables))
+    got = out.cpu().numpy()
+    ref_in = bits_in.cpu().numpy()
+    for i in range(6):
+        assert np.array_equal(got[i], ref_in[conn[i, i]])
+
+
+# --------------------------------------------------------------------- head
+
+HEAD_CASES = [
+    # n, c, g, density
+    (64, 1, 1, 0.5),
+    (100, 3, 5, 0.5),          # g < 8: ripple-only counter
+    (4096 + 33, 10, 100, 0.5),
+    (2048, 100, 64, 0.5),
+    (700, 10, 6400, 0.5),      # long groups, split counters
+    (1000, 7, 1000, 0.0),      # all zero: every class ties at 0 -> argmax 0
+    (1000, 7, 1000, 1.0),      # all one: ties at g -> argmax 0
+    (1500, 10, 3200, 0.5),
+    (128, 4, 65535, 0.02),      # the largest group size
+]
+
+
+@pytest.mark.parametrize("n,c,g,density", HEAD_CASES)
+def test_head_parity(n, c, g, density):
+    rng = np.random.default_rng(n + c * 31 + g)
+    w = c * g
+    v = (rng.random((n, w), dtype=np.float32) < density).astype(np.uint8)
+    bits = pack(v)
+    scores, argmax = bl.bitlogic_groupsum_head(bits, n, c)
+    ref_s, ref_p = oracle.groupsum(v, c)
+    got_s, got_p = scores.cpu().numpy(), argmax.cpu().numpy()
+    assert np.array_equal(got_s, ref_s), _report("scores", got_s, ref_s)
+    assert np.array_equal(got_p, ref_p), _report("argmax", got_p, ref_p)
+
+
+def test_head_argmax_only_and_padding_ignored():
+    rng = np.random.default_rng(8)
+    n, c, g = 130, 5, 40
+    v = rng.integers(0, 2, size=(n, c * g), dtype=np.uint8)
+    bits = pack(v)
+    # set every padding bit: the head must ignore samples >= n
+    W = bits.shape[1]
+    pad = np.zeros((W * 64, c * g), np.uint8)
+    pad[:n] = v
+    pad[n:] = 1
+    bits = pack(pad)
+    _, argmax = bl.bitlogic_groupsum_head(bits, n, c, want_scores=False)
+    assert np.array_equal(argmax.cpu().numpy(), oracle.groupsum(v, c)[1])
+
+
+# ------------------------------------------------------------ whole network
+
+def _check_forward(wl, idx=None):
+    model = bl.BitlogicModel.from_numpy(wl.thresholds, wl.layers, wl.n_classes, device=DEV)
+    x = torch.from_numpy(wl.x).to(DEV)
+    scores, argmax = model.forward(x)
+    torch.cuda.synchronize()
+    got_s, got_p = scores.cpu().numpy(), argmax.cpu().numpy()
+    if idx is None:
+        ref_s, ref_p = oracle.forward(wl.x, wl.thresholds, wl.layers, wl.n_classes)
+        sel = slice(None)
+    else:
+        ref_s, ref_p = oracle.forward(wl.x[idx], wl.thresholds, wl.layers, wl.n_classes)
+        sel = idx
+    assert np.array_equal(got_s[sel], ref_s), _report("scores", got_s[sel], ref_s)
+    assert np.array_equal(got_p[sel], ref_p), _report("argmax", got_p[sel], ref_p)
+    return got_s, got_p
+
+
+@pytest.mark.parametrize("name", CONFIG_ORDER)
+def test_forward_reduced_batch(name):
+    # several 16-word windows plus a ragged last word
+    wl = make_workload(name, seed=0, n=64 * 16 * 2 + 64 * 3 + 17)
+    _check_forward(wl)
+
+
+@pytest.mark.parametrize("name", CONFIG_ORDER)
+def test_forward_full_batch_sampled(name):
+    cfg = CONFIGS[name]
+    wl = make_workload(name, seed=0)
+    rng = np.random.default_rng(99)
+    if cfg.n <= 4096:
+        idx = None                      # the oracle checks every sample
+    else:
+        idx = np.unique(np.concatenate([np.arange(64), np.arange(cfg.n - 64, cfg.n),
+                                        rng.choice(cfg.n, size=1024, replace=False)]))
+    print(f"[full] {name}: n={cfg.n} sampled={None if idx is None else idx.size}", flush=True)
+    _check_forward(wl, idx)
+
+
+def test_forward_matches_staged_calls_and_is_deterministic():
+    wl = make_workload("c3_cifar10", seed=3, n=5000)
+    model = bl.BitlogicModel.from_numpy(wl.thresholds, wl.layers, wl.n_classes, device=DEV)
+    x = torch.from_numpy(wl.x).to(DEV)
+    s1, p1 = model.forward(x)
+    s2, p2 = model.forward(x)
+    bits = bl.bitlogic_encode(x, model.thresholds)
+    for conn, tab in model.layers:
+        bits = bl.bitlogic_lut_layer(bits, conn, tab)
+    s3, p3 = bl.bitlogic_groupsum_head(bits, wl.n, wl.n_classes)
+    assert torch.equal(s1, s2) and torch.equal(p1, p2)
+    assert torch.equal(s1, s3) and torch.equal(p1, p3)
+
+
+def test_forward_single_layer_and_deep_stack():
+    rng = np.random.default_rng(12)
+    n, d, b = 1500, 50, 2
+    x = rng.integers(0, 256, size=(n, d), dtype=np.uint8)
+    th = rng.integers(0, 256, size=(d, b), dtype=np.uint8)
+    widths, ks = [120, 90, 60, 40, 30], [6, 5, 4, 3, 2]
+    layers, w_in = [], d * b
+    for w, k in zip(widths, ks):
+        conn = np.stack([rng.choice(w_in, size=k, replace=False) for _ in range(w)]).astype(np.int32)
+        layers.append((conn, rng.integers(0, 1 << 63, size=w).astype(np.uint64)))
+        w_in = w
+    for L, c in ((1, 6), (5, 3)):
+        m = bl.BitlogicModel.from_numpy(th, layers[:L], c, device=DEV)
+        s, p = m.forward(torch.from_numpy(x).to(DEV))
+        rs, rp = oracle.forward(x, th, layers[:L], c)
+        assert np.array_equal(s.cpu().numpy(), rs) and np.array_equal(p.cpu().numpy(), rp)
+
+
+def test_forward_on_side_stream():
+    wl = make_workload("c1_mnist_tiny", seed=4, n=1000)
+    model = bl.BitlogicModel.from_numpy(wl.thresholds, wl.layers, wl.n_classes, device=DEV)
+    x = torch.from_numpy(wl.x).to(DEV)
+    st = torch.cuda.Stream()
+    st.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(st):
+        s, p = model.forward(x)
+    st.synchronize()
+    rs, rp = oracle.forward(wl.x, wl.thresholds, wl.layers, wl.n_classes)
+    assert np.array_equal(s.cpu().numpy(), rs) and np.array_equal(p.cpu().numpy(), rp)
