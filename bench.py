@@ -48,6 +48,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--stage-steps", type=int, default=None,
                     help="steps of the per-kernel (staged) timing loop; default = --steps")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="also run a plain device copy of this many MiB (reference kernel "
+                         "for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     return ap.parse_args()
 
 
@@ -116,6 +119,17 @@ def main():
     def step():
         bl.bitlogic_forward(x, model.thresholds, model.layers, model.n_classes,
                             scores=scores, argmax=argmax, workspace=ws, stream=stream)
+
+    if args.calibrate_copy_mib:
+        nbytes = args.calibrate_copy_mib << 20
+        src = torch.ones(nbytes // 8, dtype=torch.int64, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        print(f"[bench] copy calibration: 3 x {nbytes} bytes read + written", file=sys.stderr,
+              flush=True)
 
     # ---- warmup, then exactly K timed steps
     for _ in range(args.warmup):
@@ -206,7 +220,7 @@ def main():
     if not args.no_cpu_baseline:
         import oracle
         threads = oracle.max_threads()
-        probe = min(n, 64)
+        probe = min(n, 2048)
         t0 = time.perf_counter()
         oracle.forward(wl.x[:probe], wl.thresholds, wl.layers, wl.n_classes)
         per = (time.perf_counter() - t0) / probe
