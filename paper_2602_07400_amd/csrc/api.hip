@@ -93,8 +93,12 @@ int check_head(const uint64_t *bits, int32_t w, int64_t n, int32_t c, const int3
     return BITLOGIC_OK;
 }
 
+// bitlogic_forward keeps its encoded and intermediate bit tensors in the slab
+// layout [Wp / 4][rows][4] (Wp = W rounded up to whole 4-word slabs), which
+// gives the LUT-layer gathers a small per-XCD working set (see lut_layer.hip).
 struct ForwardPlan {
     int64_t W;
+    int64_t n_slabs;
     int32_t widest;
     size_t off_enc, off_a, off_b, off_head, total;
     bl::HeadPlan head;
@@ -134,9 +138,11 @@ int plan_forward(int64_t n, int32_t d, int32_t b, const bitlogic_layer *layers, 
     if (w_last / c > 65535)
         return fail(BITLOGIC_ERR_SHAPE, "forward: group size %d > 65535", w_last / c);
     fp->W = words_of(n);
+    fp->n_slabs = (fp->W + bl::kSlabWords - 1) / bl::kSlabWords;
     fp->widest = widest;
-    const size_t enc = (size_t)d * b * fp->W * sizeof(uint64_t);
-    const size_t act = (size_t)widest * fp->W * sizeof(uint64_t);
+    const int64_t Wp = fp->n_slabs * bl::kSlabWords;
+    const size_t enc = (size_t)d * b * Wp * sizeof(uint64_t);
+    const size_t act = (size_t)widest * Wp * sizeof(uint64_t);
     fp->head = bl::plan_head(w_last, n, c);
     fp->off_enc = 0;
     fp->off_a = round_up(enc);
@@ -160,7 +166,7 @@ int bitlogic_encode(const uint8_t *x, int64_t n_samples, int32_t n_features,
     if (n_samples == 0)
         return ok();
     return hip_status(bl::launch_encode(x, n_samples, n_features, thresholds, n_thresholds,
-                                        bits_out, (hipStream_t)stream),
+                                        bits_out, bl::kLayoutRowMajor, (hipStream_t)stream),
                       "encode launch");
 }
 
@@ -204,7 +210,7 @@ int bitlogic_groupsum_head(const uint64_t *bits, int32_t w, int64_t n_samples,
     if (n_samples == 0)
         return ok();
     return hip_status(bl::launch_head(bits, w, n_samples, n_classes, scores, argmax, workspace,
-                                      plan, (hipStream_t)stream),
+                                      plan, bl::kLayoutRowMajor, (hipStream_t)stream),
                       "head launch");
 }
 
@@ -248,22 +254,23 @@ int bitlogic_forward(const uint8_t *x, int64_t n_samples, int32_t n_features,
     uint64_t *enc = reinterpret_cast<uint64_t *>(ws + fp.off_enc);
     uint64_t *act[2] = {reinterpret_cast<uint64_t *>(ws + fp.off_a),
                         reinterpret_cast<uint64_t *>(ws + fp.off_b)};
-    hipError_t e = bl::launch_encode(x, n_samples, n_features, thresholds, n_thresholds, enc, s);
+    hipError_t e = bl::launch_encode(x, n_samples, n_features, thresholds, n_thresholds, enc,
+                                     bl::kLayoutSlab, s);
     if (e != hipSuccess)
         return hip_status(e, "forward: encode launch");
     const uint64_t *cur = enc;
     int32_t w_in = n_features * n_thresholds;
     for (int32_t l = 0; l < n_layers; ++l) {
         uint64_t *dst = act[l & 1];
-        e = bl::launch_lut_layer(cur, w_in, fp.W, layers[l].conn, layers[l].tables,
-                                 layers[l].w_out, layers[l].k, dst, s);
+        e = bl::launch_lut_layer_slab(cur, w_in, fp.n_slabs, layers[l].conn, layers[l].tables,
+                                      layers[l].w_out, layers[l].k, dst, s);
         if (e != hipSuccess)
             return fail(BITLOGIC_ERR_HIP, "forward: layer %d launch: %s", l, hipGetErrorString(e));
         cur = dst;
         w_in = layers[l].w_out;
     }
     e = bl::launch_head(cur, w_in, n_samples, n_classes, scores, argmax, ws + fp.off_head,
-                        fp.head, s);
+                        fp.head, bl::kLayoutSlab, s);
     return hip_status(e, "forward: head launch");
 }
 

@@ -10,6 +10,21 @@ namespace bl {
 
 constexpr int kWave = 64;       // CDNA wavefront width
 constexpr int kXcds = 8;        // MI355X: 8 accelerator dies, each with its own L2
+constexpr int kSlabWords = 4;   // words per row segment in the slab layout (256 samples)
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Layouts of packed bit tensors: row-major [rows][W] (the public calls) or
+// slabs (bitlogic_forward's intermediates in its workspace).
+constexpr int kLayoutRowMajor = 0;
+constexpr int kLayoutSlab = 1;
+
+// Word (row r, column wb) of a packed tensor with `rows` rows in the slab
+// layout of bitlogic_forward's intermediates, [W / kSlabWords][rows][kSlabWords].
+__host__ __device__ inline int64_t slab_index(int64_t r, int64_t wb, int64_t rows)
+{
+    return ((wb / kSlabWords) * rows + r) * kSlabWords + (wb % kSlabWords);
+}
 
 // Workgroups are dealt to the XCDs round-robin by workgroup id.  These helpers
 // turn a linear id into (xcd, index within that xcd).
@@ -19,8 +34,13 @@ __device__ __forceinline__ int local_of(int bid) { return bid / kXcds; }
 // ---- launchers (each returns the hipError_t of its launch) ----
 
 hipError_t launch_encode(const uint8_t *x, int64_t n, int32_t d,
-                         const uint8_t *thresholds, int32_t b, uint64_t *out,
+                         const uint8_t *thresholds, int32_t b, uint64_t *out, int layout,
                          hipStream_t stream);
+
+// Slab-layout LUT layer over n_slabs slabs (bitlogic_forward's intermediates).
+hipError_t launch_lut_layer_slab(const uint64_t *in, int32_t w_in, int64_t n_slabs,
+                                 const int32_t *conn, const uint64_t *tables, int32_t w_out,
+                                 int32_t k, uint64_t *out, hipStream_t stream);
 
 hipError_t launch_lut_layer(const uint64_t *in, int32_t w_in, int64_t n_words,
                             const int32_t *conn, const uint64_t *tables,
@@ -37,6 +57,6 @@ HeadPlan plan_head(int32_t w, int64_t n, int32_t c);
 
 hipError_t launch_head(const uint64_t *bits, int32_t w, int64_t n, int32_t c,
                        int32_t *scores, int32_t *argmax, void *ws,
-                       const HeadPlan &plan, hipStream_t stream);
+                       const HeadPlan &plan, int layout, hipStream_t stream);
 
 }  // namespace bl

@@ -4,33 +4,188 @@
 // heads"; App. A "Initialization"), packed 64 samples per 64-bit word along
 // the batch (App. C.1 "Bit-packed inference").
 //
-// Mapping: one lane per sample, one wave per 64-sample column, so a wave64
-// ballot of the comparison is exactly the packed word of one wire.  Ballots
-// land in SGPRs; v_writelane moves wire q's word into lane (q mod 64) of an
-// accumulator pair, and once 64 wires are collected every lane stores the
-// word of "its" wire, so each wave writes 64 rows at one column.
+// Two kernels, one lane per sample and one wave per 64-sample column in both:
 //
-// Tile: 32 features x 16 columns (1024 samples).  The 1024 x 32-byte pixel
-// tile is staged in LDS with coalesced loads (rows are read as 32 contiguous
-// bytes), then lanes read their own sample's byte from LDS.  The row stride
-// is padded to 36 bytes (9 dwords, odd) so the 64 lanes of a wave spread
-// over the LDS banks.  16 columns per tile make each wire's output segment
-// 128 bytes, one full cache line.
+// k_encode_t (b <= 8, the hot path).  A block first fills an LDS code table
+// code[f][v] = sum_t (v > theta[f][t]) << t for its tile of features and every
+// pixel value v, then reuses it for many slabs of 256 samples.  Per slab the
+// 256 x FT pixel tile is staged in LDS; each lane assembles, for a group of
+// floor(64/b) features, the 64-bit row of its sample's wires (one table read
+// and one shift-or per feature), and a 64x64 bit transpose across the wave
+// (v_permlane32_swap for the 32-lane halves, then five ds_swizzle xor stages,
+// each a rotate (v_alignbit) and a bit-field merge (v_bfi) per register) turns
+// rows of samples into packed words of wires: lane p ends with wire p's word.
 //
-// XCD-aware order: tile (column group cg, feature tile ft) runs on
-// XCD cg % 8, and each XCD walks the feature tiles of one column group in
-// order, so the pixel lines shared by neighbouring feature tiles are
-// fetched once into that XCD's L2.
+// k_encode_ballot (any b <= 64).  Each comparison is a wave64 ballot, i.e. the
+// packed word of one wire; v_writelane collects 64 such words into one lane
+// each before they are stored.
+//
+// Both write either the row-major layout [wires][W] of bitlogic_encode or the
+// slab layout [W/4][wires][4] of bitlogic_forward's intermediates.
 #include "bl_internal.h"
 
 namespace bl {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kFeat = 32;              // features per tile
-constexpr int kRow = kFeat + 4;        // LDS bytes per staged sample row
-constexpr int kCols = 16;              // 64-sample columns per tile
-constexpr int kSamples = kCols * kWave;
+
+template <int LAYOUT>
+__device__ __forceinline__ int64_t out_index(int64_t wire, int64_t wb, int64_t W, int64_t rows)
+{
+    if constexpr (LAYOUT == kLayoutSlab)
+        return slab_index(wire, wb, rows);
+    else
+        return wire * W + wb;
+}
+
+__device__ __forceinline__ uint32_t bfi(uint32_t sel, uint32_t one, uint32_t zero)
+{
+    return (sel & one) | (~sel & zero);
+}
+
+// One block-swap stage of the 32x32 transpose inside each 32-lane half: lanes
+// l and l^S exchange the S-bit blocks that sit off the diagonal.
+template <int S, int K>
+__device__ __forceinline__ void swap_stage(uint32_t &v, const uint32_t (&amt)[5],
+                                           const uint32_t (&msk)[5])
+{
+    constexpr int kPattern = 0x1F | (S << 10);     // ds_swizzle bit mode: lane ^ S
+    const uint32_t y = (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, kPattern);
+    v = bfi(msk[K], v, __builtin_amdgcn_alignbit(y, y, amt[K]));
+}
+
+// 64x64 bit transpose across a wave.  In: lane l holds bits (lo, hi) = row l.
+// Out: lane p holds column p (bit l of (lo, hi) = old bit p of lane l).
+__device__ __forceinline__ void transpose64(uint32_t &lo, uint32_t &hi,
+                                            const uint32_t (&amt)[5], const uint32_t (&msk)[5])
+{
+    // off-diagonal 32x32 blocks: hi of lanes 0..31 <-> lo of lanes 32..63
+    const auto sw = __builtin_amdgcn_permlane32_swap(lo, hi, false, false);
+    lo = sw[0];
+    hi = sw[1];
+    // each register is now a 32x32 block per 32-lane half: recursive block swap
+    swap_stage<16, 0>(lo, amt, msk); swap_stage<16, 0>(hi, amt, msk);
+    swap_stage<8, 1>(lo, amt, msk);  swap_stage<8, 1>(hi, amt, msk);
+    swap_stage<4, 2>(lo, amt, msk);  swap_stage<4, 2>(hi, amt, msk);
+    swap_stage<2, 3>(lo, amt, msk);  swap_stage<2, 3>(hi, amt, msk);
+    swap_stage<1, 4>(lo, amt, msk);  swap_stage<1, 4>(hi, amt, msk);
+}
+
+template <int B>
+struct EncGeom {
+    static constexpr int kFPG = 64 / B;                  // features per 64-wire group
+    static constexpr int kWPG = kFPG * B;                // wires per group (<= 64)
+    static constexpr int kG = (B <= 2) ? 1 : (B == 4) ? 2 : (B == 5) ? 3 : 4;
+    static constexpr int kFT = kFPG * kG;                // features per tile
+    static constexpr int kRowB = ((kFT / 4) % 2 == 1) ? kFT : kFT + 4;  // odd dword stride
+    static_assert(kFT % 4 == 0, "feature tile must be whole dwords");
+};
+
+template <int B, int LAYOUT>
+__global__ __launch_bounds__(kThreads) void k_encode_t(
+    const uint8_t *__restrict__ x, int64_t n, int32_t d, const uint8_t *__restrict__ th,
+    uint64_t *__restrict__ out, int64_t W, int32_t n_ftiles, int32_t slabs_per_block,
+    int64_t n_slabs, int64_t n_sgroups, int aligned4)
+{
+    using G = EncGeom<B>;
+    __shared__ uint8_t lut[G::kFT * 256];
+    __shared__ uint8_t xs[4 * kWave * G::kRowB];
+    __shared__ uint8_t ths[G::kFT * B];
+
+    const int bid = blockIdx.x;
+    const int64_t loc = local_of(bid);
+    const int64_t sg = (int64_t)xcd_of(bid) + (int64_t)kXcds * (loc / n_ftiles);
+    const int ft = (int)(loc % n_ftiles);
+    if (sg >= n_sgroups)
+        return;
+    const int f0 = ft * G::kFT;
+    const int nf = min(G::kFT, d - f0);
+    const int64_t D0 = (int64_t)d * B;
+    const int lane = threadIdx.x % kWave;
+    const int wave = threadIdx.x / kWave;
+
+    // ---- code table for this feature tile
+    for (int q = threadIdx.x; q < nf * B; q += kThreads)
+        ths[q] = th[(int64_t)f0 * B + q];
+    __syncthreads();
+    for (int q = threadIdx.x; q < G::kFT * 256; q += kThreads) {
+        const int f = q >> 8;
+        const uint32_t v = q & 255;
+        uint32_t code = 0;
+        if (f < nf) {
+#pragma unroll
+            for (int t = B - 1; t >= 0; --t)
+                code = 2 * code + (v > (uint32_t)ths[f * B + t] ? 1u : 0u);
+        }
+        lut[q] = (uint8_t)code;
+    }
+
+    // per-lane constants of the transpose stages
+    uint32_t amt[5], msk[5];
+    {
+        const uint32_t low[5] = {0x0000FFFFu, 0x00FF00FFu, 0x0F0F0F0Fu, 0x33333333u, 0x55555555u};
+#pragma unroll
+        for (int k = 0; k < 5; ++k) {
+            const int s = 16 >> k;
+            const bool up = (lane & s) != 0;
+            amt[k] = up ? s : 32 - s;
+            msk[k] = up ? ~low[k] : low[k];
+        }
+    }
+
+    const int64_t slab0 = sg * slabs_per_block;
+    const int64_t slab1 = min(slab0 + slabs_per_block, n_slabs);
+    for (int64_t slab = slab0; slab < slab1; ++slab) {
+        __syncthreads();     // table ready / previous tile consumed
+        const int64_t s0 = slab * 4 * kWave;
+        if (aligned4) {
+            constexpr int kDw = G::kFT / 4;
+            for (int q = threadIdx.x; q < 4 * kWave * kDw; q += kThreads) {
+                const int r = q / kDw, dw = q % kDw;
+                const int64_t s = s0 + r;
+                uint32_t v = 0;
+                if (s < n && 4 * dw < nf)
+                    v = *reinterpret_cast<const uint32_t *>(x + s * d + f0 + 4 * dw);
+                *reinterpret_cast<uint32_t *>(&xs[r * G::kRowB + 4 * dw]) = v;
+            }
+        } else {
+            for (int q = threadIdx.x; q < 4 * kWave * G::kFT; q += kThreads) {
+                const int r = q / G::kFT, f = q % G::kFT;
+                const int64_t s = s0 + r;
+                xs[r * G::kRowB + f] = (s < n && f < nf) ? x[s * d + f0 + f] : 0;
+            }
+        }
+        __syncthreads();
+
+        const int64_t wb = slab * 4 + wave;
+        const bool col_ok = (LAYOUT == kLayoutSlab) || wb < W;
+        const uint8_t *xrow = &xs[(wave * kWave + lane) * G::kRowB];
+#pragma unroll
+        for (int gi = 0; gi < G::kG; ++gi) {
+            uint32_t lo = 0, hi = 0;
+#pragma unroll
+            for (int fl = 0; fl < G::kFPG; ++fl) {
+                const int f = gi * G::kFPG + fl;
+                const uint32_t code = lut[f * 256 + xrow[f]];
+                const int pos = fl * B;
+                if (pos + B <= 32) {
+                    lo |= code << pos;
+                } else if (pos >= 32) {
+                    hi |= code << (pos - 32);
+                } else {
+                    lo |= code << pos;
+                    hi |= code >> (32 - pos);
+                }
+            }
+            transpose64(lo, hi, amt, msk);
+            const int fg = gi * G::kFPG;              // first feature of the group in the tile
+            if (col_ok && lane < G::kWPG && fg + lane / B < nf) {
+                const int64_t wire = (int64_t)(f0 + fg) * B + lane;
+                out[out_index<LAYOUT>(wire, wb, W, D0)] = ((uint64_t)hi << 32) | lo;
+            }
+        }
+    }
+}
 
 // Write a wave-uniform value into one lane of a VGPR (v_writelane_b32).  The
 // lane select goes through M0: with the value already in an SGPR, a second
@@ -43,14 +198,19 @@ __device__ __forceinline__ uint32_t write_lane(uint32_t acc, uint32_t value, int
     return acc;
 }
 
-template <bool kAligned4>
-__global__ __launch_bounds__(kThreads) void k_encode(
+constexpr int kBFeat = 32;             // features per tile
+constexpr int kBRow = kBFeat + 4;      // LDS bytes per staged sample row (9 dwords)
+constexpr int kBCols = 16;             // 64-sample columns per tile
+constexpr int kBSamples = kBCols * kWave;
+
+template <bool kAligned4, int LAYOUT>
+__global__ __launch_bounds__(kThreads) void k_encode_ballot(
     const uint8_t *__restrict__ x, int64_t n, int32_t d,
     const uint8_t *__restrict__ th, int32_t b, uint64_t *__restrict__ out,
-    int64_t W, int32_t n_ftiles, int64_t n_cgroups)
+    int64_t W, int64_t W_cols, int32_t n_ftiles, int64_t n_cgroups)
 {
-    __shared__ uint8_t xs[kSamples * kRow];
-    __shared__ uint8_t ths[kFeat * 64];
+    __shared__ uint8_t xs[kBSamples * kBRow];
+    __shared__ uint8_t ths[kBFeat * 64];
 
     const int bid = blockIdx.x;
     const int64_t loc = local_of(bid);
@@ -58,42 +218,40 @@ __global__ __launch_bounds__(kThreads) void k_encode(
     const int ft = (int)(loc % n_ftiles);
     if (cg >= n_cgroups)
         return;
-    const int f0 = ft * kFeat;
-    const int nf = min(kFeat, d - f0);
-    const int64_t s0 = cg * kSamples;
+    const int f0 = ft * kBFeat;
+    const int nf = min(kBFeat, d - f0);
+    const int64_t s0 = cg * kBSamples;
+    const int64_t D0 = (int64_t)d * b;
 
-    // ---- stage thresholds and the pixel tile in LDS
     for (int q = threadIdx.x; q < nf * b; q += kThreads)
         ths[q] = th[(int64_t)f0 * b + q];
     if (kAligned4) {
-        // 8 dwords per sample row; features >= d are zero (never read)
-        for (int q = threadIdx.x; q < kSamples * (kFeat / 4); q += kThreads) {
-            const int r = q / (kFeat / 4), dw = q % (kFeat / 4);
+        for (int q = threadIdx.x; q < kBSamples * (kBFeat / 4); q += kThreads) {
+            const int r = q / (kBFeat / 4), dw = q % (kBFeat / 4);
             const int64_t s = s0 + r;
             uint32_t v = 0;
             if (s < n && 4 * dw < nf)
                 v = *reinterpret_cast<const uint32_t *>(x + s * d + f0 + 4 * dw);
-            *reinterpret_cast<uint32_t *>(&xs[r * kRow + 4 * dw]) = v;
+            *reinterpret_cast<uint32_t *>(&xs[r * kBRow + 4 * dw]) = v;
         }
     } else {
-        for (int q = threadIdx.x; q < kSamples * kFeat; q += kThreads) {
-            const int r = q / kFeat, f = q % kFeat;
+        for (int q = threadIdx.x; q < kBSamples * kBFeat; q += kThreads) {
+            const int r = q / kBFeat, f = q % kBFeat;
             const int64_t s = s0 + r;
-            xs[r * kRow + f] = (s < n && f < nf) ? x[s * d + f0 + f] : 0;
+            xs[r * kBRow + f] = (s < n && f < nf) ? x[s * d + f0 + f] : 0;
         }
     }
     __syncthreads();
 
-    // ---- ballots: wave w handles columns w, w+4, w+8, w+12 of the tile
     const int lane = threadIdx.x % kWave;
     const int wave = threadIdx.x / kWave;
     const int nwires = nf * b;
     const int64_t wire0 = (int64_t)f0 * b;
-    for (int c = wave; c < kCols; c += kThreads / kWave) {
-        const int64_t col = cg * kCols + c;
-        if (col >= W)
+    for (int c = wave; c < kBCols; c += kThreads / kWave) {
+        const int64_t col = cg * kBCols + c;
+        if (col >= W_cols)
             break;
-        const uint8_t *xrow = &xs[(c * kWave + lane) * kRow];
+        const uint8_t *xrow = &xs[(c * kWave + lane) * kBRow];
         uint32_t acc_lo = 0, acc_hi = 0;
         int q = 0;
         for (int f = 0; f < nf; ++f) {
@@ -105,39 +263,89 @@ __global__ __launch_bounds__(kThreads) void k_encode(
                 acc_hi = write_lane(acc_hi, (uint32_t)(m >> 32), pos);
                 if (pos == kWave - 1) {
                     const int64_t wire = wire0 + (q - (kWave - 1)) + lane;
-                    out[wire * W + col] = ((uint64_t)acc_hi << 32) | acc_lo;
+                    out[out_index<LAYOUT>(wire, col, W, D0)] = ((uint64_t)acc_hi << 32) | acc_lo;
                 }
             }
         }
         const int rem = nwires & (kWave - 1);
         if (rem != 0 && lane < rem) {
             const int64_t wire = wire0 + (nwires - rem) + lane;
-            out[wire * W + col] = ((uint64_t)acc_hi << 32) | acc_lo;
+            out[out_index<LAYOUT>(wire, col, W, D0)] = ((uint64_t)acc_hi << 32) | acc_lo;
         }
     }
 }
 
-}  // namespace
+template <int B, int LAYOUT>
+hipError_t launch_t(const uint8_t *x, int64_t n, int32_t d, const uint8_t *th, uint64_t *out,
+                    hipStream_t stream)
+{
+    using G = EncGeom<B>;
+    const int64_t W = (n + 63) / 64;
+    const int64_t n_slabs = (W + 3) / 4;
+    const int32_t n_ftiles = (d + G::kFT - 1) / G::kFT;
+    // enough blocks to fill the chip; at most 32 slabs reuse one code table
+    int64_t spb = n_slabs * n_ftiles / 2048;
+    spb = spb < 1 ? 1 : (spb > 32 ? 32 : spb);
+    const int64_t n_sg = (n_slabs + spb - 1) / spb;
+    const int64_t n_sg_pad = (n_sg + kXcds - 1) / kXcds * kXcds;
+    const int64_t blocks = n_sg_pad * n_ftiles;
+    if (blocks > 0x7fffffff)
+        return hipErrorInvalidConfiguration;
+    const int aligned4 = (d % 4 == 0) && ((uintptr_t)x % 4 == 0);
+    hipLaunchKernelGGL((k_encode_t<B, LAYOUT>), dim3((unsigned)blocks), dim3(kThreads), 0, stream,
+                       x, n, d, th, out, W, n_ftiles, (int32_t)spb, n_slabs, n_sg, aligned4);
+    return hipGetLastError();
+}
 
-hipError_t launch_encode(const uint8_t *x, int64_t n, int32_t d,
-                         const uint8_t *thresholds, int32_t b, uint64_t *out,
-                         hipStream_t stream)
+template <int LAYOUT>
+hipError_t launch_ballot(const uint8_t *x, int64_t n, int32_t d, const uint8_t *th, int32_t b,
+                         uint64_t *out, hipStream_t stream)
 {
     const int64_t W = (n + 63) / 64;
-    const int32_t n_ftiles = (d + kFeat - 1) / kFeat;
-    const int64_t n_cg = (W + kCols - 1) / kCols;
+    // the slab layout has whole slabs of 4 columns (padding columns are zero)
+    const int64_t W_cols = (LAYOUT == kLayoutSlab) ? (W + 3) / 4 * 4 : W;
+    const int32_t n_ftiles = (d + kBFeat - 1) / kBFeat;
+    const int64_t n_cg = (W_cols + kBCols - 1) / kBCols;
     const int64_t n_cg_pad = (n_cg + kXcds - 1) / kXcds * kXcds;
     const int64_t blocks = n_cg_pad * n_ftiles;
     if (blocks > 0x7fffffff)
         return hipErrorInvalidConfiguration;
     const bool aligned4 = (d % 4 == 0) && ((uintptr_t)x % 4 == 0);
     if (aligned4)
-        hipLaunchKernelGGL(k_encode<true>, dim3((unsigned)blocks), dim3(kThreads), 0, stream,
-                           x, n, d, thresholds, b, out, W, n_ftiles, n_cg);
+        hipLaunchKernelGGL((k_encode_ballot<true, LAYOUT>), dim3((unsigned)blocks), dim3(kThreads),
+                           0, stream, x, n, d, th, b, out, W, W_cols, n_ftiles, n_cg);
     else
-        hipLaunchKernelGGL(k_encode<false>, dim3((unsigned)blocks), dim3(kThreads), 0, stream,
-                           x, n, d, thresholds, b, out, W, n_ftiles, n_cg);
+        hipLaunchKernelGGL((k_encode_ballot<false, LAYOUT>), dim3((unsigned)blocks),
+                           dim3(kThreads), 0, stream, x, n, d, th, b, out, W, W_cols, n_ftiles,
+                           n_cg);
     return hipGetLastError();
+}
+
+template <int LAYOUT>
+hipError_t launch_layout(const uint8_t *x, int64_t n, int32_t d, const uint8_t *th, int32_t b,
+                         uint64_t *out, hipStream_t stream)
+{
+    switch (b) {
+    case 1: return launch_t<1, LAYOUT>(x, n, d, th, out, stream);
+    case 2: return launch_t<2, LAYOUT>(x, n, d, th, out, stream);
+    case 3: return launch_t<3, LAYOUT>(x, n, d, th, out, stream);
+    case 4: return launch_t<4, LAYOUT>(x, n, d, th, out, stream);
+    case 5: return launch_t<5, LAYOUT>(x, n, d, th, out, stream);
+    case 6: return launch_t<6, LAYOUT>(x, n, d, th, out, stream);
+    case 7: return launch_t<7, LAYOUT>(x, n, d, th, out, stream);
+    case 8: return launch_t<8, LAYOUT>(x, n, d, th, out, stream);
+    default: return launch_ballot<LAYOUT>(x, n, d, th, b, out, stream);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_encode(const uint8_t *x, int64_t n, int32_t d, const uint8_t *thresholds,
+                         int32_t b, uint64_t *out, int layout, hipStream_t stream)
+{
+    if (layout == kLayoutSlab)
+        return launch_layout<kLayoutSlab>(x, n, d, thresholds, b, out, stream);
+    return launch_layout<kLayoutRowMajor>(x, n, d, thresholds, b, out, stream);
 }
 
 }  // namespace bl

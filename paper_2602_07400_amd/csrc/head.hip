@@ -13,7 +13,8 @@
 // into row ranges so the launch fills the chip.  Stage 2 runs one lane per
 // sample: it reads the planes of its column (wave-uniform scalar loads),
 // assembles each class score bit by bit, sums the splits and tracks the
-// running argmax.
+// running argmax; the score tile of the column is staged in LDS and written
+// as one contiguous block.
 #include "bl_internal.h"
 
 namespace bl {
@@ -44,10 +45,10 @@ __device__ __forceinline__ void ripple_add(uint64_t (&cnt)[P], uint64_t carry, i
     }
 }
 
-template <int P>
+template <int P, int LAYOUT>
 __global__ __launch_bounds__(kThreads) void k_head_planes(
-    const uint64_t *__restrict__ bits, int64_t W, int32_t g, int32_t S, int32_t rps,
-    int32_t c, uint64_t *__restrict__ planes, int64_t n_cb)
+    const uint64_t *__restrict__ bits, int64_t W, int32_t w, int32_t g, int32_t S,
+    int32_t rps, int32_t c, uint64_t *__restrict__ planes, int64_t n_cb)
 {
     const int lane = threadIdx.x % kWave;
     const int64_t task = (int64_t)blockIdx.x * kWaves + threadIdx.x / kWave;
@@ -62,18 +63,28 @@ __global__ __launch_bounds__(kThreads) void k_head_planes(
     const int64_t r0 = (int64_t)i * g + (int64_t)q * rps;
     const int64_t r1 = min(r0 + rps, (int64_t)(i + 1) * g);
 
+    // word (r, colc) = src[r * stride]
+    const uint64_t *src;
+    int64_t stride;
+    if constexpr (LAYOUT == kLayoutSlab) {
+        src = bits + slab_index(0, colc, w);
+        stride = kSlabWords;
+    } else {
+        src = bits + colc;
+        stride = W;
+    }
+
     uint64_t cnt[P];
 #pragma unroll
     for (int p = 0; p < P; ++p)
         cnt[p] = 0;
-    const uint64_t *src = bits + colc;
     int64_t r = r0;
     if constexpr (P >= 4) {
         for (; r + 8 <= r1; r += 8) {
             uint64_t d[8];
 #pragma unroll
             for (int u = 0; u < 8; ++u)
-                d[u] = src[(r + u) * W];
+                d[u] = src[(r + u) * stride];
             uint64_t twosA, twosB, foursA, foursB, eights;
             csa(twosA, cnt[0], cnt[0], d[0], d[1]);
             csa(twosB, cnt[0], cnt[0], d[2], d[3]);
@@ -86,44 +97,64 @@ __global__ __launch_bounds__(kThreads) void k_head_planes(
         }
     }
     for (; r < r1; ++r)
-        ripple_add<P>(cnt, src[r * W], 0);
+        ripple_add<P>(cnt, src[r * stride], 0);
 
+    // planes of one column are contiguous: [col][class][split][plane]
     if (col < W) {
-        uint64_t *dst = planes + ((int64_t)(i * S + q) * P) * W + col;
+        uint64_t *dst = planes + ((col * c + i) * (int64_t)S + q) * P;
 #pragma unroll
         for (int p = 0; p < P; ++p)
-            dst[(int64_t)p * W] = cnt[p];
+            dst[p] = cnt[p];
     }
 }
 
+constexpr int kFinishClasses = 128;   // at most this many classes per LDS score tile
+
+// One wave per 64-sample column: assemble each class score from its bit
+// planes (wave-uniform scalar loads), track the argmax, and stage the
+// 64 x classes score tile in LDS so it is written as one contiguous block.
 template <int P>
-__global__ __launch_bounds__(kThreads) void k_head_finish(
+__global__ __launch_bounds__(kWave) void k_head_finish(
     const uint64_t *__restrict__ planes, int64_t W, int64_t n, int32_t c, int32_t S,
     int32_t *__restrict__ scores, int32_t *__restrict__ argmax)
 {
-    const int lane = threadIdx.x % kWave;
-    const int64_t col = (int64_t)blockIdx.x * kWaves +
-                        __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    extern __shared__ int32_t tile[];     // [64][min(c, kFinishClasses)]
+    const int lane = threadIdx.x;
+    const int64_t col = blockIdx.x;
     if (col >= W)
         return;
     const int64_t s = col * kWave + lane;
+    const uint64_t *pc = planes + col * (int64_t)c * S * P;
     int32_t best = -1, besti = 0;
-    for (int i = 0; i < c; ++i) {
-        int32_t cnt = 0;
-        for (int q = 0; q < S; ++q) {
-            const uint64_t *pl = planes + ((int64_t)(i * S + q) * P) * W + col;
-            int32_t part = 0;
+    for (int c0 = 0; c0 < c; c0 += kFinishClasses) {
+        const int cn = min(kFinishClasses, c - c0);
+        for (int ii = 0; ii < cn; ++ii) {
+            const int i = c0 + ii;
+            int32_t cnt = 0;
+            for (int q = 0; q < S; ++q) {
+                const uint64_t *pl = pc + ((int64_t)i * S + q) * P;
+                int32_t part = 0;
 #pragma unroll
-            for (int p = 0; p < P; ++p)
-                part |= (int32_t)((pl[(int64_t)p * W] >> lane) & 1u) << p;
-            cnt += part;
+                for (int p = 0; p < P; ++p)
+                    part |= (int32_t)((pl[p] >> lane) & 1u) << p;
+                cnt += part;
+            }
+            tile[lane * cn + ii] = cnt;
+            if (cnt > best) {
+                best = cnt;
+                besti = i;
+            }
         }
-        if (scores && s < n)
-            scores[s * c + i] = cnt;
-        if (cnt > best) {
-            best = cnt;
-            besti = i;
+        __syncthreads();
+        if (scores) {
+            const int64_t s0 = col * kWave;
+            for (int e = lane; e < kWave * cn; e += kWave) {
+                const int64_t ss = s0 + e / cn;
+                if (ss < n)
+                    scores[ss * c + c0 + e % cn] = tile[e];
+            }
         }
+        __syncthreads();
     }
     if (argmax && s < n)
         argmax[s] = besti;
@@ -132,21 +163,27 @@ __global__ __launch_bounds__(kThreads) void k_head_finish(
 template <int P>
 hipError_t launch_p(const uint64_t *bits, int32_t w, int64_t n, int32_t c,
                     int32_t *scores, int32_t *argmax, uint64_t *planes,
-                    const HeadPlan &plan, hipStream_t stream)
+                    const HeadPlan &plan, int layout, hipStream_t stream)
 {
     const int64_t W = (n + 63) / 64;
     const int64_t n_cb = (W + kWave - 1) / kWave;
     const int64_t tasks = n_cb * plan.splits * c;
     const int64_t blocks1 = (tasks + kWaves - 1) / kWaves;
-    const int64_t blocks2 = (W + kWaves - 1) / kWaves;
-    if (blocks1 > 0x7fffffff || blocks2 > 0x7fffffff)
+    if (blocks1 > 0x7fffffff || W > 0x7fffffff)
         return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL(k_head_planes<P>, dim3((unsigned)blocks1), dim3(kThreads), 0, stream,
-                       bits, W, w / c, plan.splits, plan.rows_per_split, c, planes, n_cb);
+    if (layout == kLayoutSlab)
+        hipLaunchKernelGGL((k_head_planes<P, kLayoutSlab>), dim3((unsigned)blocks1),
+                           dim3(kThreads), 0, stream, bits, W, w, w / c, plan.splits,
+                           plan.rows_per_split, c, planes, n_cb);
+    else
+        hipLaunchKernelGGL((k_head_planes<P, kLayoutRowMajor>), dim3((unsigned)blocks1),
+                           dim3(kThreads), 0, stream, bits, W, w, w / c, plan.splits,
+                           plan.rows_per_split, c, planes, n_cb);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL(k_head_finish<P>, dim3((unsigned)blocks2), dim3(kThreads), 0, stream,
+    const size_t lds = (size_t)kWave * (c < kFinishClasses ? c : kFinishClasses) * sizeof(int32_t);
+    hipLaunchKernelGGL(k_head_finish<P>, dim3((unsigned)W), dim3(kWave), lds, stream,
                        planes, W, n, c, plan.splits, scores, argmax);
     return hipGetLastError();
 }
@@ -194,12 +231,12 @@ HeadPlan plan_head(int32_t w, int64_t n, int32_t c)
 
 hipError_t launch_head(const uint64_t *bits, int32_t w, int64_t n, int32_t c,
                        int32_t *scores, int32_t *argmax, void *ws, const HeadPlan &plan,
-                       hipStream_t stream)
+                       int layout, hipStream_t stream)
 {
     uint64_t *planes = static_cast<uint64_t *>(ws);
     switch (plan.planes) {
 #define BL_CASE(P) \
-    case P: return launch_p<P>(bits, w, n, c, scores, argmax, planes, plan, stream);
+    case P: return launch_p<P>(bits, w, n, c, scores, argmax, planes, plan, layout, stream);
     BL_CASE(1) BL_CASE(2) BL_CASE(3) BL_CASE(4) BL_CASE(5) BL_CASE(6) BL_CASE(7) BL_CASE(8)
     BL_CASE(9) BL_CASE(10) BL_CASE(11) BL_CASE(12) BL_CASE(13) BL_CASE(14) BL_CASE(15)
     BL_CASE(16)

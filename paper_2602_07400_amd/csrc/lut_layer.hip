@@ -168,6 +168,93 @@ __global__ __launch_bounds__(kThreads) void k_lut_layer(
     }
 }
 
+// ---------------------------------------------------------------------------
+// Slab layout (used for the intermediate tensors of bitlogic_forward): the
+// batch is cut into slabs of kSlabWords words (256 samples); within a slab the
+// rows are contiguous, 32 bytes each:
+//     word (row r, column wb) at ((wb / kSlabWords) * rows + r) * kSlabWords + wb % kSlabWords
+// One lane evaluates one node on one slab: it gathers K 32-byte row segments
+// (two 16-byte loads each) and writes one 32-byte segment, so a wave's store
+// is 2 KB contiguous.  The per-XCD working set of a slab is w_in * 32 bytes
+// (2 MB for a 64000-wide input), small enough for the XCD's 4 MB L2, and every
+// line fetched is fully used.  Output stores are non-temporal so the output
+// stream does not evict the input slab.
+template <int K, int NB>
+__global__ __launch_bounds__(kThreads) void k_lut_slab(
+    const uint64_t *__restrict__ in, int32_t w_in, const int32_t *__restrict__ conn,
+    const uint64_t *__restrict__ tables, int32_t w_out, uint64_t *__restrict__ out,
+    int32_t n_nblk, int32_t n_slabs)
+{
+    static_assert(NB % kThreads == 0, "node block must be whole passes");
+    __shared__ int32_t s_conn[NB * K];
+    __shared__ uint64_t s_tab[NB];
+
+    const int bid = blockIdx.x;
+    const int loc = local_of(bid);
+    const int slab = (loc / n_nblk) * kXcds + xcd_of(bid);
+    const int nblk = loc % n_nblk;
+    if (slab >= n_slabs)
+        return;
+    const int node0 = nblk * NB;
+    const int nodes = min(NB, w_out - node0);
+
+    for (int q = threadIdx.x; q < NB * K; q += kThreads)
+        s_conn[q] = (q < nodes * K) ? conn[(int64_t)node0 * K + q] : 0;
+    for (int q = threadIdx.x; q < NB; q += kThreads)
+        s_tab[q] = (q < nodes) ? tables[node0 + q] : 0;
+    __syncthreads();
+
+    const u32x4 *src = reinterpret_cast<const u32x4 *>(in + (int64_t)slab * w_in * kSlabWords);
+    u32x4 *dst = reinterpret_cast<u32x4 *>(out + ((int64_t)slab * w_out + node0) * kSlabWords);
+
+#pragma unroll 1
+    for (int pass = 0; pass < NB / kThreads; ++pass) {
+        if (pass * kThreads >= nodes)
+            break;
+        const int jl = pass * kThreads + threadIdx.x;
+        uint32_t xv[2 * kSlabWords][K];
+#pragma unroll
+        for (int i = 0; i < K; ++i) {
+            const u32x4 *p = src + 2 * s_conn[jl * K + i];
+            const u32x4 a = p[0], b = p[1];
+            xv[0][i] = a.x; xv[1][i] = a.y; xv[2][i] = a.z; xv[3][i] = a.w;
+            xv[4][i] = b.x; xv[5][i] = b.y; xv[6][i] = b.z; xv[7][i] = b.w;
+        }
+        const uint64_t T = s_tab[jl];
+        const uint32_t t_lo = (uint32_t)T, t_hi = (uint32_t)(T >> 32);
+        uint32_t m[1 << K];
+#pragma unroll
+        for (int a = 0; a < (1 << K); ++a)
+            m[a] = 0u - (((a < 32 ? t_lo : t_hi) >> (a & 31)) & 1u);
+        uint32_t o[2 * kSlabWords];
+#pragma unroll
+        for (int h = 0; h < 2 * kSlabWords; ++h)
+            o[h] = mux_tree<K>(xv[h], m);
+        if (jl < nodes) {
+            u32x4 *q = dst + 2 * jl;
+            __builtin_nontemporal_store(u32x4{o[0], o[1], o[2], o[3]}, q);
+            __builtin_nontemporal_store(u32x4{o[4], o[5], o[6], o[7]}, q + 1);
+        }
+    }
+}
+
+constexpr int kSlabNB = 512;
+
+template <int K>
+hipError_t launch_slab_k(const uint64_t *in, int32_t w_in, int64_t n_slabs,
+                         const int32_t *conn, const uint64_t *tables, int32_t w_out,
+                         uint64_t *out, hipStream_t stream)
+{
+    const int32_t n_nblk = (w_out + kSlabNB - 1) / kSlabNB;
+    const int64_t slabs_pad = (n_slabs + kXcds - 1) / kXcds * kXcds;
+    const int64_t blocks = slabs_pad * n_nblk;
+    if (blocks > 0x7fffffff)
+        return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((k_lut_slab<K, kSlabNB>), dim3((unsigned)blocks), dim3(kThreads), 0,
+                       stream, in, w_in, conn, tables, w_out, out, n_nblk, (int32_t)n_slabs);
+    return hipGetLastError();
+}
+
 constexpr int kLPN = 4;
 constexpr int kR = 4;
 constexpr int kNB = 256;
@@ -211,6 +298,21 @@ hipError_t launch_k(const uint64_t *in, int64_t W, const int32_t *conn,
 }
 
 }  // namespace
+
+hipError_t launch_lut_layer_slab(const uint64_t *in, int32_t w_in, int64_t n_slabs,
+                                 const int32_t *conn, const uint64_t *tables, int32_t w_out,
+                                 int32_t k, uint64_t *out, hipStream_t stream)
+{
+    switch (k) {
+    case 1: return launch_slab_k<1>(in, w_in, n_slabs, conn, tables, w_out, out, stream);
+    case 2: return launch_slab_k<2>(in, w_in, n_slabs, conn, tables, w_out, out, stream);
+    case 3: return launch_slab_k<3>(in, w_in, n_slabs, conn, tables, w_out, out, stream);
+    case 4: return launch_slab_k<4>(in, w_in, n_slabs, conn, tables, w_out, out, stream);
+    case 5: return launch_slab_k<5>(in, w_in, n_slabs, conn, tables, w_out, out, stream);
+    case 6: return launch_slab_k<6>(in, w_in, n_slabs, conn, tables, w_out, out, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
 
 hipError_t launch_lut_layer(const uint64_t *in, int32_t w_in, int64_t n_words,
                             const int32_t *conn, const uint64_t *tables,

@@ -299,3 +299,20 @@ def test_forward_on_side_stream():
     st.synchronize()
     rs, rp = oracle.forward(wl.x, wl.thresholds, wl.layers, wl.n_classes)
     assert np.array_equal(s.cpu().numpy(), rs) and np.array_equal(p.cpu().numpy(), rp)
+
+
+@pytest.mark.parametrize("n,d,b", [(64 * 4 * 3 + 77, 30, 10), (1000, 13, 64), (300, 7, 8)])
+def test_forward_encoder_variants(n, d, b):
+    """b > 8 takes the ballot encoder; d % 4 != 0 takes the byte-staging path."""
+    rng = np.random.default_rng(n + d + b)
+    x = rng.integers(0, 256, size=(n, d), dtype=np.uint8)
+    th = rng.integers(0, 256, size=(d, b), dtype=np.uint8)
+    layers, w_in = [], d * b
+    for w, k in ((200, 6), (120, 4)):
+        conn = np.stack([rng.choice(w_in, size=k, replace=False) for _ in range(w)]).astype(np.int32)
+        layers.append((conn, rng.integers(0, 1 << 63, size=w).astype(np.uint64)))
+        w_in = w
+    m = bl.BitlogicModel.from_numpy(th, layers, 6, device=DEV)
+    s, p = m.forward(torch.from_numpy(x).to(DEV))
+    rs, rp = oracle.forward(x, th, layers, 6)
+    assert np.array_equal(s.cpu().numpy(), rs) and np.array_equal(p.cpu().numpy(), rp)
