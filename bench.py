@@ -10,7 +10,8 @@ bitlogic_forward.  Default workload: the CIFAR-100-shaped wide network
 Prints ONE JSON line.  Besides the driver's fields it carries
   roofline      the dominant kernel (the LUT layer, integer-VALU bound at
                 k = 6) against the chip's 32-bit VALU peak, from per-launch
-                HIP-event times over a staged copy of the timed loop;
+                HIP-event times that the library records between the stages
+                of the same forward (bitlogic_forward_timed);
   cpu_baseline  the CPU oracle timed on a bounded sample of the same
                 workload on this host (and its agreement with the GPU there);
   detail        per-stage times, algorithmic bytes/ops and roofline fractions.
@@ -49,8 +50,8 @@ def parse():
     ap.add_argument("--stage-steps", type=int, default=None,
                     help="steps of the per-kernel (staged) timing loop; default = --steps")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
-                    help="also run a plain device copy of this many MiB (reference kernel "
-                         "for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE)")
+                    help="also run a write-only fill and a read-only sum over this many MiB "
+                         "(reference kernels for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     return ap.parse_args()
 
 
@@ -121,15 +122,19 @@ def main():
                             scores=scores, argmax=argmax, workspace=ws, stream=stream)
 
     if args.calibrate_copy_mib:
+        # reference kernels of known traffic for scaling rocprofv3's
+        # FETCH_SIZE / WRITE_SIZE: a read-only reduction and a write-only fill
         nbytes = args.calibrate_copy_mib << 20
-        src = torch.ones(nbytes // 8, dtype=torch.int64, device=dev)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
+        buf = torch.empty(nbytes // 8, dtype=torch.int64, device=dev)
+        for _ in range(2):
+            buf.fill_(1)
         torch.cuda.synchronize()
-        del src, dst
-        print(f"[bench] copy calibration: 3 x {nbytes} bytes read + written", file=sys.stderr,
-              flush=True)
+        for _ in range(2):
+            total = buf.sum()
+        torch.cuda.synchronize()
+        del buf, total
+        print(f"[bench] calibration: fill_ writes and sum reads {nbytes} bytes, twice each",
+              file=sys.stderr, flush=True)
 
     # ---- warmup, then exactly K timed steps
     for _ in range(args.warmup):
@@ -145,41 +150,20 @@ def main():
     print(f"[bench] timed {args.steps} steps: {ms_per_step:.3f} ms/step, {value:.2f} MSamples/s",
           file=sys.stderr, flush=True)
 
-    # ---- per-kernel times: the same kernels launched stage by stage on the
-    # same stream, HIP events between the stages
-    D0 = cfg.d * cfg.b
-    W = (n + 63) // 64
-    enc = torch.empty((D0, W), dtype=torch.int64, device=dev)
-    acts = [torch.empty((w, W), dtype=torch.int64, device=dev) for w in cfg.widths]
-    hws = torch.empty(max(1, bl.bitlogic_groupsum_head_workspace_bytes(cfg.widths[-1], n,
-                                                                       cfg.n_classes)),
-                      dtype=torch.uint8, device=dev)
+    # ---- per-kernel times: the same forward with HIP events recorded by the
+    # library at its stage boundaries, on the stream its kernels run on
     names = ["encode"] + [f"layer{l + 1}" for l in range(len(cfg.widths))] + ["head"]
-
-    def staged(events=None):
-        rec = (lambda i: events[i].record(stream)) if events else (lambda i: None)
-        rec(0)
-        bl.bitlogic_encode(x, model.thresholds, bits_out=enc, stream=stream)
-        rec(1)
-        cur = enc
-        for l, (conn, tab) in enumerate(model.layers):
-            bl.bitlogic_lut_layer(cur, conn, tab, bits_out=acts[l], stream=stream)
-            cur = acts[l]
-            rec(2 + l)
-        bl.bitlogic_groupsum_head(cur, n, cfg.n_classes, scores=scores, argmax=argmax,
-                                  workspace=hws, stream=stream)
-        rec(2 + len(model.layers))
-
-    for _ in range(3):
-        staged()
-    torch.cuda.synchronize()
     ksteps = args.stage_steps or args.steps
     sums = np.zeros(len(names))
-    for _ in range(ksteps):
+    for it in range(ksteps + 2):
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
-        staged(ev)
+        for e in ev:
+            e.record(stream)          # creates the HIP event handles
+        bl.bitlogic_forward_timed(x, model.thresholds, model.layers, model.n_classes, ev,
+                                  scores=scores, argmax=argmax, workspace=ws, stream=stream)
         torch.cuda.synchronize()
-        sums += [ev[i].elapsed_time(ev[i + 1]) for i in range(len(names))]
+        if it >= 2:                   # two untimed passes first
+            sums += [ev[i].elapsed_time(ev[i + 1]) for i in range(len(names))]
     stage_ms = dict(zip(names, (sums / ksteps).tolist()))
 
     alg = algorithmic(cfg, n)
@@ -197,7 +181,7 @@ def main():
     roofline = {"bound": layer_bound, "achieved": round(achieved, 3), "peak": round(peak, 3),
                 "unit": unit, "frac": round(achieved / peak, 4),
                 "traffic": traffic_for_current_kernel() if cfg.name == "c4_cifar100_wide" else None,
-                "kernel": "k_lut_layer (one LUT layer launch; mean of the layer launches)",
+                "kernel": "k_lut_slab (one LUT layer launch of the forward; mean of its layers)",
                 "per_launch": f"2*(2^k-1)*w*W = {layer_ops} int32 lane-ops"}
 
     detail = {

@@ -150,6 +150,21 @@ int bitlogic_forward(const uint8_t *x, int64_t n_samples, int32_t n_features,
                      int32_t n_classes, int32_t *scores, int32_t *argmax,
                      void *workspace, size_t workspace_bytes, void *stream);
 
+/* bitlogic_forward plus stage timing, for profiling: the same kernels on the
+ * same stream, and hipEventRecord(events[i], stream) at every stage boundary:
+ * events[0] before the encoder, events[1] after it, events[1 + l] after
+ * layer l (l = 1..n_layers), events[n_layers + 2] after the head.
+ * `events` is a host array of n_events = n_layers + 3 hipEvent_t handles
+ * (passed as void*) created by the caller; the timing is read with
+ * hipEventElapsedTime.  Errors as bitlogic_forward, plus BITLOGIC_ERR_SHAPE
+ * if n_events is wrong and BITLOGIC_ERR_NULL if an event is NULL. */
+int bitlogic_forward_timed(const uint8_t *x, int64_t n_samples, int32_t n_features,
+                           const uint8_t *thresholds, int32_t n_thresholds,
+                           const bitlogic_layer *layers, int32_t n_layers,
+                           int32_t n_classes, int32_t *scores, int32_t *argmax,
+                           void *workspace, size_t workspace_bytes, void *stream,
+                           void *const *events, int32_t n_events);
+
 /* Static description of a status code. */
 const char *bitlogic_status_string(int status);
 

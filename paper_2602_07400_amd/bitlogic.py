@@ -21,7 +21,7 @@ import torch
 
 __all__ = [
     "BitlogicError", "bitlogic_encode", "bitlogic_lut_layer", "bitlogic_groupsum_head",
-    "bitlogic_forward", "bitlogic_forward_workspace_bytes",
+    "bitlogic_forward", "bitlogic_forward_timed", "bitlogic_forward_workspace_bytes",
     "bitlogic_groupsum_head_workspace_bytes", "bitlogic_status_string", "bitlogic_version",
     "BitlogicModel", "library_path", "load_library", "words",
 ]
@@ -66,6 +66,8 @@ def load_library():
         "bitlogic_groupsum_head": ([P, i32, i64, i32, P, P, P, sz, P], ctypes.c_int),
         "bitlogic_forward_workspace_bytes": ([i64, i32, i32, P, i32, i32], sz),
         "bitlogic_forward": ([P, i64, i32, P, i32, P, i32, i32, P, P, P, sz, P], ctypes.c_int),
+        "bitlogic_forward_timed": ([P, i64, i32, P, i32, P, i32, i32, P, P, P, sz, P, P, i32],
+                                   ctypes.c_int),
         "bitlogic_status_string": ([ctypes.c_int], ctypes.c_char_p),
         "bitlogic_last_error": ([], ctypes.c_char_p),
         "bitlogic_version": ([], ctypes.c_int),
@@ -200,13 +202,8 @@ def bitlogic_forward_workspace_bytes(n_samples: int, n_features: int, n_threshol
         n_classes))
 
 
-def bitlogic_forward(x: torch.Tensor, thresholds: torch.Tensor,
-                     layers: Sequence[Tuple[torch.Tensor, torch.Tensor]], n_classes: int,
-                     scores: Optional[torch.Tensor] = None,
-                     argmax: Optional[torch.Tensor] = None,
-                     workspace: Optional[torch.Tensor] = None, stream=None,
-                     want_scores: bool = True):
-    """Whole forward: pixels uint8 [N][d] -> (scores int32 [N][c], argmax int32 [N])."""
+def _forward(x, thresholds, layers, n_classes, scores, argmax, workspace, stream, want_scores,
+             events):
     n, d = x.shape
     b = thresholds.shape[1]
     dev = x.device
@@ -214,21 +211,47 @@ def bitlogic_forward(x: torch.Tensor, thresholds: torch.Tensor,
     lib = load_library()
     need = int(lib.bitlogic_forward_workspace_bytes(
         n, d, b, ctypes.cast(arr, ctypes.c_void_p), len(arr), n_classes))
-    if need == 0:
-        _check(lib.bitlogic_forward(_dev(x, "x", _U8), n, d, _dev(thresholds, "thresholds", _U8),
-                                    b, ctypes.cast(arr, ctypes.c_void_p), len(arr), n_classes,
-                                    None, None, None, 0, _stream(stream, dev)))
     if scores is None and want_scores:
         scores = torch.empty((n, n_classes), dtype=torch.int32, device=dev)
     if argmax is None:
         argmax = torch.empty((n,), dtype=torch.int32, device=dev)
     ws_ptr, ws_bytes = _workspace(need, dev, workspace)
-    _check(lib.bitlogic_forward(
-        _dev(x, "x", _U8), n, d, _dev(thresholds, "thresholds", _U8), b,
-        ctypes.cast(arr, ctypes.c_void_p), len(arr), n_classes,
-        _dev(scores, "scores", _I32) if scores is not None else None,
-        _dev(argmax, "argmax", _I32), ws_ptr, ws_bytes, _stream(stream, dev)))
+    args = [_dev(x, "x", _U8), n, d, _dev(thresholds, "thresholds", _U8), b,
+            ctypes.cast(arr, ctypes.c_void_p), len(arr), n_classes,
+            _dev(scores, "scores", _I32) if scores is not None else None,
+            _dev(argmax, "argmax", _I32), ws_ptr, ws_bytes, _stream(stream, dev)]
+    if events is None:
+        _check(lib.bitlogic_forward(*args))
+    else:
+        handles = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
+        _check(lib.bitlogic_forward_timed(*args, ctypes.cast(handles, ctypes.c_void_p),
+                                          len(events)))
     return scores, argmax
+
+
+def bitlogic_forward(x: torch.Tensor, thresholds: torch.Tensor,
+                     layers: Sequence[Tuple[torch.Tensor, torch.Tensor]], n_classes: int,
+                     scores: Optional[torch.Tensor] = None,
+                     argmax: Optional[torch.Tensor] = None,
+                     workspace: Optional[torch.Tensor] = None, stream=None,
+                     want_scores: bool = True):
+    """Whole forward: pixels uint8 [N][d] -> (scores int32 [N][c], argmax int32 [N])."""
+    return _forward(x, thresholds, layers, n_classes, scores, argmax, workspace, stream,
+                    want_scores, None)
+
+
+def bitlogic_forward_timed(x: torch.Tensor, thresholds: torch.Tensor,
+                           layers: Sequence[Tuple[torch.Tensor, torch.Tensor]], n_classes: int,
+                           events: Sequence["torch.cuda.Event"],
+                           scores: Optional[torch.Tensor] = None,
+                           argmax: Optional[torch.Tensor] = None,
+                           workspace: Optional[torch.Tensor] = None, stream=None,
+                           want_scores: bool = True):
+    """bitlogic_forward with torch.cuda.Events recorded at the stage boundaries
+    (len(layers) + 3 events, created with enable_timing=True and recorded once
+    beforehand so that their HIP handles exist)."""
+    return _forward(x, thresholds, layers, n_classes, scores, argmax, workspace, stream,
+                    want_scores, list(events))
 
 
 @dataclass

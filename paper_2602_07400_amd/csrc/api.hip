@@ -94,8 +94,8 @@ int check_head(const uint64_t *bits, int32_t w, int64_t n, int32_t c, const int3
 }
 
 // bitlogic_forward keeps its encoded and intermediate bit tensors in the slab
-// layout [Wp / 4][rows][4] (Wp = W rounded up to whole 4-word slabs), which
-// gives the LUT-layer gathers a small per-XCD working set (see lut_layer.hip).
+// layout [Wp / S][rows][S] (S = kSlabWords, Wp = W rounded up to whole slabs),
+// which bounds the LUT-layer gathers' per-XCD working set (see lut_layer.hip).
 struct ForwardPlan {
     int64_t W;
     int64_t n_slabs;
@@ -166,7 +166,8 @@ int bitlogic_encode(const uint8_t *x, int64_t n_samples, int32_t n_features,
     if (n_samples == 0)
         return ok();
     return hip_status(bl::launch_encode(x, n_samples, n_features, thresholds, n_thresholds,
-                                        bits_out, bl::kLayoutRowMajor, (hipStream_t)stream),
+                                        bits_out, bl::kLayoutRowMajor, words_of(n_samples),
+                                        (hipStream_t)stream),
                       "encode launch");
 }
 
@@ -225,11 +226,15 @@ size_t bitlogic_forward_workspace_bytes(int64_t n_samples, int32_t n_features,
     return fp.total;
 }
 
-int bitlogic_forward(const uint8_t *x, int64_t n_samples, int32_t n_features,
-                     const uint8_t *thresholds, int32_t n_thresholds,
-                     const bitlogic_layer *layers, int32_t n_layers, int32_t n_classes,
-                     int32_t *scores, int32_t *argmax, void *workspace, size_t workspace_bytes,
-                     void *stream)
+}  // extern "C"
+
+namespace {
+
+int forward_impl(const uint8_t *x, int64_t n_samples, int32_t n_features,
+                 const uint8_t *thresholds, int32_t n_thresholds, const bitlogic_layer *layers,
+                 int32_t n_layers, int32_t n_classes, int32_t *scores, int32_t *argmax,
+                 void *workspace, size_t workspace_bytes, void *stream,
+                 void *const *events, int32_t n_events)
 {
     if (!x || !thresholds || (!scores && !argmax))
         return fail(BITLOGIC_ERR_NULL, "forward: NULL pixels/thresholds or both outputs NULL");
@@ -246,16 +251,31 @@ int bitlogic_forward(const uint8_t *x, int64_t n_samples, int32_t n_features,
         return fail(BITLOGIC_ERR_ALIGN, "forward: workspace not 256-byte aligned");
     if ((scores && !aligned(scores, 4)) || (argmax && !aligned(argmax, 4)))
         return fail(BITLOGIC_ERR_ALIGN, "forward: misaligned output");
+    if (events) {
+        if (n_events != n_layers + 3)
+            return fail(BITLOGIC_ERR_SHAPE, "forward_timed: need %d events, got %d",
+                        n_layers + 3, n_events);
+        for (int32_t i = 0; i < n_events; ++i)
+            if (!events[i])
+                return fail(BITLOGIC_ERR_NULL, "forward_timed: event %d is NULL", i);
+    }
     if (n_samples == 0)
         return ok();
 
     hipStream_t s = (hipStream_t)stream;
+    auto mark = [&](int i) -> hipError_t {
+        return events ? hipEventRecord((hipEvent_t)events[i], s) : hipSuccess;
+    };
     char *ws = static_cast<char *>(workspace);
     uint64_t *enc = reinterpret_cast<uint64_t *>(ws + fp.off_enc);
     uint64_t *act[2] = {reinterpret_cast<uint64_t *>(ws + fp.off_a),
                         reinterpret_cast<uint64_t *>(ws + fp.off_b)};
-    hipError_t e = bl::launch_encode(x, n_samples, n_features, thresholds, n_thresholds, enc,
-                                     bl::kLayoutSlab, s);
+    hipError_t e = mark(0);
+    if (e == hipSuccess)
+        e = bl::launch_encode(x, n_samples, n_features, thresholds, n_thresholds, enc,
+                              bl::kLayoutSlab, fp.n_slabs * bl::kSlabWords, s);
+    if (e == hipSuccess)
+        e = mark(1);
     if (e != hipSuccess)
         return hip_status(e, "forward: encode launch");
     const uint64_t *cur = enc;
@@ -264,6 +284,8 @@ int bitlogic_forward(const uint8_t *x, int64_t n_samples, int32_t n_features,
         uint64_t *dst = act[l & 1];
         e = bl::launch_lut_layer_slab(cur, w_in, fp.n_slabs, layers[l].conn, layers[l].tables,
                                       layers[l].w_out, layers[l].k, dst, s);
+        if (e == hipSuccess)
+            e = mark(2 + l);
         if (e != hipSuccess)
             return fail(BITLOGIC_ERR_HIP, "forward: layer %d launch: %s", l, hipGetErrorString(e));
         cur = dst;
@@ -271,7 +293,37 @@ int bitlogic_forward(const uint8_t *x, int64_t n_samples, int32_t n_features,
     }
     e = bl::launch_head(cur, w_in, n_samples, n_classes, scores, argmax, ws + fp.off_head,
                         fp.head, bl::kLayoutSlab, s);
+    if (e == hipSuccess)
+        e = mark(n_layers + 2);
     return hip_status(e, "forward: head launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+int bitlogic_forward(const uint8_t *x, int64_t n_samples, int32_t n_features,
+                     const uint8_t *thresholds, int32_t n_thresholds,
+                     const bitlogic_layer *layers, int32_t n_layers, int32_t n_classes,
+                     int32_t *scores, int32_t *argmax, void *workspace, size_t workspace_bytes,
+                     void *stream)
+{
+    return forward_impl(x, n_samples, n_features, thresholds, n_thresholds, layers, n_layers,
+                        n_classes, scores, argmax, workspace, workspace_bytes, stream, nullptr, 0);
+}
+
+int bitlogic_forward_timed(const uint8_t *x, int64_t n_samples, int32_t n_features,
+                           const uint8_t *thresholds, int32_t n_thresholds,
+                           const bitlogic_layer *layers, int32_t n_layers, int32_t n_classes,
+                           int32_t *scores, int32_t *argmax, void *workspace,
+                           size_t workspace_bytes, void *stream, void *const *events,
+                           int32_t n_events)
+{
+    if (!events)
+        return fail(BITLOGIC_ERR_NULL, "forward_timed: NULL event array");
+    return forward_impl(x, n_samples, n_features, thresholds, n_thresholds, layers, n_layers,
+                        n_classes, scores, argmax, workspace, workspace_bytes, stream, events,
+                        n_events);
 }
 
 const char *bitlogic_status_string(int status)

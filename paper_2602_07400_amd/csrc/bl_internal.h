@@ -10,7 +10,17 @@ namespace bl {
 
 constexpr int kWave = 64;       // CDNA wavefront width
 constexpr int kXcds = 8;        // MI355X: 8 accelerator dies, each with its own L2
-constexpr int kSlabWords = 4;   // words per row segment in the slab layout (256 samples)
+#ifndef BL_SLAB_WORDS
+#define BL_SLAB_WORDS 16
+#endif
+#ifndef BL_SLAB_LPN
+#define BL_SLAB_LPN 4
+#endif
+// Words per row segment in the slab layout (BL_SLAB_WORDS * 64 samples) and
+// lanes that share one node's segment in the slab LUT kernel.
+constexpr int kSlabWords = BL_SLAB_WORDS;
+constexpr int kSlabLanes = BL_SLAB_LPN;
+static_assert(kSlabWords % kSlabLanes == 0, "each lane takes whole words");
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -33,9 +43,12 @@ __device__ __forceinline__ int local_of(int bid) { return bid / kXcds; }
 
 // ---- launchers (each returns the hipError_t of its launch) ----
 
+// Encoder into either layout; W_cols = columns (words) to write: W for the
+// row-major layout, W rounded up to whole slabs for the slab layout (columns
+// past the batch get zero bits).
 hipError_t launch_encode(const uint8_t *x, int64_t n, int32_t d,
                          const uint8_t *thresholds, int32_t b, uint64_t *out, int layout,
-                         hipStream_t stream);
+                         int64_t W_cols, hipStream_t stream);
 
 // Slab-layout LUT layer over n_slabs slabs (bitlogic_forward's intermediates).
 hipError_t launch_lut_layer_slab(const uint64_t *in, int32_t w_in, int64_t n_slabs,

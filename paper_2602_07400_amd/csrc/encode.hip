@@ -8,20 +8,24 @@
 //
 // k_encode_t (b <= 8, the hot path).  A block first fills an LDS code table
 // code[f][v] = sum_t (v > theta[f][t]) << t for its tile of features and every
-// pixel value v, then reuses it for many slabs of 256 samples.  Per slab the
-// 256 x FT pixel tile is staged in LDS; each lane assembles, for a group of
-// floor(64/b) features, the 64-bit row of its sample's wires (one table read
-// and one shift-or per feature), and a 64x64 bit transpose across the wave
+// pixel value v, then reuses it for several tiles of 16 columns (1024
+// samples); each wave packs 4 of the 16 columns, one at a time.  A lane loads
+// its own sample's FT feature bytes (the next column's bytes are in flight
+// while the current one is packed) and assembles, for a group of floor(64/b)
+// features, the 64-bit row of its sample's wires (one table read and one
+// shift-or per feature), and a 64x64 bit transpose across the wave
 // (v_permlane32_swap for the 32-lane halves, then five ds_swizzle xor stages,
 // each a rotate (v_alignbit) and a bit-field merge (v_bfi) per register) turns
 // rows of samples into packed words of wires: lane p ends with wire p's word.
+// The words of a 16-column tile are collected in LDS and written as whole
+// 128-byte row segments.
 //
 // k_encode_ballot (any b <= 64).  Each comparison is a wave64 ballot, i.e. the
 // packed word of one wire; v_writelane collects 64 such words into one lane
 // each before they are stored.
 //
 // Both write either the row-major layout [wires][W] of bitlogic_encode or the
-// slab layout [W/4][wires][4] of bitlogic_forward's intermediates.
+// slab layout [Wp/S][wires][S] of bitlogic_forward's intermediates.
 #include "bl_internal.h"
 
 namespace bl {
@@ -77,26 +81,60 @@ struct EncGeom {
     static constexpr int kWPG = kFPG * B;                // wires per group (<= 64)
     static constexpr int kG = (B <= 2) ? 1 : (B == 4) ? 2 : (B == 5) ? 3 : 4;
     static constexpr int kFT = kFPG * kG;                // features per tile
-    static constexpr int kRowB = ((kFT / 4) % 2 == 1) ? kFT : kFT + 4;  // odd dword stride
+    static constexpr int kDw = kFT / 4;                  // pixel dwords per sample
     static_assert(kFT % 4 == 0, "feature tile must be whole dwords");
 };
+
+constexpr int kEncCols = 16;     // columns per output tile: 128-byte row segments
+constexpr int kOtRow = kEncCols + 1;   // LDS words per tile row (odd: no bank conflicts)
+constexpr int kColsPerWave = kEncCols / (kThreads / kWave);
+
+// This lane's kDw pixel dwords (features f0 .. f0 + 4*kDw - 1 of sample s);
+// zero past the batch or past the last feature.
+template <int kDw>
+__device__ __forceinline__ void load_pixels(const uint8_t *__restrict__ x, int64_t s, int64_t n,
+                                            int32_t d, int f0, int nf, int aligned4,
+                                            uint32_t (&px)[kDw])
+{
+    const uint8_t *row = x + s * d + f0;
+    if (s < n && aligned4) {
+#pragma unroll
+        for (int q = 0; q < kDw; ++q)
+            px[q] = (4 * q < nf) ? reinterpret_cast<const uint32_t *>(row)[q] : 0u;
+    } else if (s < n) {
+#pragma unroll
+        for (int q = 0; q < kDw; ++q) {
+            uint32_t v = 0;
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (4 * q + u < nf)
+                    v |= (uint32_t)row[4 * q + u] << (8 * u);
+            px[q] = v;
+        }
+    } else {
+#pragma unroll
+        for (int q = 0; q < kDw; ++q)
+            px[q] = 0;
+    }
+}
 
 template <int B, int LAYOUT>
 __global__ __launch_bounds__(kThreads) void k_encode_t(
     const uint8_t *__restrict__ x, int64_t n, int32_t d, const uint8_t *__restrict__ th,
-    uint64_t *__restrict__ out, int64_t W, int32_t n_ftiles, int32_t slabs_per_block,
-    int64_t n_slabs, int64_t n_sgroups, int aligned4)
+    uint64_t *__restrict__ out, int64_t W, int64_t W_cols, int32_t n_ftiles,
+    int32_t tiles_per_block, int64_t n_tiles, int64_t n_tgroups, int aligned4)
 {
     using G = EncGeom<B>;
+    constexpr int kWires = G::kG * G::kWPG;              // wire rows of one output tile
     __shared__ uint8_t lut[G::kFT * 256];
-    __shared__ uint8_t xs[4 * kWave * G::kRowB];
     __shared__ uint8_t ths[G::kFT * B];
+    __shared__ uint64_t otile[kWires * kOtRow];
 
     const int bid = blockIdx.x;
     const int64_t loc = local_of(bid);
-    const int64_t sg = (int64_t)xcd_of(bid) + (int64_t)kXcds * (loc / n_ftiles);
+    const int64_t tg = (int64_t)xcd_of(bid) + (int64_t)kXcds * (loc / n_ftiles);
     const int ft = (int)(loc % n_ftiles);
-    if (sg >= n_sgroups)
+    if (tg >= n_tgroups)
         return;
     const int f0 = ft * G::kFT;
     const int nf = min(G::kFT, d - f0);
@@ -119,6 +157,7 @@ __global__ __launch_bounds__(kThreads) void k_encode_t(
         }
         lut[q] = (uint8_t)code;
     }
+    __syncthreads();
 
     // per-lane constants of the transpose stages
     uint32_t amt[5], msk[5];
@@ -133,57 +172,75 @@ __global__ __launch_bounds__(kThreads) void k_encode_t(
         }
     }
 
-    const int64_t slab0 = sg * slabs_per_block;
-    const int64_t slab1 = min(slab0 + slabs_per_block, n_slabs);
-    for (int64_t slab = slab0; slab < slab1; ++slab) {
-        __syncthreads();     // table ready / previous tile consumed
-        const int64_t s0 = slab * 4 * kWave;
-        if (aligned4) {
-            constexpr int kDw = G::kFT / 4;
-            for (int q = threadIdx.x; q < 4 * kWave * kDw; q += kThreads) {
-                const int r = q / kDw, dw = q % kDw;
-                const int64_t s = s0 + r;
-                uint32_t v = 0;
-                if (s < n && 4 * dw < nf)
-                    v = *reinterpret_cast<const uint32_t *>(x + s * d + f0 + 4 * dw);
-                *reinterpret_cast<uint32_t *>(&xs[r * G::kRowB + 4 * dw]) = v;
+    const int64_t t0 = tg * tiles_per_block;
+    const int64_t t1 = min(t0 + tiles_per_block, n_tiles);
+    // this wave's columns: kColsPerWave consecutive columns of every tile
+    uint32_t px[G::kDw];
+    load_pixels<G::kDw>(x, (t0 * kEncCols + wave * kColsPerWave) * kWave + lane, n, d, f0, nf,
+                        aligned4, px);
+    for (int64_t tile = t0; tile < t1; ++tile) {
+        for (int cw = 0; cw < kColsPerWave; ++cw) {
+            const int col = wave * kColsPerWave + cw;      // column inside the tile
+            // prefetch the next column's pixels while this one is packed
+            uint32_t nx[G::kDw];
+            const bool more = cw + 1 < kColsPerWave || tile + 1 < t1;
+            if (more) {
+                const int64_t ncol = (cw + 1 < kColsPerWave) ? tile * kEncCols + col + 1
+                                                             : (tile + 1) * kEncCols + wave * kColsPerWave;
+                load_pixels<G::kDw>(x, ncol * kWave + lane, n, d, f0, nf, aligned4, nx);
             }
-        } else {
-            for (int q = threadIdx.x; q < 4 * kWave * G::kFT; q += kThreads) {
-                const int r = q / G::kFT, f = q % G::kFT;
-                const int64_t s = s0 + r;
-                xs[r * G::kRowB + f] = (s < n && f < nf) ? x[s * d + f0 + f] : 0;
+#pragma unroll
+            for (int gi = 0; gi < G::kG; ++gi) {
+                uint32_t lo = 0, hi = 0;
+#pragma unroll
+                for (int fl = 0; fl < G::kFPG; ++fl) {
+                    const int f = gi * G::kFPG + fl;
+                    const uint32_t byte = (px[f / 4] >> (8 * (f % 4))) & 0xFFu;
+                    const uint32_t code = lut[f * 256 + byte];
+                    const int pos = fl * B;
+                    if (pos + B <= 32) {
+                        lo |= code << pos;
+                    } else if (pos >= 32) {
+                        hi |= code << (pos - 32);
+                    } else {
+                        lo |= code << pos;
+                        hi |= code >> (32 - pos);
+                    }
+                }
+                transpose64(lo, hi, amt, msk);
+                if (lane < G::kWPG)
+                    otile[(gi * G::kWPG + lane) * kOtRow + col] = ((uint64_t)hi << 32) | lo;
+            }
+            if (more) {
+#pragma unroll
+                for (int q = 0; q < G::kDw; ++q)
+                    px[q] = nx[q];
             }
         }
         __syncthreads();
-
-        const int64_t wb = slab * 4 + wave;
-        const bool col_ok = (LAYOUT == kLayoutSlab) || wb < W;
-        const uint8_t *xrow = &xs[(wave * kWave + lane) * G::kRowB];
-#pragma unroll
-        for (int gi = 0; gi < G::kG; ++gi) {
-            uint32_t lo = 0, hi = 0;
-#pragma unroll
-            for (int fl = 0; fl < G::kFPG; ++fl) {
-                const int f = gi * G::kFPG + fl;
-                const uint32_t code = lut[f * 256 + xrow[f]];
-                const int pos = fl * B;
-                if (pos + B <= 32) {
-                    lo |= code << pos;
-                } else if (pos >= 32) {
-                    hi |= code << (pos - 32);
-                } else {
-                    lo |= code << pos;
-                    hi |= code >> (32 - pos);
-                }
-            }
-            transpose64(lo, hi, amt, msk);
-            const int fg = gi * G::kFPG;              // first feature of the group in the tile
-            if (col_ok && lane < G::kWPG && fg + lane / B < nf) {
-                const int64_t wire = (int64_t)(f0 + fg) * B + lane;
-                out[out_index<LAYOUT>(wire, wb, W, D0)] = ((uint64_t)hi << 32) | lo;
+        // write the tile: each wire's 16 words are one contiguous row segment
+        const int64_t wb0 = tile * kEncCols;
+        for (int e = threadIdx.x; e < kWires * (kEncCols / 2); e += kThreads) {
+            const int r = e / (kEncCols / 2);              // tile wire row
+            const int c2 = 2 * (e % (kEncCols / 2));       // even column
+            const int gi = r / G::kWPG, p = r % G::kWPG;
+            const int fg = gi * G::kFPG + p / B;           // feature of this wire in the tile
+            const int64_t wb = wb0 + c2;
+            if (fg >= nf || wb >= W_cols)
+                continue;
+            const int64_t wire = (int64_t)(f0 + gi * G::kFPG) * B + p;
+            const uint64_t w0 = otile[r * kOtRow + c2], w1 = otile[r * kOtRow + c2 + 1];
+            uint64_t *q = out + out_index<LAYOUT>(wire, wb, W, D0);
+            if (wb + 1 < W_cols && (LAYOUT == kLayoutSlab || ((uintptr_t)q % 16) == 0)) {
+                *reinterpret_cast<u32x4 *>(q) =
+                    u32x4{(uint32_t)w0, (uint32_t)(w0 >> 32), (uint32_t)w1, (uint32_t)(w1 >> 32)};
+            } else {
+                q[0] = w0;
+                if (wb + 1 < W_cols)
+                    out[out_index<LAYOUT>(wire, wb + 1, W, D0)] = w1;
             }
         }
+        __syncthreads();       // tile written before the next one reuses it
     }
 }
 
@@ -277,33 +334,32 @@ __global__ __launch_bounds__(kThreads) void k_encode_ballot(
 
 template <int B, int LAYOUT>
 hipError_t launch_t(const uint8_t *x, int64_t n, int32_t d, const uint8_t *th, uint64_t *out,
-                    hipStream_t stream)
+                    int64_t W_cols, hipStream_t stream)
 {
     using G = EncGeom<B>;
     const int64_t W = (n + 63) / 64;
-    const int64_t n_slabs = (W + 3) / 4;
+    const int64_t n_tiles = (W_cols + kEncCols - 1) / kEncCols;
     const int32_t n_ftiles = (d + G::kFT - 1) / G::kFT;
-    // enough blocks to fill the chip; at most 32 slabs reuse one code table
-    int64_t spb = n_slabs * n_ftiles / 2048;
-    spb = spb < 1 ? 1 : (spb > 32 ? 32 : spb);
-    const int64_t n_sg = (n_slabs + spb - 1) / spb;
-    const int64_t n_sg_pad = (n_sg + kXcds - 1) / kXcds * kXcds;
-    const int64_t blocks = n_sg_pad * n_ftiles;
+    // enough blocks to fill the chip; at most 8 column tiles reuse one code table
+    int64_t tpb = n_tiles * n_ftiles / 2048;
+    tpb = tpb < 1 ? 1 : (tpb > 8 ? 8 : tpb);
+    const int64_t n_tg = (n_tiles + tpb - 1) / tpb;
+    const int64_t n_tg_pad = (n_tg + kXcds - 1) / kXcds * kXcds;
+    const int64_t blocks = n_tg_pad * n_ftiles;
     if (blocks > 0x7fffffff)
         return hipErrorInvalidConfiguration;
     const int aligned4 = (d % 4 == 0) && ((uintptr_t)x % 4 == 0);
     hipLaunchKernelGGL((k_encode_t<B, LAYOUT>), dim3((unsigned)blocks), dim3(kThreads), 0, stream,
-                       x, n, d, th, out, W, n_ftiles, (int32_t)spb, n_slabs, n_sg, aligned4);
+                       x, n, d, th, out, W, W_cols, n_ftiles, (int32_t)tpb, n_tiles, n_tg,
+                       aligned4);
     return hipGetLastError();
 }
 
 template <int LAYOUT>
 hipError_t launch_ballot(const uint8_t *x, int64_t n, int32_t d, const uint8_t *th, int32_t b,
-                         uint64_t *out, hipStream_t stream)
+                         uint64_t *out, int64_t W_cols, hipStream_t stream)
 {
     const int64_t W = (n + 63) / 64;
-    // the slab layout has whole slabs of 4 columns (padding columns are zero)
-    const int64_t W_cols = (LAYOUT == kLayoutSlab) ? (W + 3) / 4 * 4 : W;
     const int32_t n_ftiles = (d + kBFeat - 1) / kBFeat;
     const int64_t n_cg = (W_cols + kBCols - 1) / kBCols;
     const int64_t n_cg_pad = (n_cg + kXcds - 1) / kXcds * kXcds;
@@ -323,29 +379,30 @@ hipError_t launch_ballot(const uint8_t *x, int64_t n, int32_t d, const uint8_t *
 
 template <int LAYOUT>
 hipError_t launch_layout(const uint8_t *x, int64_t n, int32_t d, const uint8_t *th, int32_t b,
-                         uint64_t *out, hipStream_t stream)
+                         uint64_t *out, int64_t W_cols, hipStream_t stream)
 {
     switch (b) {
-    case 1: return launch_t<1, LAYOUT>(x, n, d, th, out, stream);
-    case 2: return launch_t<2, LAYOUT>(x, n, d, th, out, stream);
-    case 3: return launch_t<3, LAYOUT>(x, n, d, th, out, stream);
-    case 4: return launch_t<4, LAYOUT>(x, n, d, th, out, stream);
-    case 5: return launch_t<5, LAYOUT>(x, n, d, th, out, stream);
-    case 6: return launch_t<6, LAYOUT>(x, n, d, th, out, stream);
-    case 7: return launch_t<7, LAYOUT>(x, n, d, th, out, stream);
-    case 8: return launch_t<8, LAYOUT>(x, n, d, th, out, stream);
-    default: return launch_ballot<LAYOUT>(x, n, d, th, b, out, stream);
+    case 1: return launch_t<1, LAYOUT>(x, n, d, th, out, W_cols, stream);
+    case 2: return launch_t<2, LAYOUT>(x, n, d, th, out, W_cols, stream);
+    case 3: return launch_t<3, LAYOUT>(x, n, d, th, out, W_cols, stream);
+    case 4: return launch_t<4, LAYOUT>(x, n, d, th, out, W_cols, stream);
+    case 5: return launch_t<5, LAYOUT>(x, n, d, th, out, W_cols, stream);
+    case 6: return launch_t<6, LAYOUT>(x, n, d, th, out, W_cols, stream);
+    case 7: return launch_t<7, LAYOUT>(x, n, d, th, out, W_cols, stream);
+    case 8: return launch_t<8, LAYOUT>(x, n, d, th, out, W_cols, stream);
+    default: return launch_ballot<LAYOUT>(x, n, d, th, b, out, W_cols, stream);
     }
 }
 
 }  // namespace
 
 hipError_t launch_encode(const uint8_t *x, int64_t n, int32_t d, const uint8_t *thresholds,
-                         int32_t b, uint64_t *out, int layout, hipStream_t stream)
+                         int32_t b, uint64_t *out, int layout, int64_t W_cols,
+                         hipStream_t stream)
 {
     if (layout == kLayoutSlab)
-        return launch_layout<kLayoutSlab>(x, n, d, thresholds, b, out, stream);
-    return launch_layout<kLayoutRowMajor>(x, n, d, thresholds, b, out, stream);
+        return launch_layout<kLayoutSlab>(x, n, d, thresholds, b, out, W_cols, stream);
+    return launch_layout<kLayoutRowMajor>(x, n, d, thresholds, b, out, W_cols, stream);
 }
 
 }  // namespace bl

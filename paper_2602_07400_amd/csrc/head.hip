@@ -109,40 +109,65 @@ __global__ __launch_bounds__(kThreads) void k_head_planes(
 }
 
 constexpr int kFinishClasses = 128;   // at most this many classes per LDS score tile
+constexpr int kFinishPlaneWords = 2048; // plane words of a column staged in LDS at once
 
-// One wave per 64-sample column: assemble each class score from its bit
-// planes (wave-uniform scalar loads), track the argmax, and stage the
-// 64 x classes score tile in LDS so it is written as one contiguous block.
+// One wave per 64-sample column.  The column's bit planes (contiguous,
+// [class][split][plane]) are staged in LDS with coalesced loads; each lane
+// then assembles its sample's class scores from broadcast LDS reads, tracks
+// the argmax, and the 64 x classes score tile is written from LDS as one
+// contiguous block.
 template <int P>
 __global__ __launch_bounds__(kWave) void k_head_finish(
     const uint64_t *__restrict__ planes, int64_t W, int64_t n, int32_t c, int32_t S,
     int32_t *__restrict__ scores, int32_t *__restrict__ argmax)
 {
     extern __shared__ int32_t tile[];     // [64][min(c, kFinishClasses)]
+    __shared__ uint64_t pl_lds[kFinishPlaneWords];
     const int lane = threadIdx.x;
     const int64_t col = blockIdx.x;
     if (col >= W)
         return;
     const int64_t s = col * kWave + lane;
     const uint64_t *pc = planes + col * (int64_t)c * S * P;
+    const int per_class = S * P;
+    // classes whose planes fit the LDS staging buffer at once
+    const int cls_stage = max(1, kFinishPlaneWords / per_class);
     int32_t best = -1, besti = 0;
     for (int c0 = 0; c0 < c; c0 += kFinishClasses) {
         const int cn = min(kFinishClasses, c - c0);
-        for (int ii = 0; ii < cn; ++ii) {
-            const int i = c0 + ii;
-            int32_t cnt = 0;
-            for (int q = 0; q < S; ++q) {
-                const uint64_t *pl = pc + ((int64_t)i * S + q) * P;
-                int32_t part = 0;
-#pragma unroll
-                for (int p = 0; p < P; ++p)
-                    part |= (int32_t)((pl[p] >> lane) & 1u) << p;
-                cnt += part;
+        for (int ii0 = 0; ii0 < cn; ii0 += cls_stage) {
+            const int cs = min(cls_stage, cn - ii0);
+            const bool staged = per_class <= kFinishPlaneWords;
+            if (staged) {
+                __syncthreads();
+                const uint64_t *src = pc + (int64_t)(c0 + ii0) * per_class;
+                for (int e = lane; e < cs * per_class; e += kWave)
+                    pl_lds[e] = src[e];
+                __syncthreads();
             }
-            tile[lane * cn + ii] = cnt;
-            if (cnt > best) {
-                best = cnt;
-                besti = i;
+            for (int ii = ii0; ii < ii0 + cs; ++ii) {
+                const int i = c0 + ii;
+                int32_t cnt = 0;
+                for (int q = 0; q < S; ++q) {
+                    int32_t part = 0;
+                    if (staged) {
+                        const uint64_t *pl = &pl_lds[((ii - ii0) * S + q) * P];
+#pragma unroll
+                        for (int p = 0; p < P; ++p)
+                            part |= (int32_t)((pl[p] >> lane) & 1u) << p;
+                    } else {
+                        const uint64_t *pl = pc + ((int64_t)i * S + q) * P;
+#pragma unroll
+                        for (int p = 0; p < P; ++p)
+                            part |= (int32_t)((pl[p] >> lane) & 1u) << p;
+                    }
+                    cnt += part;
+                }
+                tile[lane * cn + ii] = cnt;
+                if (cnt > best) {
+                    best = cnt;
+                    besti = i;
+                }
             }
         }
         __syncthreads();

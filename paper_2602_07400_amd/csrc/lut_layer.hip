@@ -170,22 +170,123 @@ __global__ __launch_bounds__(kThreads) void k_lut_layer(
 
 // ---------------------------------------------------------------------------
 // Slab layout (used for the intermediate tensors of bitlogic_forward): the
-// batch is cut into slabs of kSlabWords words (256 samples); within a slab the
-// rows are contiguous, 32 bytes each:
-//     word (row r, column wb) at ((wb / kSlabWords) * rows + r) * kSlabWords + wb % kSlabWords
-// One lane evaluates one node on one slab: it gathers K 32-byte row segments
-// (two 16-byte loads each) and writes one 32-byte segment, so a wave's store
-// is 2 KB contiguous.  The per-XCD working set of a slab is w_in * 32 bytes
-// (2 MB for a 64000-wide input), small enough for the XCD's 4 MB L2, and every
-// line fetched is fully used.  Output stores are non-temporal so the output
-// stream does not evict the input slab.
-template <int K, int NB>
-__global__ __launch_bounds__(kThreads) void k_lut_slab(
+// batch is cut into slabs of S = kSlabWords words; within a slab the rows are
+// contiguous, S * 8 bytes each:
+//     word (row r, column wb) at ((wb / S) * rows + r) * S + wb % S
+// The LPN lanes of a node split its S words (R = S / LPN words each, loaded
+// as 16-byte pieces); a block handles one slab and NB nodes, so a wave's
+// stores are contiguous.  The per-XCD working set of a slab is w_in * S * 8
+// bytes.  Output stores are non-temporal so the output stream does not evict
+// the input slab from L2.
+#ifndef BL_LUT_PREFETCH
+#define BL_LUT_PREFETCH 0
+#endif
+#ifndef BL_NT_STORE
+#define BL_NT_STORE 1
+#endif
+
+template <int K, int R>
+__device__ __forceinline__ void gather(const uint64_t *src, const int32_t *c, int S,
+                                       uint32_t (&xv)[2 * R][K])
+{
+#pragma unroll
+    for (int i = 0; i < K; ++i) {
+        const uint64_t *p = src + (int64_t)c[i] * S;
+        if constexpr (R == 1) {
+            const uint2 a = *reinterpret_cast<const uint2 *>(p);
+            xv[0][i] = a.x;
+            xv[1][i] = a.y;
+        } else {
+#pragma unroll
+            for (int r = 0; r < R; r += 2) {
+                const u32x4 a = reinterpret_cast<const u32x4 *>(p)[r / 2];
+                xv[2 * r + 0][i] = a.x;
+                xv[2 * r + 1][i] = a.y;
+                xv[2 * r + 2][i] = a.z;
+                xv[2 * r + 3][i] = a.w;
+            }
+        }
+    }
+}
+
+// Fold a K-input subtree whose 2^K leaf masks come from bits [base, base + 2^K)
+// of the table word t (a 32-bit half of the table).
+template <int K, int H>
+__device__ __forceinline__ void subtree(uint32_t t, const uint32_t (&xv)[H][6], uint32_t (&o)[H])
+{
+    uint32_t m[1 << K];
+#pragma unroll
+    for (int a = 0; a < (1 << K); ++a)
+        m[a] = 0u - ((t >> a) & 1u);
+#pragma unroll
+    for (int h = 0; h < H; ++h) {
+        uint32_t sel[K];
+#pragma unroll
+        for (int i = 0; i < K; ++i)
+            sel[i] = xv[h][i];
+        o[h] = mux_tree<K>(sel, m);
+    }
+}
+
+template <int K, int R>
+__device__ __forceinline__ void eval_store(uint64_t T, const uint32_t (&xv)[2 * R][K],
+                                           uint64_t *q, bool ok)
+{
+    uint32_t o[2 * R];
+    if constexpr (K == 6) {
+        // Shannon split on x5: the two 5-input halves of the table are folded
+        // one after the other, so only 32 masks are live at a time
+        uint32_t lo[2 * R], hi[2 * R];
+        subtree<5, 2 * R>((uint32_t)T, xv, lo);
+        __builtin_amdgcn_sched_barrier(0);   // keep the two halves' masks apart
+        subtree<5, 2 * R>((uint32_t)(T >> 32), xv, hi);
+#pragma unroll
+        for (int h = 0; h < 2 * R; ++h)
+            o[h] = (xv[h][5] & hi[h]) | (~xv[h][5] & lo[h]);
+    } else {
+        const uint32_t t_lo = (uint32_t)T, t_hi = (uint32_t)(T >> 32);
+        uint32_t m[1 << K];
+#pragma unroll
+        for (int a = 0; a < (1 << K); ++a)
+            m[a] = 0u - (((a < 32 ? t_lo : t_hi) >> (a & 31)) & 1u);
+#pragma unroll
+        for (int h = 0; h < 2 * R; ++h)
+            o[h] = mux_tree<K>(xv[h], m);
+    }
+    if (ok) {
+        if constexpr (R == 1) {
+            const uint64_t v = (uint64_t)o[1] << 32 | o[0];
+            if (BL_NT_STORE)
+                __builtin_nontemporal_store(v, q);
+            else
+                *q = v;
+        } else {
+#pragma unroll
+            for (int r = 0; r < R; r += 2) {
+                const u32x4 v = u32x4{o[2 * r], o[2 * r + 1], o[2 * r + 2], o[2 * r + 3]};
+                if (BL_NT_STORE)
+                    __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(q) + r / 2);
+                else
+                    reinterpret_cast<u32x4 *>(q)[r / 2] = v;
+            }
+        }
+    }
+}
+
+#ifndef BL_LUT_MINWAVES
+#define BL_LUT_MINWAVES 1
+#endif
+
+template <int K, int S, int LPN, int NB>
+__global__ __launch_bounds__(kThreads, BL_LUT_MINWAVES) void k_lut_slab(
     const uint64_t *__restrict__ in, int32_t w_in, const int32_t *__restrict__ conn,
     const uint64_t *__restrict__ tables, int32_t w_out, uint64_t *__restrict__ out,
     int32_t n_nblk, int32_t n_slabs)
 {
-    static_assert(NB % kThreads == 0, "node block must be whole passes");
+    constexpr int R = S / LPN;                         // words per lane
+    constexpr int kPassNodes = kThreads / LPN;
+    static_assert(NB % kPassNodes == 0, "node block must be whole passes");
+    static_assert(R == 1 || R % 2 == 0, "R words are loaded as 8- or 16-byte pieces");
     __shared__ int32_t s_conn[NB * K];
     __shared__ uint64_t s_tab[NB];
 
@@ -204,36 +305,36 @@ __global__ __launch_bounds__(kThreads) void k_lut_slab(
         s_tab[q] = (q < nodes) ? tables[node0 + q] : 0;
     __syncthreads();
 
-    const u32x4 *src = reinterpret_cast<const u32x4 *>(in + (int64_t)slab * w_in * kSlabWords);
-    u32x4 *dst = reinterpret_cast<u32x4 *>(out + ((int64_t)slab * w_out + node0) * kSlabWords);
+    const int sub = threadIdx.x % LPN;
+    const int lnode = threadIdx.x / LPN;
+    const uint64_t *src = in + (int64_t)slab * w_in * S + sub * R;
+    uint64_t *dst = out + ((int64_t)slab * w_out + node0) * S + sub * R;
+    const int npass = (nodes + kPassNodes - 1) / kPassNodes;
 
+    if constexpr (BL_LUT_PREFETCH) {
+        // two register sets: the next pass's gathers are in flight while
+        // the current pass is evaluated
+        uint32_t xa[2 * R][K], xb[2 * R][K];
+        gather<K, R>(src, &s_conn[lnode * K], S, xa);
 #pragma unroll 1
-    for (int pass = 0; pass < NB / kThreads; ++pass) {
-        if (pass * kThreads >= nodes)
-            break;
-        const int jl = pass * kThreads + threadIdx.x;
-        uint32_t xv[2 * kSlabWords][K];
-#pragma unroll
-        for (int i = 0; i < K; ++i) {
-            const u32x4 *p = src + 2 * s_conn[jl * K + i];
-            const u32x4 a = p[0], b = p[1];
-            xv[0][i] = a.x; xv[1][i] = a.y; xv[2][i] = a.z; xv[3][i] = a.w;
-            xv[4][i] = b.x; xv[5][i] = b.y; xv[6][i] = b.z; xv[7][i] = b.w;
+        for (int pass = 0; pass < npass; pass += 2) {
+            const int ja = pass * kPassNodes + lnode, jb = ja + kPassNodes;
+            if (pass + 1 < npass)
+                gather<K, R>(src, &s_conn[jb * K], S, xb);
+            eval_store<K, R>(s_tab[ja], xa, dst + (int64_t)ja * S, ja < nodes);
+            if (pass + 1 >= npass)
+                break;
+            if (pass + 2 < npass)
+                gather<K, R>(src, &s_conn[(jb + kPassNodes) * K], S, xa);
+            eval_store<K, R>(s_tab[jb], xb, dst + (int64_t)jb * S, jb < nodes);
         }
-        const uint64_t T = s_tab[jl];
-        const uint32_t t_lo = (uint32_t)T, t_hi = (uint32_t)(T >> 32);
-        uint32_t m[1 << K];
-#pragma unroll
-        for (int a = 0; a < (1 << K); ++a)
-            m[a] = 0u - (((a < 32 ? t_lo : t_hi) >> (a & 31)) & 1u);
-        uint32_t o[2 * kSlabWords];
-#pragma unroll
-        for (int h = 0; h < 2 * kSlabWords; ++h)
-            o[h] = mux_tree<K>(xv[h], m);
-        if (jl < nodes) {
-            u32x4 *q = dst + 2 * jl;
-            __builtin_nontemporal_store(u32x4{o[0], o[1], o[2], o[3]}, q);
-            __builtin_nontemporal_store(u32x4{o[4], o[5], o[6], o[7]}, q + 1);
+    } else {
+#pragma unroll 1
+        for (int pass = 0; pass < npass; ++pass) {
+            const int jl = pass * kPassNodes + lnode;
+            uint32_t xv[2 * R][K];
+            gather<K, R>(src, &s_conn[jl * K], S, xv);
+            eval_store<K, R>(s_tab[jl], xv, dst + (int64_t)jl * S, jl < nodes);
         }
     }
 }
@@ -250,8 +351,9 @@ hipError_t launch_slab_k(const uint64_t *in, int32_t w_in, int64_t n_slabs,
     const int64_t blocks = slabs_pad * n_nblk;
     if (blocks > 0x7fffffff)
         return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((k_lut_slab<K, kSlabNB>), dim3((unsigned)blocks), dim3(kThreads), 0,
-                       stream, in, w_in, conn, tables, w_out, out, n_nblk, (int32_t)n_slabs);
+    hipLaunchKernelGGL((k_lut_slab<K, kSlabWords, kSlabLanes, kSlabNB>), dim3((unsigned)blocks),
+                       dim3(kThreads), 0, stream, in, w_in, conn, tables, w_out, out, n_nblk,
+                       (int32_t)n_slabs);
     return hipGetLastError();
 }
 

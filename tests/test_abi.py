@@ -150,3 +150,14 @@ def test_model_checks_connection_range():
     conn = np.array([[0, 8]], np.int32)          # 8 >= w_in = 8
     with pytest.raises(ValueError, match="outside"):
         bl.BitlogicModel.from_numpy(th, [(conn, np.zeros(1, np.uint64))], 1, device="cpu")
+
+
+def test_forward_timed_validation(lib):
+    p, keep = _layers([(1000, 6), (1000, 6)])
+    need = lib.bitlogic_forward_workspace_bytes(4096, 784, 1, p, 2, 10)
+    ev = (ctypes.c_void_p * 5)(*([FAKE] * 5))
+    base = [FAKE, 4096, 784, FAKE, 1, p, 2, 10, FAKE, FAKE, FAKE * 16, need, None]
+    assert lib.bitlogic_forward_timed(*base, None, 5) == ENULL
+    assert lib.bitlogic_forward_timed(*base, ctypes.cast(ev, ctypes.c_void_p), 4) == ESHAPE
+    ev[3] = None
+    assert lib.bitlogic_forward_timed(*base, ctypes.cast(ev, ctypes.c_void_p), 5) == ENULL

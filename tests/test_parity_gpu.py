@@ -316,3 +316,18 @@ def test_forward_encoder_variants(n, d, b):
     s, p = m.forward(torch.from_numpy(x).to(DEV))
     rs, rp = oracle.forward(x, th, layers, 6)
     assert np.array_equal(s.cpu().numpy(), rs) and np.array_equal(p.cpu().numpy(), rp)
+
+
+def test_forward_timed_records_stage_events():
+    wl = make_workload("c3_cifar10", seed=5, n=3000)
+    model = bl.BitlogicModel.from_numpy(wl.thresholds, wl.layers, wl.n_classes, device=DEV)
+    x = torch.from_numpy(wl.x).to(DEV)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(wl.layers) + 3)]
+    for e in ev:
+        e.record()
+    s1, p1 = bl.bitlogic_forward_timed(x, model.thresholds, model.layers, model.n_classes, ev)
+    torch.cuda.synchronize()
+    times = [ev[i].elapsed_time(ev[i + 1]) for i in range(len(ev) - 1)]
+    assert all(t >= 0 for t in times) and sum(times) > 0
+    s2, p2 = model.forward(x)
+    assert torch.equal(s1, s2) and torch.equal(p1, p2)
