@@ -42,9 +42,13 @@ __device__ __forceinline__ int64_t out_index(int64_t wire, int64_t wb, int64_t W
         return wire * W + wb;
 }
 
+// (sel & one) | (~sel & zero) as a single v_bfi_b32 (left to itself the
+// compiler splits it into and/or with an extra inverted-mask register)
 __device__ __forceinline__ uint32_t bfi(uint32_t sel, uint32_t one, uint32_t zero)
 {
-    return (sel & one) | (~sel & zero);
+    uint32_t r;
+    asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(sel), "v"(one), "v"(zero));
+    return r;
 }
 
 // One block-swap stage of the 32x32 transpose inside each 32-lane half: lanes
@@ -90,14 +94,20 @@ constexpr int kOtRow = kEncCols + 1;   // LDS words per tile row (odd: no bank c
 constexpr int kColsPerWave = kEncCols / (kThreads / kWave);
 
 // This lane's kDw pixel dwords (features f0 .. f0 + 4*kDw - 1 of sample s);
-// zero past the batch or past the last feature.
+// zero past the batch or past the last feature.  `full` (wave-uniform): the
+// whole column is inside the batch, the tile holds kFT features and rows are
+// dword aligned, so the loads need no guards.
 template <int kDw>
 __device__ __forceinline__ void load_pixels(const uint8_t *__restrict__ x, int64_t s, int64_t n,
-                                            int32_t d, int f0, int nf, int aligned4,
+                                            int32_t d, int f0, int nf, int aligned4, bool full,
                                             uint32_t (&px)[kDw])
 {
     const uint8_t *row = x + s * d + f0;
-    if (s < n && aligned4) {
+    if (full) {
+#pragma unroll
+        for (int q = 0; q < kDw; ++q)
+            px[q] = reinterpret_cast<const uint32_t *>(row)[q];
+    } else if (s < n && aligned4) {
 #pragma unroll
         for (int q = 0; q < kDw; ++q)
             px[q] = (4 * q < nf) ? reinterpret_cast<const uint32_t *>(row)[q] : 0u;
@@ -175,9 +185,14 @@ __global__ __launch_bounds__(kThreads) void k_encode_t(
     const int64_t t0 = tg * tiles_per_block;
     const int64_t t1 = min(t0 + tiles_per_block, n_tiles);
     // this wave's columns: kColsPerWave consecutive columns of every tile
+    // columns whose 64 samples are all in the batch, in a full aligned tile
+    const bool tile_full = aligned4 && nf == G::kFT;
+    auto col_full = [&](int64_t gcol) { return tile_full && (gcol + 1) * kWave <= n; };
     uint32_t px[G::kDw];
-    load_pixels<G::kDw>(x, (t0 * kEncCols + wave * kColsPerWave) * kWave + lane, n, d, f0, nf,
-                        aligned4, px);
+    {
+        const int64_t gcol = t0 * kEncCols + wave * kColsPerWave;
+        load_pixels<G::kDw>(x, gcol * kWave + lane, n, d, f0, nf, aligned4, col_full(gcol), px);
+    }
     for (int64_t tile = t0; tile < t1; ++tile) {
         for (int cw = 0; cw < kColsPerWave; ++cw) {
             const int col = wave * kColsPerWave + cw;      // column inside the tile
@@ -187,7 +202,8 @@ __global__ __launch_bounds__(kThreads) void k_encode_t(
             if (more) {
                 const int64_t ncol = (cw + 1 < kColsPerWave) ? tile * kEncCols + col + 1
                                                              : (tile + 1) * kEncCols + wave * kColsPerWave;
-                load_pixels<G::kDw>(x, ncol * kWave + lane, n, d, f0, nf, aligned4, nx);
+                load_pixels<G::kDw>(x, ncol * kWave + lane, n, d, f0, nf, aligned4, col_full(ncol),
+                                    nx);
             }
 #pragma unroll
             for (int gi = 0; gi < G::kG; ++gi) {

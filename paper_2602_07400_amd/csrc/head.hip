@@ -11,10 +11,10 @@
 // (v_bitop3 full adders, ~2 ops per word per 32 samples), one lane per column
 // so every row load is a coalesced 512-byte segment.  Long groups are split
 // into row ranges so the launch fills the chip.  Stage 2 runs one lane per
-// sample: it reads the planes of its column (wave-uniform scalar loads),
-// assembles each class score bit by bit, sums the splits and tracks the
-// running argmax; the score tile of the column is staged in LDS and written
-// as one contiguous block.
+// sample and one block per column: its waves share the classes, assemble each
+// class score bit by bit from the column's planes (wave-uniform scalar loads)
+// and sum the splits into an LDS score tile, from which the argmax is taken
+// and the scores are written as one contiguous block.
 #include "bl_internal.h"
 
 namespace bl {
@@ -108,72 +108,53 @@ __global__ __launch_bounds__(kThreads) void k_head_planes(
     }
 }
 
-constexpr int kFinishClasses = 128;   // at most this many classes per LDS score tile
-constexpr int kFinishPlaneWords = 2048; // plane words of a column staged in LDS at once
+constexpr int kFinishClasses = 128;   // classes per LDS score tile
 
-// One wave per 64-sample column.  The column's bit planes (contiguous,
-// [class][split][plane]) are staged in LDS with coalesced loads; each lane
-// then assembles its sample's class scores from broadcast LDS reads, tracks
-// the argmax, and the 64 x classes score tile is written from LDS as one
-// contiguous block.
+// One block (4 waves) per 64-sample column, one lane per sample.  The waves
+// take classes round-robin; a class score is assembled bit by bit from the
+// column's planes (contiguous [class][split][plane], wave-uniform scalar
+// loads) and parked in an LDS tile [64][classes]; then every lane scans its
+// sample's row of the tile for the argmax (lowest index on ties) and the tile
+// is written to scores as one contiguous block.
 template <int P>
-__global__ __launch_bounds__(kWave) void k_head_finish(
+__global__ __launch_bounds__(kThreads) void k_head_finish(
     const uint64_t *__restrict__ planes, int64_t W, int64_t n, int32_t c, int32_t S,
     int32_t *__restrict__ scores, int32_t *__restrict__ argmax)
 {
     extern __shared__ int32_t tile[];     // [64][min(c, kFinishClasses)]
-    __shared__ uint64_t pl_lds[kFinishPlaneWords];
-    const int lane = threadIdx.x;
+    const int lane = threadIdx.x % kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int64_t col = blockIdx.x;
-    if (col >= W)
-        return;
-    const int64_t s = col * kWave + lane;
+    const int64_t s0 = col * kWave;
     const uint64_t *pc = planes + col * (int64_t)c * S * P;
-    const int per_class = S * P;
-    // classes whose planes fit the LDS staging buffer at once
-    const int cls_stage = max(1, kFinishPlaneWords / per_class);
     int32_t best = -1, besti = 0;
     for (int c0 = 0; c0 < c; c0 += kFinishClasses) {
         const int cn = min(kFinishClasses, c - c0);
-        for (int ii0 = 0; ii0 < cn; ii0 += cls_stage) {
-            const int cs = min(cls_stage, cn - ii0);
-            const bool staged = per_class <= kFinishPlaneWords;
-            if (staged) {
-                __syncthreads();
-                const uint64_t *src = pc + (int64_t)(c0 + ii0) * per_class;
-                for (int e = lane; e < cs * per_class; e += kWave)
-                    pl_lds[e] = src[e];
-                __syncthreads();
+        for (int ii = wave; ii < cn; ii += kWaves) {
+            const int i = c0 + ii;
+            int32_t cnt = 0;
+            for (int q = 0; q < S; ++q) {
+                const uint64_t *pl = pc + ((int64_t)i * S + q) * P;
+                int32_t part = 0;
+#pragma unroll
+                for (int p = 0; p < P; ++p)
+                    part |= (int32_t)((pl[p] >> lane) & 1u) << p;
+                cnt += part;
             }
-            for (int ii = ii0; ii < ii0 + cs; ++ii) {
-                const int i = c0 + ii;
-                int32_t cnt = 0;
-                for (int q = 0; q < S; ++q) {
-                    int32_t part = 0;
-                    if (staged) {
-                        const uint64_t *pl = &pl_lds[((ii - ii0) * S + q) * P];
-#pragma unroll
-                        for (int p = 0; p < P; ++p)
-                            part |= (int32_t)((pl[p] >> lane) & 1u) << p;
-                    } else {
-                        const uint64_t *pl = pc + ((int64_t)i * S + q) * P;
-#pragma unroll
-                        for (int p = 0; p < P; ++p)
-                            part |= (int32_t)((pl[p] >> lane) & 1u) << p;
-                    }
-                    cnt += part;
-                }
-                tile[lane * cn + ii] = cnt;
-                if (cnt > best) {
-                    best = cnt;
-                    besti = i;
+            tile[lane * cn + ii] = cnt;
+        }
+        __syncthreads();
+        if (wave == 0) {
+            for (int ii = 0; ii < cn; ++ii) {
+                const int32_t v = tile[lane * cn + ii];
+                if (v > best) {
+                    best = v;
+                    besti = c0 + ii;
                 }
             }
         }
-        __syncthreads();
         if (scores) {
-            const int64_t s0 = col * kWave;
-            for (int e = lane; e < kWave * cn; e += kWave) {
+            for (int e = threadIdx.x; e < kWave * cn; e += kThreads) {
                 const int64_t ss = s0 + e / cn;
                 if (ss < n)
                     scores[ss * c + c0 + e % cn] = tile[e];
@@ -181,8 +162,8 @@ __global__ __launch_bounds__(kWave) void k_head_finish(
         }
         __syncthreads();
     }
-    if (argmax && s < n)
-        argmax[s] = besti;
+    if (wave == 0 && argmax && s0 + lane < n)
+        argmax[s0 + lane] = besti;
 }
 
 template <int P>
@@ -208,7 +189,7 @@ hipError_t launch_p(const uint64_t *bits, int32_t w, int64_t n, int32_t c,
     if (e != hipSuccess)
         return e;
     const size_t lds = (size_t)kWave * (c < kFinishClasses ? c : kFinishClasses) * sizeof(int32_t);
-    hipLaunchKernelGGL(k_head_finish<P>, dim3((unsigned)W), dim3(kWave), lds, stream,
+    hipLaunchKernelGGL(k_head_finish<P>, dim3((unsigned)W), dim3(kThreads), lds, stream,
                        planes, W, n, c, plan.splits, scores, argmax);
     return hipGetLastError();
 }
