@@ -3,8 +3,9 @@
 // rejected call enqueues nothing (and needs no GPU to be rejected).
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 
-#include "../../include/bitlogic.h"
+#include "bitlogic.h"
 #include "bl_internal.h"
 
 namespace {
@@ -93,6 +94,14 @@ int check_head(const uint64_t *bits, int32_t w, int64_t n, int32_t c, const int3
     return BITLOGIC_OK;
 }
 
+// BITLOGIC_UNFUSED_HEAD=1 in the environment runs the last layer and the head
+// as separate kernels (for comparison; results are identical).
+bool fused_head_enabled()
+{
+    const char *e = getenv("BITLOGIC_UNFUSED_HEAD");
+    return !(e && e[0] == '1');
+}
+
 // bitlogic_forward keeps its encoded and intermediate bit tensors in the slab
 // layout [Wp / S][rows][S] (S = kSlabWords, Wp = W rounded up to whole slabs),
 // which bounds the LUT-layer gathers' per-XCD working set (see lut_layer.hip).
@@ -102,6 +111,7 @@ struct ForwardPlan {
     int32_t widest;
     size_t off_enc, off_a, off_b, off_head, total;
     bl::HeadPlan head;
+    bool fused;            // last layer + head in one kernel
 };
 
 int plan_forward(int64_t n, int32_t d, int32_t b, const bitlogic_layer *layers, int32_t L,
@@ -143,7 +153,10 @@ int plan_forward(int64_t n, int32_t d, int32_t b, const bitlogic_layer *layers, 
     const int64_t Wp = fp->n_slabs * bl::kSlabWords;
     const size_t enc = (size_t)d * b * Wp * sizeof(uint64_t);
     const size_t act = (size_t)widest * Wp * sizeof(uint64_t);
-    fp->head = bl::plan_head(w_last, n, c);
+    // the last layer and the head run fused when the group size allows it
+    const int32_t nb = bl::fused_head_nodes(w_last / c);
+    fp->fused = nb > 0 && fused_head_enabled();
+    fp->head = fp->fused ? bl::plan_fused_head(w_last, n, c, nb) : bl::plan_head(w_last, n, c);
     fp->off_enc = 0;
     fp->off_a = round_up(enc);
     fp->off_b = fp->off_a + round_up(act);
@@ -280,10 +293,17 @@ int forward_impl(const uint8_t *x, int64_t n_samples, int32_t n_features,
         return hip_status(e, "forward: encode launch");
     const uint64_t *cur = enc;
     int32_t w_in = n_features * n_thresholds;
+    uint64_t *planes = reinterpret_cast<uint64_t *>(ws + fp.off_head);
     for (int32_t l = 0; l < n_layers; ++l) {
+        const bool last_fused = fp.fused && l == n_layers - 1;
         uint64_t *dst = act[l & 1];
-        e = bl::launch_lut_layer_slab(cur, w_in, fp.n_slabs, layers[l].conn, layers[l].tables,
-                                      layers[l].w_out, layers[l].k, dst, s);
+        if (last_fused)
+            e = bl::launch_lut_slab_head(cur, w_in, fp.n_slabs, layers[l].conn, layers[l].tables,
+                                         layers[l].w_out, layers[l].k, n_classes, fp.W, planes,
+                                         fp.head.planes, s);
+        else
+            e = bl::launch_lut_layer_slab(cur, w_in, fp.n_slabs, layers[l].conn,
+                                          layers[l].tables, layers[l].w_out, layers[l].k, dst, s);
         if (e == hipSuccess)
             e = mark(2 + l);
         if (e != hipSuccess)
@@ -291,8 +311,11 @@ int forward_impl(const uint8_t *x, int64_t n_samples, int32_t n_features,
         cur = dst;
         w_in = layers[l].w_out;
     }
-    e = bl::launch_head(cur, w_in, n_samples, n_classes, scores, argmax, ws + fp.off_head,
-                        fp.head, bl::kLayoutSlab, s);
+    if (fp.fused)
+        e = bl::launch_head_finish(planes, n_samples, n_classes, scores, argmax, fp.head, s);
+    else
+        e = bl::launch_head(cur, w_in, n_samples, n_classes, scores, argmax, planes, fp.head,
+                            bl::kLayoutSlab, s);
     if (e == hipSuccess)
         e = mark(n_layers + 2);
     return hip_status(e, "forward: head launch");

@@ -60,6 +60,16 @@ hipError_t launch_lut_layer(const uint64_t *in, int32_t w_in, int64_t n_words,
                             int32_t w_out, int32_t k, uint64_t *out,
                             hipStream_t stream);
 
+// Last LUT layer fused with the GroupSum head (slab layout): writes the head's
+// bit planes instead of the layer's bits.  fused_head_nodes(g) is the node
+// count of one block (a divisor of the group size g), or 0 when g does not
+// allow the fused kernel.
+int32_t fused_head_nodes(int32_t g);
+hipError_t launch_lut_slab_head(const uint64_t *in, int32_t w_in, int64_t n_slabs,
+                                const int32_t *conn, const uint64_t *tables, int32_t w_out,
+                                int32_t k, int32_t c, int64_t W, uint64_t *planes, int32_t P,
+                                hipStream_t stream);
+
 struct HeadPlan {
     int32_t splits;        // row splits per class group
     int32_t planes;        // bit planes per split counter
@@ -67,6 +77,11 @@ struct HeadPlan {
     size_t ws_bytes;       // scratch bytes
 };
 HeadPlan plan_head(int32_t w, int64_t n, int32_t c);
+// Plan of the fused last layer + head: splits = g / nb, planes = bit length of nb.
+HeadPlan plan_fused_head(int32_t w, int64_t n, int32_t c, int32_t nb);
+// Finish step only (planes -> scores, argmax).
+hipError_t launch_head_finish(const uint64_t *planes, int64_t n, int32_t c, int32_t *scores,
+                              int32_t *argmax, const HeadPlan &plan, hipStream_t stream);
 
 hipError_t launch_head(const uint64_t *bits, int32_t w, int64_t n, int32_t c,
                        int32_t *scores, int32_t *argmax, void *ws,

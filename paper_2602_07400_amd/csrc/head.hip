@@ -235,6 +235,45 @@ HeadPlan plan_head(int32_t w, int64_t n, int32_t c)
     return p;
 }
 
+HeadPlan plan_fused_head(int32_t w, int64_t n, int32_t c, int32_t nb)
+{
+    HeadPlan p{};
+    const int64_t W = (n + 63) / 64;
+    const int32_t g = w / c;
+    p.splits = g / nb;
+    p.rows_per_split = nb;
+    p.planes = bit_length(nb);
+    p.ws_bytes = (size_t)c * p.splits * p.planes * W * sizeof(uint64_t);
+    return p;
+}
+
+template <int P>
+hipError_t launch_finish_p(const uint64_t *planes, int64_t n, int32_t c, int32_t *scores,
+                           int32_t *argmax, const HeadPlan &plan, hipStream_t stream)
+{
+    const int64_t W = (n + 63) / 64;
+    if (W > 0x7fffffff)
+        return hipErrorInvalidConfiguration;
+    const size_t lds = (size_t)kWave * (c < kFinishClasses ? c : kFinishClasses) * sizeof(int32_t);
+    hipLaunchKernelGGL(k_head_finish<P>, dim3((unsigned)W), dim3(kThreads), lds, stream,
+                       planes, W, n, c, plan.splits, scores, argmax);
+    return hipGetLastError();
+}
+
+hipError_t launch_head_finish(const uint64_t *planes, int64_t n, int32_t c, int32_t *scores,
+                              int32_t *argmax, const HeadPlan &plan, hipStream_t stream)
+{
+    switch (plan.planes) {
+#define BL_CASE(P) \
+    case P: return launch_finish_p<P>(planes, n, c, scores, argmax, plan, stream);
+    BL_CASE(1) BL_CASE(2) BL_CASE(3) BL_CASE(4) BL_CASE(5) BL_CASE(6) BL_CASE(7) BL_CASE(8)
+    BL_CASE(9) BL_CASE(10) BL_CASE(11) BL_CASE(12) BL_CASE(13) BL_CASE(14) BL_CASE(15)
+    BL_CASE(16)
+#undef BL_CASE
+    default: return hipErrorInvalidValue;
+    }
+}
+
 hipError_t launch_head(const uint64_t *bits, int32_t w, int64_t n, int32_t c,
                        int32_t *scores, int32_t *argmax, void *ws, const HeadPlan &plan,
                        int layout, hipStream_t stream)

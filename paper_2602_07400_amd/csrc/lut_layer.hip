@@ -228,11 +228,11 @@ __device__ __forceinline__ void subtree(uint32_t t, const uint32_t (&xv)[H][6], 
     }
 }
 
+// Evaluate one node on 2R half-words (32 samples each).
 template <int K, int R>
-__device__ __forceinline__ void eval_store(uint64_t T, const uint32_t (&xv)[2 * R][K],
-                                           uint64_t *q, bool ok)
+__device__ __forceinline__ void eval_node(uint64_t T, const uint32_t (&xv)[2 * R][K],
+                                          uint32_t (&o)[2 * R])
 {
-    uint32_t o[2 * R];
     if constexpr (K == 6) {
         // Shannon split on x5: the two 5-input halves of the table are folded
         // one after the other, so only 32 masks are live at a time
@@ -253,6 +253,14 @@ __device__ __forceinline__ void eval_store(uint64_t T, const uint32_t (&xv)[2 * 
         for (int h = 0; h < 2 * R; ++h)
             o[h] = mux_tree<K>(xv[h], m);
     }
+}
+
+template <int K, int R>
+__device__ __forceinline__ void eval_store(uint64_t T, const uint32_t (&xv)[2 * R][K],
+                                           uint64_t *q, bool ok)
+{
+    uint32_t o[2 * R];
+    eval_node<K, R>(T, xv, o);
     if (ok) {
         if constexpr (R == 1) {
             const uint64_t v = (uint64_t)o[1] << 32 | o[0];
@@ -357,6 +365,191 @@ hipError_t launch_slab_k(const uint64_t *in, int32_t w_in, int64_t n_slabs,
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Last LUT layer fused with the GroupSum head (Sec. 3 "Encoders and heads";
+// Sec. 5 "Head").  Instead of storing the last layer's bits, every block
+// counts them: its NB nodes lie inside one class group, each lane adds the
+// output bits of the nodes it evaluates into bit-sliced counters (plane p =
+// bit p of 32 per-sample counts per half-word), and at the end the block's
+// lanes are summed through LDS and ds_swizzle into the same per-column bit
+// planes ([column][class][split][plane], split = block within the class)
+// that the head's finish kernel turns into scores and argmax.  The last
+// layer's output tensor is never written or read back.
+//
+// Mapping: slab width 16 words, 8 lanes per node (2 words = 4 half-words
+// each), 32 nodes per pass of the 256-thread block.
+constexpr int kHeadLPN = 8;
+constexpr int kHeadR = 2;
+constexpr int kHeadPassNodes = kThreads / kHeadLPN;   // 32
+constexpr int kHeadCP = 5;                            // counter planes: up to 31 passes
+constexpr int kHeadMaxPasses = 20;                    // nodes per block <= 640
+constexpr int kHeadHalves = 2 * kSlabWords;           // 32 half-words per slab
+
+// acc (NP planes) += v (NQ planes), bit-sliced ripple carry
+template <int NP, int NQ>
+__device__ __forceinline__ void bs_add(uint32_t (&acc)[NP], const uint32_t (&v)[NQ])
+{
+    uint32_t carry = 0;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+        const uint32_t b = (p < NQ) ? v[p < NQ ? p : 0] : 0u;
+        const uint32_t a = acc[p];
+        acc[p] = a ^ b ^ carry;
+        carry = (a & b) | (carry & (a ^ b));
+    }
+}
+
+template <int K, int P>
+__global__ __launch_bounds__(kThreads) void k_lut_slab_head(
+    const uint64_t *__restrict__ in, int32_t w_in, const int32_t *__restrict__ conn,
+    const uint64_t *__restrict__ tables, int32_t g, int32_t nb, int32_t n_nblk,
+    int32_t n_slabs, int64_t W, int32_t c, int32_t splits, uint64_t *__restrict__ planes)
+{
+    static_assert(kSlabWords == 16 && kSlabWords == kHeadLPN * kHeadR, "slab of 16 words");
+    static_assert(P >= kHeadCP, "final planes hold the per-lane counters");
+    // connections and tables while the nodes run, then the counter reduction
+    constexpr int kStageBytes = kHeadMaxPasses * kHeadPassNodes * (K * 4 + 8);
+    constexpr int kRedBytes = kHeadHalves * kHeadPassNodes * kHeadCP * 4;
+    __shared__ __attribute__((aligned(16))) uint8_t s_mem[kStageBytes > kRedBytes ? kStageBytes
+                                                                                  : kRedBytes];
+    uint64_t *s_tab = reinterpret_cast<uint64_t *>(s_mem);
+    int32_t *s_conn = reinterpret_cast<int32_t *>(s_mem + kHeadMaxPasses * kHeadPassNodes * 8);
+    auto s_red = reinterpret_cast<uint32_t (*)[kHeadPassNodes][kHeadCP]>(s_mem);
+
+    const int bid = blockIdx.x;
+    const int loc = local_of(bid);
+    const int slab = (loc / n_nblk) * kXcds + xcd_of(bid);
+    const int nblk = loc % n_nblk;
+    if (slab >= n_slabs)
+        return;
+    const int node0 = nblk * nb;                 // nb divides g: one class per block
+    const int cls = node0 / g;
+    const int split = (node0 % g) / nb;
+    const int passes = nb / kHeadPassNodes;
+
+    for (int q = threadIdx.x; q < nb * K; q += kThreads)
+        s_conn[q] = conn[(int64_t)node0 * K + q];
+    for (int q = threadIdx.x; q < nb; q += kThreads)
+        s_tab[q] = tables[node0 + q];
+    __syncthreads();
+
+    const int sub = threadIdx.x % kHeadLPN;
+    const int lnode = threadIdx.x / kHeadLPN;
+    const uint64_t *src = in + (int64_t)slab * w_in * kSlabWords + sub * kHeadR;
+
+    uint32_t ctr[2 * kHeadR][kHeadCP];
+#pragma unroll
+    for (int h = 0; h < 2 * kHeadR; ++h)
+#pragma unroll
+        for (int p = 0; p < kHeadCP; ++p)
+            ctr[h][p] = 0;
+#pragma unroll 1
+    for (int pass = 0; pass < passes; ++pass) {
+        const int jl = pass * kHeadPassNodes + lnode;
+        uint32_t xv[2 * kHeadR][K];
+        gather<K, kHeadR>(src, &s_conn[jl * K], kSlabWords, xv);
+        uint32_t o[2 * kHeadR];
+        eval_node<K, kHeadR>(s_tab[jl], xv, o);
+#pragma unroll
+        for (int h = 0; h < 2 * kHeadR; ++h) {
+            uint32_t carry = o[h];
+#pragma unroll
+            for (int p = 0; p < kHeadCP; ++p) {
+                const uint32_t t = ctr[h][p] & carry;
+                ctr[h][p] ^= carry;
+                carry = t;
+            }
+        }
+    }
+
+    // lane counters -> LDS (over the staging area), one row of 32 node lanes
+    // per half-word
+    __syncthreads();
+#pragma unroll
+    for (int h = 0; h < 2 * kHeadR; ++h)
+#pragma unroll
+        for (int p = 0; p < kHeadCP; ++p)
+            s_red[sub * 2 * kHeadR + h][lnode][p] = ctr[h][p];
+    __syncthreads();
+
+    // thread t sums 4 node lanes of half-word t/8; the 8 threads of a
+    // half-word then combine with xor swizzles over lanes 1, 2, 4
+    const int hw = threadIdx.x / 8;
+    const int part = threadIdx.x % 8;
+    uint32_t acc[P];
+#pragma unroll
+    for (int p = 0; p < P; ++p)
+        acc[p] = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        uint32_t v[kHeadCP];
+#pragma unroll
+        for (int p = 0; p < kHeadCP; ++p)
+            v[p] = s_red[hw][part * 4 + q][p];
+        bs_add<P, kHeadCP>(acc, v);
+    }
+    {
+        uint32_t v[P];
+#pragma unroll
+        for (int p = 0; p < P; ++p)
+            v[p] = (uint32_t)__builtin_amdgcn_ds_swizzle((int)acc[p], 0x1F | (1 << 10));
+        bs_add<P, P>(acc, v);
+#pragma unroll
+        for (int p = 0; p < P; ++p)
+            v[p] = (uint32_t)__builtin_amdgcn_ds_swizzle((int)acc[p], 0x1F | (2 << 10));
+        bs_add<P, P>(acc, v);
+#pragma unroll
+        for (int p = 0; p < P; ++p)
+            v[p] = (uint32_t)__builtin_amdgcn_ds_swizzle((int)acc[p], 0x1F | (4 << 10));
+        bs_add<P, P>(acc, v);
+    }
+    // half-words 2m and 2m+1 (8 lanes apart) form word m of the slab
+    uint32_t odd[P];
+#pragma unroll
+    for (int p = 0; p < P; ++p)
+        odd[p] = (uint32_t)__builtin_amdgcn_ds_swizzle((int)acc[p], 0x1F | (8 << 10));
+    const int64_t col = (int64_t)slab * kSlabWords + hw / 2;
+    if (part == 0 && (hw % 2) == 0 && col < W) {
+        uint64_t *dst = planes + ((col * c + cls) * (int64_t)splits + split) * P;
+#pragma unroll
+        for (int p = 0; p < P; ++p)
+            dst[p] = ((uint64_t)odd[p] << 32) | acc[p];
+    }
+}
+
+template <int K, int P>
+hipError_t launch_slab_head_kp(const uint64_t *in, int32_t w_in, int64_t n_slabs,
+                               const int32_t *conn, const uint64_t *tables, int32_t w_out,
+                               int32_t g, int32_t nb, int64_t W, int32_t c, uint64_t *planes,
+                               hipStream_t stream)
+{
+    const int32_t n_nblk = w_out / nb;
+    const int64_t slabs_pad = (n_slabs + kXcds - 1) / kXcds * kXcds;
+    const int64_t blocks = slabs_pad * n_nblk;
+    if (blocks > 0x7fffffff)
+        return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((k_lut_slab_head<K, P>), dim3((unsigned)blocks), dim3(kThreads), 0,
+                       stream, in, w_in, conn, tables, g, nb, n_nblk, (int32_t)n_slabs, W, c,
+                       g / nb, planes);
+    return hipGetLastError();
+}
+
+template <int K>
+hipError_t launch_slab_head_k(const uint64_t *in, int32_t w_in, int64_t n_slabs,
+                              const int32_t *conn, const uint64_t *tables, int32_t w_out,
+                              int32_t g, int32_t nb, int32_t P, int64_t W, int32_t c,
+                              uint64_t *planes, hipStream_t stream)
+{
+    switch (P) {
+    case 6: return launch_slab_head_kp<K, 6>(in, w_in, n_slabs, conn, tables, w_out, g, nb, W, c, planes, stream);
+    case 7: return launch_slab_head_kp<K, 7>(in, w_in, n_slabs, conn, tables, w_out, g, nb, W, c, planes, stream);
+    case 8: return launch_slab_head_kp<K, 8>(in, w_in, n_slabs, conn, tables, w_out, g, nb, W, c, planes, stream);
+    case 9: return launch_slab_head_kp<K, 9>(in, w_in, n_slabs, conn, tables, w_out, g, nb, W, c, planes, stream);
+    case 10: return launch_slab_head_kp<K, 10>(in, w_in, n_slabs, conn, tables, w_out, g, nb, W, c, planes, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
 constexpr int kLPN = 4;
 constexpr int kR = 4;
 constexpr int kNB = 256;
@@ -412,6 +605,37 @@ hipError_t launch_lut_layer_slab(const uint64_t *in, int32_t w_in, int64_t n_sla
     case 4: return launch_slab_k<4>(in, w_in, n_slabs, conn, tables, w_out, out, stream);
     case 5: return launch_slab_k<5>(in, w_in, n_slabs, conn, tables, w_out, out, stream);
     case 6: return launch_slab_k<6>(in, w_in, n_slabs, conn, tables, w_out, out, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+int32_t fused_head_nodes(int32_t g)
+{
+    if (kSlabWords != 16 || g <= 0 || g % kHeadPassNodes != 0)
+        return 0;
+    const int32_t units = g / kHeadPassNodes;
+    for (int p = kHeadMaxPasses; p >= 1; --p)
+        if (units % p == 0)
+            return p * kHeadPassNodes;
+    return 0;
+}
+
+hipError_t launch_lut_slab_head(const uint64_t *in, int32_t w_in, int64_t n_slabs,
+                                const int32_t *conn, const uint64_t *tables, int32_t w_out,
+                                int32_t k, int32_t c, int64_t W, uint64_t *planes, int32_t P,
+                                hipStream_t stream)
+{
+    const int32_t g = w_out / c;
+    const int32_t nb = fused_head_nodes(g);
+    if (nb == 0)
+        return hipErrorInvalidValue;
+    switch (k) {
+    case 1: return launch_slab_head_k<1>(in, w_in, n_slabs, conn, tables, w_out, g, nb, P, W, c, planes, stream);
+    case 2: return launch_slab_head_k<2>(in, w_in, n_slabs, conn, tables, w_out, g, nb, P, W, c, planes, stream);
+    case 3: return launch_slab_head_k<3>(in, w_in, n_slabs, conn, tables, w_out, g, nb, P, W, c, planes, stream);
+    case 4: return launch_slab_head_k<4>(in, w_in, n_slabs, conn, tables, w_out, g, nb, P, W, c, planes, stream);
+    case 5: return launch_slab_head_k<5>(in, w_in, n_slabs, conn, tables, w_out, g, nb, P, W, c, planes, stream);
+    case 6: return launch_slab_head_k<6>(in, w_in, n_slabs, conn, tables, w_out, g, nb, P, W, c, planes, stream);
     default: return hipErrorInvalidValue;
     }
 }

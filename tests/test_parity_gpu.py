@@ -331,3 +331,28 @@ def test_forward_timed_records_stage_events():
     assert all(t >= 0 for t in times) and sum(times) > 0
     s2, p2 = model.forward(x)
     assert torch.equal(s1, s2) and torch.equal(p1, p2)
+
+
+@pytest.mark.parametrize("g,c,k,n", [(32, 3, 6, 1000), (96, 5, 4, 64 * 16 + 7), (736, 2, 6, 2500),
+                                     (800, 4, 5, 64 * 16 * 3), (640, 7, 6, 3000), (64, 40, 2, 777)])
+def test_forward_fused_head_matches_oracle_and_unfused(g, c, k, n, monkeypatch):
+    """The last layer fused with the head gives the oracle's result, and the
+    same result as the separate layer + head kernels."""
+    rng = np.random.default_rng(g * 7 + c + k + n)
+    d, b = 60, 3
+    x = rng.integers(0, 256, size=(n, d), dtype=np.uint8)
+    th = np.sort(rng.integers(0, 256, size=(d, b)), axis=1).astype(np.uint8)
+    w1, w2 = 500, g * c
+    layers = []
+    for w, w_in in ((w1, d * b), (w2, w1)):
+        conn = np.stack([rng.choice(w_in, size=k, replace=False) for _ in range(w)]).astype(np.int32)
+        layers.append((conn, rng.integers(0, 1 << 63, size=w).astype(np.uint64)))
+    m = bl.BitlogicModel.from_numpy(th, layers, c, device=DEV)
+    xt = torch.from_numpy(x).to(DEV)
+    s_f, p_f = m.forward(xt)
+    monkeypatch.setenv("BITLOGIC_UNFUSED_HEAD", "1")
+    s_u, p_u = m.forward(xt)
+    monkeypatch.delenv("BITLOGIC_UNFUSED_HEAD")
+    rs, rp = oracle.forward(x, th, layers, c)
+    assert np.array_equal(s_f.cpu().numpy(), rs) and np.array_equal(p_f.cpu().numpy(), rp)
+    assert torch.equal(s_f, s_u) and torch.equal(p_f, p_u)
