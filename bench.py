@@ -8,13 +8,19 @@ bitlogic_forward.  Default workload: the CIFAR-100-shaped wide network
 2 x 64000 nodes with k = 6, 100 classes x 640), synthetic seeded data.
 
 Prints ONE JSON line.  Besides the driver's fields it carries
-  roofline      the dominant kernel (the LUT layer, integer-VALU bound at
-                k = 6) against the chip's 32-bit VALU peak, from per-launch
-                HIP-event times that the library records between the stages
-                of the same forward (bitlogic_forward_timed);
+  roofline      the dominant kernel (the stage of the forward with the longest
+                launch; on C4 a k = 6 LUT layer, integer-VALU bound) against
+                the chip's peak for its bound, from per-launch HIP-event times
+                that the library records between the stages of the same
+                forward (bitlogic_forward_timed);
   cpu_baseline  the CPU oracle timed on a bounded sample of the same
                 workload on this host (and its agreement with the GPU there);
   detail        per-stage times, algorithmic bytes/ops and roofline fractions.
+
+Algorithmic work follows the path the library takes (bitlogic_forward_plan):
+when the last LUT layer is fused with the GroupSum head its output bits are
+never stored, so that stage's compulsory bytes are its input only and the
+head's counting is charged to it.
 """
 from __future__ import annotations
 
@@ -33,8 +39,8 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0
 PEAK_VALU_TOPS = 256 * 64 * 2.4e9 / 1e12      # 39.32 T lane-ops/s
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lut_layer_c4_traffic.json")
-LUT_SOURCE = os.path.join(ROOT, "paper_2602_07400_amd", "csrc", "lut_layer.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "forward_c4_traffic.json")
+CSRC = os.path.join(ROOT, "paper_2602_07400_amd", "csrc")
 
 
 def parse():
@@ -55,37 +61,54 @@ def parse():
     return ap.parse_args()
 
 
-def algorithmic(cfg, n):
+def algorithmic(cfg, n, fused_head):
     """Compulsory bytes and algorithmic 32-bit lane-ops per stage of one forward."""
     W = (n + 63) // 64
     D0 = cfg.d * cfg.b
     st = {"encode": {"bytes": n * cfg.d + D0 * W * 8, "ops": n * D0}}
     w_in = D0
+    L = len(cfg.widths)
     for l, w in enumerate(cfg.widths):
-        st[f"layer{l + 1}"] = {"bytes": (w_in + w) * W * 8,
-                               "ops": 2 * ((1 << cfg.k) - 1) * w * W}
+        last_fused = fused_head and l == L - 1
+        st[f"layer{l + 1}"] = {
+            # a fused last layer reads its input and hands counts to the head
+            "bytes": (w_in + (0 if last_fused else w)) * W * 8,
+            "ops": 2 * ((1 << cfg.k) - 1) * w * W + (n * w // 32 if last_fused else 0)}
         w_in = w
-    st["head"] = {"bytes": w_in * W * 8 + 4 * n * cfg.n_classes + 4 * n,
-                  "ops": n * w_in // 32}
+    out_bytes = 4 * n * cfg.n_classes + 4 * n
+    if fused_head:
+        st["head"] = {"bytes": out_bytes, "ops": n * cfg.n_classes}
+    else:
+        st["head"] = {"bytes": w_in * W * 8 + out_bytes, "ops": n * w_in // 32}
     for v in st.values():
-        v["roof_ms"] = max(v["bytes"] / (PEAK_HBM_GBS * 1e9), v["ops"] / (PEAK_VALU_TOPS * 1e12)) * 1e3
-        v["bound"] = "hbm" if v["bytes"] / (PEAK_HBM_GBS * 1e9) >= v["ops"] / (PEAK_VALU_TOPS * 1e12) else "alu"
+        t_mem = v["bytes"] / (PEAK_HBM_GBS * 1e9)
+        t_alu = v["ops"] / (PEAK_VALU_TOPS * 1e12)
+        v["roof_ms"] = max(t_mem, t_alu) * 1e3
+        v["bound"] = "hbm" if t_mem >= t_alu else "alu"
     return st
 
 
-def traffic_for_current_kernel():
-    """HBM bytes per LUT-layer launch from the committed rocprofv3 counter
-    summary, or None when the kernel source changed since it was taken."""
+def measured_traffic(stage):
+    """HBM bytes per launch of `stage` from the committed rocprofv3 counter
+    summary (FETCH_SIZE + WRITE_SIZE, scaled), or None when a kernel source
+    changed since the counters were taken or the stage was not measured."""
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f)
-        with open(LUT_SOURCE, "rb") as f:
-            h = hashlib.sha256(f.read()).hexdigest()
-    except (OSError, ValueError):
+        for name, digest in rec["sources_sha256"].items():
+            with open(os.path.join(CSRC, name), "rb") as f:
+                if hashlib.sha256(f.read()).hexdigest() != digest:
+                    return None
+        return rec["stages"][stage]["bytes"]
+    except (OSError, ValueError, KeyError):
         return None
-    if rec.get("lut_layer_sha256") != h:
-        return None
-    return rec.get("bytes_per_launch")
+
+
+STAGE_KERNELS = {"encode": "k_encode_t / k_encode_ballot (encoder + bit-pack)",
+                 "layer": "k_lut_slab (LUT layer)",
+                 "layer_fused": "k_lut_slab_head (last LUT layer fused with GroupSum counting)",
+                 "head_fused": "k_head_finish (counts -> scores, argmax)",
+                 "head": "k_head_planes + k_head_finish (GroupSum head, argmax)"}
 
 
 def main():
@@ -152,7 +175,8 @@ def main():
 
     # ---- per-kernel times: the same forward with HIP events recorded by the
     # library at its stage boundaries, on the stream its kernels run on
-    names = ["encode"] + [f"layer{l + 1}" for l in range(len(cfg.widths))] + ["head"]
+    layer_names = [f"layer{l + 1}" for l in range(len(cfg.widths))]
+    names = ["encode"] + layer_names + ["head"]
     ksteps = args.stage_steps or args.steps
     sums = np.zeros(len(names))
     for it in range(ksteps + 2):
@@ -166,23 +190,32 @@ def main():
             sums += [ev[i].elapsed_time(ev[i + 1]) for i in range(len(names))]
     stage_ms = dict(zip(names, (sums / ksteps).tolist()))
 
-    alg = algorithmic(cfg, n)
+    plan = model.plan(n)
+    fused = plan["fused_head"]
+    alg = algorithmic(cfg, n, fused)
     roof_sum = sum(v["roof_ms"] for v in alg.values())
-    layer_names = [k for k in names if k.startswith("layer")]
-    layer_ms = float(np.mean([stage_ms[k] for k in layer_names]))
-    layer_ops = alg["layer1"]["ops"]                          # identical for every layer
-    layer_bound = "alu" if alg["layer1"]["bound"] == "alu" else "hbm"
-    if layer_bound == "alu":
-        achieved = layer_ops / (layer_ms * 1e-3) / 1e12
-        peak, unit = PEAK_VALU_TOPS, "TOP/s"
+    # dominant kernel: the stage with the longest launch
+    dom = max(names, key=lambda k: stage_ms[k])
+    a = alg[dom]
+    if a["bound"] == "alu":
+        achieved = a["ops"] / (stage_ms[dom] * 1e-3) / 1e12
+        peak, unit, per = PEAK_VALU_TOPS, "TOP/s", f"{a['ops']} int32 lane-ops"
     else:
-        achieved = float(np.mean([alg[k]["bytes"] for k in layer_names])) / (layer_ms * 1e-3) / 1e9
-        peak, unit = PEAK_HBM_GBS, "GB/s"
-    roofline = {"bound": layer_bound, "achieved": round(achieved, 3), "peak": round(peak, 3),
+        achieved = a["bytes"] / (stage_ms[dom] * 1e-3) / 1e9
+        peak, unit, per = PEAK_HBM_GBS, "GB/s", f"{a['bytes']} bytes"
+    if dom == "encode":
+        kname = STAGE_KERNELS["encode"]
+    elif dom == "head":
+        kname = STAGE_KERNELS["head_fused" if fused else "head"]
+    elif dom == layer_names[-1] and fused:
+        kname = STAGE_KERNELS["layer_fused"]
+    else:
+        kname = STAGE_KERNELS["layer"]
+    roofline = {"bound": a["bound"], "achieved": round(achieved, 3), "peak": round(peak, 3),
                 "unit": unit, "frac": round(achieved / peak, 4),
-                "traffic": traffic_for_current_kernel() if cfg.name == "c4_cifar100_wide" else None,
-                "kernel": "k_lut_slab (one LUT layer launch of the forward; mean of its layers)",
-                "per_launch": f"2*(2^k-1)*w*W = {layer_ops} int32 lane-ops"}
+                "traffic": measured_traffic(dom) if cfg.name == "c4_cifar100_wide" else None,
+                "kernel": f"{kname}; stage {dom}",
+                "per_launch": per}
 
     detail = {
         "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
@@ -195,6 +228,9 @@ def main():
         "forward_roofline_ms": round(roof_sum, 4),
         "forward_roofline_frac": round(roof_sum / ms_per_step, 4),
         "staged_sum_ms": round(sum(stage_ms.values()), 4),
+        "fused_head": fused,
+        "layer_frac_of_valu_peak": {k: round(alg[k]["ops"] / (stage_ms[k] * 1e-3) / 1e12
+                                             / PEAK_VALU_TOPS, 4) for k in layer_names},
         "gpu": torch.cuda.get_device_name(dev),
         "hip": torch.version.hip,
     }

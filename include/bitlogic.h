@@ -138,6 +138,25 @@ size_t bitlogic_forward_workspace_bytes(int64_t n_samples, int32_t n_features,
                                         const bitlogic_layer *layers,
                                         int32_t n_layers, int32_t n_classes);
 
+/* How bitlogic_forward runs a network of this shape (host only, no HIP
+ * call, nothing enqueued).  Fills *info and returns BITLOGIC_OK, or returns
+ * the status bitlogic_forward would return for these sizes and descriptors
+ * (info untouched).  Device pointers in `layers` are not dereferenced. */
+typedef struct bitlogic_forward_info {
+    size_t workspace_bytes;   /* = bitlogic_forward_workspace_bytes(...)          */
+    int32_t slab_words;       /* intermediates are stored in slabs of this many
+                                 64-sample words: [W_pad / slab][rows][slab]     */
+    int32_t fused_head;       /* 1: the last LUT layer and the GroupSum head run
+                                 as one kernel; the last layer's bits are never
+                                 written to memory                                */
+    int32_t head_splits;      /* partial counters per (sample word, class)       */
+    int32_t head_planes;      /* bit planes per partial counter                  */
+} bitlogic_forward_info;
+
+int bitlogic_forward_plan(int64_t n_samples, int32_t n_features, int32_t n_thresholds,
+                          const bitlogic_layer *layers, int32_t n_layers,
+                          int32_t n_classes, bitlogic_forward_info *info);
+
 /* Whole forward pass, encoder -> n_layers LUT layers -> head (Sec. 3,
  * Eq. 1; App. C.1): pixels in device memory to scores and argmax in
  * device memory.  Layer 0 reads the n_features * n_thresholds encoder wires

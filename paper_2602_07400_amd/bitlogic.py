@@ -22,6 +22,7 @@ import torch
 __all__ = [
     "BitlogicError", "bitlogic_encode", "bitlogic_lut_layer", "bitlogic_groupsum_head",
     "bitlogic_forward", "bitlogic_forward_timed", "bitlogic_forward_workspace_bytes",
+    "bitlogic_forward_plan",
     "bitlogic_groupsum_head_workspace_bytes", "bitlogic_status_string", "bitlogic_version",
     "BitlogicModel", "library_path", "load_library", "words",
 ]
@@ -37,6 +38,12 @@ class BitlogicError(RuntimeError):
     def __init__(self, status: int, detail: str):
         self.status = status
         super().__init__(f"bitlogic status {status} ({bitlogic_status_string(status)}): {detail}")
+
+
+class _ForwardInfo(ctypes.Structure):
+    _fields_ = [("workspace_bytes", ctypes.c_size_t), ("slab_words", ctypes.c_int32),
+                ("fused_head", ctypes.c_int32), ("head_splits", ctypes.c_int32),
+                ("head_planes", ctypes.c_int32)]
 
 
 class _Layer(ctypes.Structure):
@@ -65,6 +72,7 @@ def load_library():
         "bitlogic_groupsum_head_workspace_bytes": ([i32, i64, i32], sz),
         "bitlogic_groupsum_head": ([P, i32, i64, i32, P, P, P, sz, P], ctypes.c_int),
         "bitlogic_forward_workspace_bytes": ([i64, i32, i32, P, i32, i32], sz),
+        "bitlogic_forward_plan": ([i64, i32, i32, P, i32, i32, P], ctypes.c_int),
         "bitlogic_forward": ([P, i64, i32, P, i32, P, i32, i32, P, P, P, sz, P], ctypes.c_int),
         "bitlogic_forward_timed": ([P, i64, i32, P, i32, P, i32, i32, P, P, P, sz, P, P, i32],
                                    ctypes.c_int),
@@ -202,6 +210,20 @@ def bitlogic_forward_workspace_bytes(n_samples: int, n_features: int, n_threshol
         n_classes))
 
 
+def bitlogic_forward_plan(n_samples: int, n_features: int, n_thresholds: int,
+                          layers, n_classes: int) -> dict:
+    """How bitlogic_forward runs this shape: workspace size, slab width, whether
+    the last layer is fused with the head, and the head's counter layout."""
+    arr = _layer_array(layers)
+    info = _ForwardInfo()
+    _check(load_library().bitlogic_forward_plan(
+        n_samples, n_features, n_thresholds, ctypes.cast(arr, ctypes.c_void_p), len(layers),
+        n_classes, ctypes.byref(info)))
+    return {"workspace_bytes": int(info.workspace_bytes), "slab_words": int(info.slab_words),
+            "fused_head": bool(info.fused_head), "head_splits": int(info.head_splits),
+            "head_planes": int(info.head_planes)}
+
+
 def _forward(x, thresholds, layers, n_classes, scores, argmax, workspace, stream, want_scores,
              events):
     n, d = x.shape
@@ -288,6 +310,10 @@ class BitlogicModel:
         return bitlogic_forward_workspace_bytes(n_samples, self.thresholds.shape[0],
                                                 self.thresholds.shape[1], self.layers,
                                                 self.n_classes)
+
+    def plan(self, n_samples: int) -> dict:
+        return bitlogic_forward_plan(n_samples, self.thresholds.shape[0],
+                                     self.thresholds.shape[1], self.layers, self.n_classes)
 
     def forward(self, x: torch.Tensor, **kw):
         return bitlogic_forward(x, self.thresholds, self.layers, self.n_classes, **kw)

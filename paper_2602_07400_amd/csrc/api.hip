@@ -239,6 +239,24 @@ size_t bitlogic_forward_workspace_bytes(int64_t n_samples, int32_t n_features,
     return fp.total;
 }
 
+int bitlogic_forward_plan(int64_t n_samples, int32_t n_features, int32_t n_thresholds,
+                          const bitlogic_layer *layers, int32_t n_layers, int32_t n_classes,
+                          bitlogic_forward_info *info)
+{
+    if (!info)
+        return fail(BITLOGIC_ERR_NULL, "forward_plan: NULL info");
+    ForwardPlan fp;
+    int st = plan_forward(n_samples, n_features, n_thresholds, layers, n_layers, n_classes, &fp);
+    if (st != BITLOGIC_OK)
+        return st;
+    info->workspace_bytes = fp.total;
+    info->slab_words = bl::kSlabWords;
+    info->fused_head = fp.fused ? 1 : 0;
+    info->head_splits = fp.head.splits;
+    info->head_planes = fp.head.planes;
+    return ok();
+}
+
 }  // extern "C"
 
 namespace {

@@ -33,6 +33,10 @@ namespace {
 
 constexpr int kThreads = 256;
 
+#ifndef BL_ENC_NT_STORE
+#define BL_ENC_NT_STORE 1
+#endif
+
 template <int LAYOUT>
 __device__ __forceinline__ int64_t out_index(int64_t wire, int64_t wb, int64_t W, int64_t rows)
 {
@@ -248,8 +252,12 @@ __global__ __launch_bounds__(kThreads) void k_encode_t(
             const uint64_t w0 = otile[r * kOtRow + c2], w1 = otile[r * kOtRow + c2 + 1];
             uint64_t *q = out + out_index<LAYOUT>(wire, wb, W, D0);
             if (wb + 1 < W_cols && (LAYOUT == kLayoutSlab || ((uintptr_t)q % 16) == 0)) {
-                *reinterpret_cast<u32x4 *>(q) =
-                    u32x4{(uint32_t)w0, (uint32_t)(w0 >> 32), (uint32_t)w1, (uint32_t)(w1 >> 32)};
+                const u32x4 v = u32x4{(uint32_t)w0, (uint32_t)(w0 >> 32), (uint32_t)w1,
+                                      (uint32_t)(w1 >> 32)};
+                if (BL_ENC_NT_STORE)
+                    __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(q));
+                else
+                    *reinterpret_cast<u32x4 *>(q) = v;
             } else {
                 q[0] = w0;
                 if (wb + 1 < W_cols)

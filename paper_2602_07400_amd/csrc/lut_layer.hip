@@ -178,9 +178,6 @@ __global__ __launch_bounds__(kThreads) void k_lut_layer(
 // stores are contiguous.  The per-XCD working set of a slab is w_in * S * 8
 // bytes.  Output stores are non-temporal so the output stream does not evict
 // the input slab from L2.
-#ifndef BL_LUT_PREFETCH
-#define BL_LUT_PREFETCH 0
-#endif
 #ifndef BL_NT_STORE
 #define BL_NT_STORE 1
 #endif
@@ -319,31 +316,12 @@ __global__ __launch_bounds__(kThreads, BL_LUT_MINWAVES) void k_lut_slab(
     uint64_t *dst = out + ((int64_t)slab * w_out + node0) * S + sub * R;
     const int npass = (nodes + kPassNodes - 1) / kPassNodes;
 
-    if constexpr (BL_LUT_PREFETCH) {
-        // two register sets: the next pass's gathers are in flight while
-        // the current pass is evaluated
-        uint32_t xa[2 * R][K], xb[2 * R][K];
-        gather<K, R>(src, &s_conn[lnode * K], S, xa);
 #pragma unroll 1
-        for (int pass = 0; pass < npass; pass += 2) {
-            const int ja = pass * kPassNodes + lnode, jb = ja + kPassNodes;
-            if (pass + 1 < npass)
-                gather<K, R>(src, &s_conn[jb * K], S, xb);
-            eval_store<K, R>(s_tab[ja], xa, dst + (int64_t)ja * S, ja < nodes);
-            if (pass + 1 >= npass)
-                break;
-            if (pass + 2 < npass)
-                gather<K, R>(src, &s_conn[(jb + kPassNodes) * K], S, xa);
-            eval_store<K, R>(s_tab[jb], xb, dst + (int64_t)jb * S, jb < nodes);
-        }
-    } else {
-#pragma unroll 1
-        for (int pass = 0; pass < npass; ++pass) {
-            const int jl = pass * kPassNodes + lnode;
-            uint32_t xv[2 * R][K];
-            gather<K, R>(src, &s_conn[jl * K], S, xv);
-            eval_store<K, R>(s_tab[jl], xv, dst + (int64_t)jl * S, jl < nodes);
-        }
+    for (int pass = 0; pass < npass; ++pass) {
+        const int jl = pass * kPassNodes + lnode;
+        uint32_t xv[2 * R][K];
+        gather<K, R>(src, &s_conn[jl * K], S, xv);
+        eval_store<K, R>(s_tab[jl], xv, dst + (int64_t)jl * S, jl < nodes);
     }
 }
 

@@ -161,3 +161,31 @@ def test_forward_timed_validation(lib):
     assert lib.bitlogic_forward_timed(*base, ctypes.cast(ev, ctypes.c_void_p), 4) == ESHAPE
     ev[3] = None
     assert lib.bitlogic_forward_timed(*base, ctypes.cast(ev, ctypes.c_void_p), 5) == ENULL
+
+
+def test_forward_plan(lib, monkeypatch):
+    monkeypatch.delenv("BITLOGIC_UNFUSED_HEAD", raising=False)
+    info = bl._ForwardInfo()
+    ref = ctypes.byref(info)
+    # group size 100 is not a multiple of 32: separate head kernels
+    p, keep = _layers([(1000, 6), (1000, 6)])
+    assert lib.bitlogic_forward_plan(4096, 784, 1, p, 2, 10, ref) == OK
+    assert info.workspace_bytes == lib.bitlogic_forward_workspace_bytes(4096, 784, 1, p, 2, 10)
+    assert info.fused_head == 0 and info.slab_words >= 1
+    assert info.head_splits >= 1 and info.head_planes >= 1
+    # group size 640: last layer and head fused; planes hold counts up to the block size
+    p4, keep4 = _layers([(64000, 6), (64000, 6)])
+    assert lib.bitlogic_forward_plan(1 << 18, 3072, 7, p4, 2, 100, ref) == OK
+    assert info.fused_head == 1
+    assert info.workspace_bytes == lib.bitlogic_forward_workspace_bytes(1 << 18, 3072, 7, p4, 2,
+                                                                        100)
+    nb = 640 // info.head_splits
+    assert nb * info.head_splits == 640 and nb % 32 == 0
+    assert (1 << info.head_planes) > nb
+    monkeypatch.setenv("BITLOGIC_UNFUSED_HEAD", "1")
+    assert lib.bitlogic_forward_plan(1 << 18, 3072, 7, p4, 2, 100, ref) == OK
+    assert info.fused_head == 0
+    # the checks of bitlogic_forward
+    assert lib.bitlogic_forward_plan(4096, 784, 1, p, 2, 10, None) == ENULL
+    assert lib.bitlogic_forward_plan(4096, 784, 1, p, 2, 7, ref) == ESHAPE
+    assert lib.bitlogic_forward_plan(4096, 784, 1, None, 2, 10, ref) == ENULL
