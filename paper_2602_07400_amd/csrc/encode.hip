@@ -9,7 +9,10 @@
 // k_encode_t (b <= 8, the hot path).  A block first fills an LDS code table
 // code[f][v] = sum_t (v > theta[f][t]) << t for its tile of features and every
 // pixel value v, then reuses it for several tiles of 16 columns (1024
-// samples); each wave packs 4 of the 16 columns, one at a time.  A lane loads
+// samples); each wave packs 4 of the 16 columns, one at a time.  The table is
+// built four codes per thread at a time: a dword holds the codes of four
+// consecutive values, and threshold t sets its bit from the first value above
+// it on.  A lane loads
 // its own sample's FT feature bytes (the next column's bytes are in flight
 // while the current one is packed) and assembles, for a group of floor(64/b)
 // features, the 64-bit row of its sample's wires (one table read and one
@@ -33,6 +36,9 @@ namespace {
 
 constexpr int kThreads = 256;
 
+#ifndef BL_ENC_TPB
+#define BL_ENC_TPB 4
+#endif
 #ifndef BL_ENC_NT_STORE
 #define BL_ENC_NT_STORE 1
 #endif
@@ -140,7 +146,7 @@ __global__ __launch_bounds__(kThreads) void k_encode_t(
 {
     using G = EncGeom<B>;
     constexpr int kWires = G::kG * G::kWPG;              // wire rows of one output tile
-    __shared__ uint8_t lut[G::kFT * 256];
+    __shared__ __attribute__((aligned(4))) uint8_t lut[G::kFT * 256];
     __shared__ uint8_t ths[G::kFT * B];
     __shared__ uint64_t otile[kWires * kOtRow];
 
@@ -156,20 +162,25 @@ __global__ __launch_bounds__(kThreads) void k_encode_t(
     const int lane = threadIdx.x % kWave;
     const int wave = threadIdx.x / kWave;
 
-    // ---- code table for this feature tile
+    // ---- code table for this feature tile: dword e holds the codes of values
+    // 4*(e%64) .. +3 of tile feature e/64 (one feature per wave); bit t of a
+    // code is set from byte position p on, p = clamp(theta_t - v0 + 1, 0, 4)
     for (int q = threadIdx.x; q < nf * B; q += kThreads)
         ths[q] = th[(int64_t)f0 * B + q];
     __syncthreads();
-    for (int q = threadIdx.x; q < G::kFT * 256; q += kThreads) {
-        const int f = q >> 8;
-        const uint32_t v = q & 255;
-        uint32_t code = 0;
+    for (int e = threadIdx.x; e < G::kFT * 64; e += kThreads) {
+        const int f = e >> 6;
+        const int v0 = 4 * (e & 63);
+        uint32_t codes = 0;
         if (f < nf) {
 #pragma unroll
-            for (int t = B - 1; t >= 0; --t)
-                code = 2 * code + (v > (uint32_t)ths[f * B + t] ? 1u : 0u);
+            for (int t = 0; t < B; ++t) {
+                const int p = min(max((int)ths[f * B + t] - v0 + 1, 0), 4);
+                const uint32_t m = (p >= 4) ? 0u : (0xFFFFFFFFu << (8 * p));
+                codes |= m & (0x01010101u << t);
+            }
         }
-        lut[q] = (uint8_t)code;
+        reinterpret_cast<uint32_t *>(lut)[e] = codes;
     }
     __syncthreads();
 
@@ -364,9 +375,11 @@ hipError_t launch_t(const uint8_t *x, int64_t n, int32_t d, const uint8_t *th, u
     const int64_t W = (n + 63) / 64;
     const int64_t n_tiles = (W_cols + kEncCols - 1) / kEncCols;
     const int32_t n_ftiles = (d + G::kFT - 1) / G::kFT;
-    // enough blocks to fill the chip; at most 8 column tiles reuse one code table
+    // enough blocks to fill the chip; at most BL_ENC_TPB column tiles reuse one
+    // code table (longer runs let the blocks that share pixel lines drift
+    // apart, and the lines are fetched again)
     int64_t tpb = n_tiles * n_ftiles / 2048;
-    tpb = tpb < 1 ? 1 : (tpb > 8 ? 8 : tpb);
+    tpb = tpb < 1 ? 1 : (tpb > BL_ENC_TPB ? BL_ENC_TPB : tpb);
     const int64_t n_tg = (n_tiles + tpb - 1) / tpb;
     const int64_t n_tg_pad = (n_tg + kXcds - 1) / kXcds * kXcds;
     const int64_t blocks = n_tg_pad * n_ftiles;
