@@ -2,7 +2,8 @@
 
 Python front end of ``bitlogic_oracle.c``: a plain per-sample C implementation
 of the paper's forward pass (thermometer encoder, LUT layers, GroupSum head and
-argmax; Sec. 3 Eq. 1, App. C.1) on unpacked bytes.  Only ``tests/``,
+argmax; Sec. 3 Eq. 1, App. C.1) on unpacked bytes, and of the quantized
+(DSP-backed) class head on the group sums (Sec. 3; Sec. 5 "Head").  Only ``tests/``,
 ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of ``bench.py`` may
 import it.  The product library (``paper_2602_07400_amd``) never imports,
 links or calls anything here, and the two share no code.
@@ -48,9 +49,10 @@ def _load():
         lib.oracle_groupsum.argtypes = [P, i64, i32, i32, P, P]
         lib.oracle_forward.argtypes = [P, i64, i32, P, i32, i32, P, P, P, P,
                                        i32, P, P, i32]
+        lib.oracle_grouped_dsp.argtypes = [P, i64, i32, P, P, P]
         lib.oracle_max_threads.argtypes = []
         for f in (lib.oracle_encode, lib.oracle_lut_layer, lib.oracle_groupsum,
-                  lib.oracle_forward, lib.oracle_max_threads):
+                  lib.oracle_grouped_dsp, lib.oracle_forward, lib.oracle_max_threads):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -104,6 +106,20 @@ def groupsum(v: np.ndarray, n_classes: int):
     _check(_load().oracle_groupsum(_ptr(v), n, w, n_classes, _ptr(scores), _ptr(pred)),
            "groupsum")
     return scores, pred
+
+
+def grouped_dsp(counts: np.ndarray, weights: np.ndarray):
+    """Quantized head: counts int32 [n][c], weights int8 [c][c] ->
+    (logits int64 [n][c], pred int32 [n]); logit i = sum_j weights[i][j] * counts[j]."""
+    counts = np.ascontiguousarray(counts, dtype=np.int32)
+    q = np.ascontiguousarray(weights, dtype=np.int8)
+    n, c = counts.shape
+    assert q.shape == (c, c)
+    logits = np.empty((n, c), dtype=np.int64)
+    pred = np.empty((n,), dtype=np.int32)
+    _check(_load().oracle_grouped_dsp(_ptr(counts), n, c, _ptr(q), _ptr(logits), _ptr(pred)),
+           "grouped_dsp")
+    return logits, pred
 
 
 def forward(x: np.ndarray, thresholds: np.ndarray, layers, n_classes: int,

@@ -21,6 +21,8 @@
  *             design choice"; App. C.1 "Bit-packed inference")
  *   Head      popcount GroupSum, c class scores            (Sec. 3, "Encoders
  *             and heads"; Sec. 5 "Head")
+ *   DSP head  c x c signed 8-bit matrix on the group sums  (Sec. 3, "Encoders
+ *             and heads"; Sec. 5 "Head", head sweep table)
  *   Argmax    predicted class index                        (App. C.2 "HDL
  *             export and emission modes": the top module outputs it)
  *
@@ -29,8 +31,9 @@
  * raw 0..255 pixel scale, encoder wire of (feature f, threshold t) is
  * f*b + t, LUT address bit i comes from connection slot i (entry a of the
  * table is bit a of a 64-bit word), class i owns the contiguous nodes
- * [i*g, (i+1)*g) with g = w/c, and argmax breaks ties toward the lowest
- * class index.
+ * [i*g, (i+1)*g) with g = w/c, argmax breaks ties toward the lowest class
+ * index, and the quantized head computes logit i from row i of its matrix
+ * (the convention of a linear layer's weight) with no bias term.
  *
  * Parity status: every function here is pinned by the CPU tests against
  * closed forms, textbook truth tables, brute force over all inputs of tiny
@@ -89,6 +92,27 @@ static void head_one(const uint8_t *v, int32_t w, int32_t c,
             s += v[j];
         scores[i] = s;
         if (s > scores[best])
+            best = i;
+    }
+    *pred = best;
+}
+
+/* Quantized class head on one sample (Sec. 3 "Encoders and heads": the
+ * quantized variant of the popcount head; Sec. 5 "Head", the DSP-backed head
+ * of the head sweep table): a c x c matrix of signed 8-bit weights multiplies
+ * the length-c group-sum vector, logit i = sum_j q[i][j] * count[j] (row i of
+ * q produces class i, no bias), and the prediction is the first class holding
+ * the largest logit.  Logits are exact in 64-bit integers. */
+static void dsp_one(const int32_t *counts, int32_t c, const int8_t *q, int64_t *logits,
+                    int32_t *pred)
+{
+    int32_t best = 0;
+    for (int32_t i = 0; i < c; ++i) {
+        int64_t acc = 0;
+        for (int32_t j = 0; j < c; ++j)
+            acc += (int64_t)q[(int64_t)i * c + j] * counts[j];
+        logits[i] = acc;
+        if (acc > logits[best])
             best = i;
     }
     *pred = best;
@@ -155,6 +179,17 @@ int oracle_groupsum(const uint8_t *v, int64_t n, int32_t w, int32_t c,
         return ORACLE_ERR_ARG;
     for (int64_t s = 0; s < n; ++s)
         head_one(v + s * w, w, c, scores + s * c, pred + s);
+    return ORACLE_OK;
+}
+
+/* counts [n][c] int32, q [c][c] int8 -> logits [n][c] int64, pred [n] */
+int oracle_grouped_dsp(const int32_t *counts, int64_t n, int32_t c, const int8_t *q,
+                       int64_t *logits, int32_t *pred)
+{
+    if (!counts || !q || !logits || !pred || n < 0 || c <= 0)
+        return ORACLE_ERR_ARG;
+    for (int64_t s = 0; s < n; ++s)
+        dsp_one(counts + s * c, c, q, logits + s * c, pred + s);
     return ORACLE_OK;
 }
 

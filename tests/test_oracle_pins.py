@@ -315,3 +315,80 @@ def test_forward_equals_staged_and_thread_invariant():
     np.testing.assert_array_equal(p1, p0)
     np.testing.assert_array_equal(s4, s0)
     np.testing.assert_array_equal(p4, p0)
+
+
+# ---------------------------------------------------------------------------
+# Quantized (DSP-backed) head on the group sums (Sec. 3 "Encoders and heads";
+# Sec. 5 "Head")
+
+def _dsp_golden():
+    rows = []
+    for line in open(os.path.join(GOLDEN, "grouped_dsp.txt")):
+        line = line.strip()
+        if not line or line.startswith("#"):
+            continue
+        cnt, q, lg, pr = [f.strip() for f in line.split("|")]
+        counts = np.array([int(v) for v in cnt.split(",")], np.int32)
+        Q = np.array([[int(v) for v in r.split(",")] for r in q.split(";")], np.int8)
+        rows.append((counts, Q, np.array([int(v) for v in lg.split(",")], np.int64), int(pr)))
+    return rows
+
+
+@pytest.mark.parametrize("case", range(6))
+def test_grouped_dsp_golden(case):
+    counts, Q, logits, pred = _dsp_golden()[case]
+    got, p = oracle.grouped_dsp(counts[None, :], Q)
+    assert np.array_equal(got[0], logits)
+    assert p[0] == pred
+
+
+def test_grouped_dsp_identity_is_groupsum():
+    # Q = identity reduces the quantized head to the popcount head
+    rng = np.random.default_rng(3)
+    counts = rng.integers(0, 50, (500, 10)).astype(np.int32)
+    logits, pred = oracle.grouped_dsp(counts, np.eye(10, dtype=np.int8))
+    assert np.array_equal(logits, counts)
+    assert np.array_equal(pred, np.argmax(counts, axis=1))
+
+
+def test_grouped_dsp_positive_scale_and_negation():
+    rng = np.random.default_rng(4)
+    counts = rng.integers(0, 20, (400, 7)).astype(np.int32)
+    for a in (1, 3, 127):
+        _, pred = oracle.grouped_dsp(counts, (a * np.eye(7)).astype(np.int8))
+        assert np.array_equal(pred, np.argmax(counts, axis=1))
+    _, pred = oracle.grouped_dsp(counts, (-np.eye(7)).astype(np.int8))
+    assert np.array_equal(pred, np.argmin(counts, axis=1))
+
+
+def test_grouped_dsp_rank_one_closed_form():
+    # Q[i][j] = u[i] * v[j]: logit i = u[i] * (v . counts); catches a
+    # transposed weight matrix (that gives v[i] * (u . counts))
+    rng = np.random.default_rng(5)
+    u = rng.integers(-11, 12, 9)
+    v = rng.integers(-11, 12, 9)
+    Q = np.outer(u, v).astype(np.int8)
+    counts = rng.integers(0, 1000, (300, 9)).astype(np.int32)
+    logits, _ = oracle.grouped_dsp(counts, Q)
+    dot = counts.astype(np.int64) @ v.astype(np.int64)
+    assert np.array_equal(logits, dot[:, None] * u[None, :].astype(np.int64))
+
+
+def test_grouped_dsp_linear_in_counts():
+    rng = np.random.default_rng(6)
+    Q = rng.integers(-127, 128, (12, 12)).astype(np.int8)
+    a = rng.integers(0, 3000, (200, 12)).astype(np.int32)
+    b = rng.integers(0, 3000, (200, 12)).astype(np.int32)
+    la, _ = oracle.grouped_dsp(a, Q)
+    lb, _ = oracle.grouped_dsp(b, Q)
+    lab, _ = oracle.grouped_dsp(a + b, Q)
+    assert np.array_equal(lab, la + lb)
+
+
+def test_grouped_dsp_extremes_exact():
+    c = 100
+    counts = np.full((2, c), 65535, np.int32)
+    lp, _ = oracle.grouped_dsp(counts, np.full((c, c), 127, np.int8))
+    ln, pred = oracle.grouped_dsp(counts, np.full((c, c), -128, np.int8))
+    assert (lp == 100 * 127 * 65535).all() and (ln == -100 * 128 * 65535).all()
+    assert (pred == 0).all()          # all logits equal: lowest index
