@@ -55,6 +55,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--stage-steps", type=int, default=None,
                     help="steps of the per-kernel (staged) timing loop; default = --steps")
+    ap.add_argument("--head", choices=["groupsum", "dsp"], default="groupsum",
+                    help="class head of the timed forward: the popcount GroupSum, or the "
+                         "quantized c x c head on the group sums (bitlogic_forward_grouped_dsp)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run a write-only fill and a read-only sum over this many MiB "
                          "(reference kernels for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE)")
@@ -140,9 +143,16 @@ def main():
     argmax = torch.empty((n,), dtype=torch.int32, device=dev)
     stream = torch.cuda.current_stream(dev)
 
+    dsp_w = torch.from_numpy(wl.dsp_weights).to(dev) if args.head == "dsp" else None
+
     def step():
-        bl.bitlogic_forward(x, model.thresholds, model.layers, model.n_classes,
-                            scores=scores, argmax=argmax, workspace=ws, stream=stream)
+        if dsp_w is None:
+            bl.bitlogic_forward(x, model.thresholds, model.layers, model.n_classes,
+                                scores=scores, argmax=argmax, workspace=ws, stream=stream)
+        else:
+            bl.bitlogic_forward_grouped_dsp(x, model.thresholds, model.layers, model.n_classes,
+                                            dsp_w, logits=scores, argmax=argmax, workspace=ws,
+                                            stream=stream)
 
     if args.calibrate_copy_mib:
         # reference kernels of known traffic for scaling rocprofv3's
@@ -190,6 +200,34 @@ def main():
             sums += [ev[i].elapsed_time(ev[i + 1]) for i in range(len(names))]
     stage_ms = dict(zip(names, (sums / ksteps).tolist()))
 
+    dsp_detail = None
+    if dsp_w is not None:
+        # the quantized head alone, on the group sums of this batch: HIP events
+        # on the launch stream around repeated calls
+        counts = torch.empty((n, cfg.n_classes), dtype=torch.int32, device=dev)
+        bl.bitlogic_forward(x, model.thresholds, model.layers, model.n_classes, scores=counts,
+                            argmax=argmax, workspace=ws, stream=stream)
+        lg = torch.empty_like(counts)
+        reps = max(ksteps, 10)
+        for _ in range(3):
+            bl.bitlogic_grouped_dsp_head(counts, dsp_w, logits=lg, argmax=argmax, stream=stream)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            bl.bitlogic_grouped_dsp_head(counts, dsp_w, logits=lg, argmax=argmax, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t_ms = e0.elapsed_time(e1) / reps
+        c = cfg.n_classes
+        hb = 8 * n * c + 4 * n + c * c            # counts in, logits + argmax out, weights
+        hops = 2 * n * c * c                      # int8 MACs on the matrix cores, x2 ops
+        dsp_detail = {"kernel": "k_grouped_dsp (bitlogic_grouped_dsp_head, 8-bit MFMA)",
+                      "ms": round(t_ms, 4), "bytes": hb, "int8_ops": hops,
+                      "bound": "hbm", "achieved_GBs": round(hb / (t_ms * 1e-3) / 1e9, 1),
+                      "frac_of_hbm_peak": round(hb / (t_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+                      "achieved_int8_TOPs": round(hops / (t_ms * 1e-3) / 1e12, 3)}
+
     plan = model.plan(n)
     fused = plan["fused_head"]
     alg = algorithmic(cfg, n, fused)
@@ -229,6 +267,8 @@ def main():
         "forward_roofline_frac": round(roof_sum / ms_per_step, 4),
         "staged_sum_ms": round(sum(stage_ms.values()), 4),
         "fused_head": fused,
+        "head": args.head,
+        "grouped_dsp_head": dsp_detail,
         "layer_frac_of_valu_peak": {k: round(alg[k]["ops"] / (stage_ms[k] * 1e-3) / 1e12
                                              / PEAK_VALU_TOPS, 4) for k in layer_names},
         "gpu": torch.cuda.get_device_name(dev),
@@ -239,6 +279,8 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
+        step()                        # outputs of the timed forward itself
+        torch.cuda.synchronize()
         threads = oracle.max_threads()
         probe = min(n, 2048)
         t0 = time.perf_counter()
@@ -250,8 +292,10 @@ def main():
         xs = np.ascontiguousarray(wl.x[idx])
         t0 = time.perf_counter()
         rs, rp = oracle.forward(xs, wl.thresholds, wl.layers, wl.n_classes)
+        if dsp_w is not None:
+            rs, rp = oracle.grouped_dsp(rs, wl.dsp_weights)
         cpu_s = time.perf_counter() - t0
-        agree = bool(np.array_equal(scores.cpu().numpy()[idx], rs) and
+        agree = bool(np.array_equal(scores.cpu().numpy()[idx].astype(np.int64), rs) and
                      np.array_equal(argmax.cpu().numpy()[idx], rp))
         cpu = {"value": round(m / cpu_s / 1e6, 6), "unit": "MSamples/s", "cores": threads,
                "kind": "oracle",
@@ -274,7 +318,9 @@ def main():
         "vs_baseline": None,
         "dtype": "u64 (bitwise on packed 64-sample words; u8 pixels, i32 scores)",
         "data": "synthetic",
-        "config": {"workload": cfg.description, "name": cfg.name, "n_samples": n,
+        "config": {"workload": cfg.description + ("" if dsp_w is None else
+                                                     "; quantized c x c head on the group sums"),
+                   "name": cfg.name, "head": args.head, "n_samples": n,
                    "features": cfg.d, "thresholds": cfg.b, "widths": list(cfg.widths),
                    "k": cfg.k, "classes": cfg.n_classes, "seed": args.seed},
         "roofline": roofline,

@@ -184,6 +184,38 @@ int bitlogic_forward_timed(const uint8_t *x, int64_t n_samples, int32_t n_featur
                            void *workspace, size_t workspace_bytes, void *stream,
                            void *const *events, int32_t n_events);
 
+/* Quantized class head (Sec. 3 "Encoders and heads": the quantized variant of
+ * the popcount head; Sec. 5 "Head", the DSP-backed head of the head sweep):
+ * a c x c matrix Q of signed 8-bit weights (trained heads snap them to the
+ * grid [-127, 127]) multiplies the length-c vector of group sums,
+ *     logits[s][i] = sum_j Q[i][j] * counts[s][j]
+ * (row i of Q produces class i, no bias), and argmax[s] = lowest i with the
+ * largest logit.  Any positive output scale leaves the argmax unchanged, so
+ * logits are returned as exact int32 integers.
+ *   counts   [n_samples][n_classes] int32, each in 0..65535 (a group sum;
+ *            values outside that range give undefined logits)
+ *   weights  [n_classes][n_classes] int8, row-major
+ *   logits   [n_samples][n_classes] int32 or NULL; argmax [n_samples] or NULL
+ *            (not both NULL)
+ * Needs 1 <= n_classes <= 128 (BITLOGIC_ERR_UNSUPPORTED otherwise).  Runs on
+ * the matrix cores (8-bit integer MFMA). */
+int bitlogic_grouped_dsp_head(const int32_t *counts, int64_t n_samples, int32_t n_classes,
+                              const int8_t *weights, int32_t *logits, int32_t *argmax,
+                              void *stream);
+
+/* bitlogic_forward with the quantized head in place of the popcount scores:
+ * the same encoder, layers, workspace (bitlogic_forward_workspace_bytes) and
+ * checks, then logits = Q * (group sums) and argmax over the logits, as in
+ * bitlogic_grouped_dsp_head.  weights [n_classes][n_classes] int8, device
+ * memory; n_classes <= 128; the group size is at most 65535 as for the
+ * popcount head, so every count is in range. */
+int bitlogic_forward_grouped_dsp(const uint8_t *x, int64_t n_samples, int32_t n_features,
+                                 const uint8_t *thresholds, int32_t n_thresholds,
+                                 const bitlogic_layer *layers, int32_t n_layers,
+                                 int32_t n_classes, const int8_t *weights, int32_t *logits,
+                                 int32_t *argmax, void *workspace, size_t workspace_bytes,
+                                 void *stream);
+
 /* Static description of a status code. */
 const char *bitlogic_status_string(int status);
 

@@ -22,7 +22,7 @@ import torch
 __all__ = [
     "BitlogicError", "bitlogic_encode", "bitlogic_lut_layer", "bitlogic_groupsum_head",
     "bitlogic_forward", "bitlogic_forward_timed", "bitlogic_forward_workspace_bytes",
-    "bitlogic_forward_plan",
+    "bitlogic_forward_plan", "bitlogic_grouped_dsp_head", "bitlogic_forward_grouped_dsp",
     "bitlogic_groupsum_head_workspace_bytes", "bitlogic_status_string", "bitlogic_version",
     "BitlogicModel", "library_path", "load_library", "words",
 ]
@@ -73,6 +73,9 @@ def load_library():
         "bitlogic_groupsum_head": ([P, i32, i64, i32, P, P, P, sz, P], ctypes.c_int),
         "bitlogic_forward_workspace_bytes": ([i64, i32, i32, P, i32, i32], sz),
         "bitlogic_forward_plan": ([i64, i32, i32, P, i32, i32, P], ctypes.c_int),
+        "bitlogic_grouped_dsp_head": ([P, i64, i32, P, P, P, P], ctypes.c_int),
+        "bitlogic_forward_grouped_dsp": ([P, i64, i32, P, i32, P, i32, i32, P, P, P, P, sz, P],
+                                         ctypes.c_int),
         "bitlogic_forward": ([P, i64, i32, P, i32, P, i32, i32, P, P, P, sz, P], ctypes.c_int),
         "bitlogic_forward_timed": ([P, i64, i32, P, i32, P, i32, i32, P, P, P, sz, P, P, i32],
                                    ctypes.c_int),
@@ -222,6 +225,59 @@ def bitlogic_forward_plan(n_samples: int, n_features: int, n_thresholds: int,
     return {"workspace_bytes": int(info.workspace_bytes), "slab_words": int(info.slab_words),
             "fused_head": bool(info.fused_head), "head_splits": int(info.head_splits),
             "head_planes": int(info.head_planes)}
+
+
+_I8 = (torch.int8,)
+
+
+def bitlogic_grouped_dsp_head(counts: torch.Tensor, weights: torch.Tensor,
+                              logits: Optional[torch.Tensor] = None,
+                              argmax: Optional[torch.Tensor] = None, stream=None,
+                              want_logits: bool = True):
+    """Quantized head: counts int32 [N][c] (0..65535), weights int8 [c][c] ->
+    (logits int32 [N][c], argmax int32 [N]); logit i = sum_j weights[i][j] * counts[j]."""
+    n, c = counts.shape
+    dev = counts.device
+    if tuple(weights.shape) != (c, c):
+        raise ValueError(f"weights must be [{c}][{c}]")
+    if logits is None and want_logits:
+        logits = torch.empty((n, c), dtype=torch.int32, device=dev)
+    if argmax is None:
+        argmax = torch.empty((n,), dtype=torch.int32, device=dev)
+    _check(load_library().bitlogic_grouped_dsp_head(
+        _dev(counts, "counts", _I32), n, c, _dev(weights, "weights", _I8),
+        _dev(logits, "logits", _I32) if logits is not None else None,
+        _dev(argmax, "argmax", _I32), _stream(stream, dev)))
+    return logits, argmax
+
+
+def bitlogic_forward_grouped_dsp(x: torch.Tensor, thresholds: torch.Tensor,
+                                 layers: Sequence[Tuple[torch.Tensor, torch.Tensor]],
+                                 n_classes: int, weights: torch.Tensor,
+                                 logits: Optional[torch.Tensor] = None,
+                                 argmax: Optional[torch.Tensor] = None,
+                                 workspace: Optional[torch.Tensor] = None, stream=None,
+                                 want_logits: bool = True):
+    """Whole forward with the quantized head: pixels uint8 [N][d] ->
+    (logits int32 [N][c], argmax int32 [N])."""
+    n, d = x.shape
+    b = thresholds.shape[1]
+    dev = x.device
+    arr = _layer_array(layers)
+    lib = load_library()
+    need = int(lib.bitlogic_forward_workspace_bytes(
+        n, d, b, ctypes.cast(arr, ctypes.c_void_p), len(arr), n_classes))
+    if logits is None and want_logits:
+        logits = torch.empty((n, n_classes), dtype=torch.int32, device=dev)
+    if argmax is None:
+        argmax = torch.empty((n,), dtype=torch.int32, device=dev)
+    ws_ptr, ws_bytes = _workspace(need, dev, workspace)
+    _check(lib.bitlogic_forward_grouped_dsp(
+        _dev(x, "x", _U8), n, d, _dev(thresholds, "thresholds", _U8), b,
+        ctypes.cast(arr, ctypes.c_void_p), len(arr), n_classes, _dev(weights, "weights", _I8),
+        _dev(logits, "logits", _I32) if logits is not None else None,
+        _dev(argmax, "argmax", _I32), ws_ptr, ws_bytes, _stream(stream, dev)))
+    return logits, argmax
 
 
 def _forward(x, thresholds, layers, n_classes, scores, argmax, workspace, stream, want_scores,

@@ -37,6 +37,7 @@ int hip_status(hipError_t e, const char *what)
 bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p % a) == 0; }
 
 constexpr int64_t kMaxRows = 0x7fffffff;
+constexpr int32_t kDspMaxClasses = 128;   // quantized head: logits below 2^31
 constexpr size_t kWsAlign = 256;
 
 size_t round_up(size_t v) { return (v + kWsAlign - 1) / kWsAlign * kWsAlign; }
@@ -223,8 +224,9 @@ int bitlogic_groupsum_head(const uint64_t *bits, int32_t w, int64_t n_samples,
         return fail(BITLOGIC_ERR_ALIGN, "head: workspace not 256-byte aligned");
     if (n_samples == 0)
         return ok();
-    return hip_status(bl::launch_head(bits, w, n_samples, n_classes, scores, argmax, workspace,
-                                      plan, bl::kLayoutRowMajor, (hipStream_t)stream),
+    return hip_status(bl::launch_head(bits, w, n_samples, n_classes, scores, argmax, nullptr,
+                                      workspace, plan, bl::kLayoutRowMajor,
+                                      (hipStream_t)stream),
                       "head launch");
 }
 
@@ -263,12 +265,15 @@ namespace {
 
 int forward_impl(const uint8_t *x, int64_t n_samples, int32_t n_features,
                  const uint8_t *thresholds, int32_t n_thresholds, const bitlogic_layer *layers,
-                 int32_t n_layers, int32_t n_classes, int32_t *scores, int32_t *argmax,
-                 void *workspace, size_t workspace_bytes, void *stream,
-                 void *const *events, int32_t n_events)
+                 int32_t n_layers, int32_t n_classes, const int8_t *dsp_weights,
+                 int32_t *scores, int32_t *argmax, void *workspace, size_t workspace_bytes,
+                 void *stream, void *const *events, int32_t n_events)
 {
     if (!x || !thresholds || (!scores && !argmax))
         return fail(BITLOGIC_ERR_NULL, "forward: NULL pixels/thresholds or both outputs NULL");
+    if (dsp_weights && n_classes > kDspMaxClasses)
+        return fail(BITLOGIC_ERR_UNSUPPORTED, "forward: quantized head needs n_classes <= %d",
+                    kDspMaxClasses);
     ForwardPlan fp;
     int st = plan_forward(n_samples, n_features, n_thresholds, layers, n_layers, n_classes, &fp);
     if (st != BITLOGIC_OK)
@@ -330,10 +335,11 @@ int forward_impl(const uint8_t *x, int64_t n_samples, int32_t n_features,
         w_in = layers[l].w_out;
     }
     if (fp.fused)
-        e = bl::launch_head_finish(planes, n_samples, n_classes, scores, argmax, fp.head, s);
+        e = bl::launch_head_finish(planes, n_samples, n_classes, scores, argmax, dsp_weights,
+                                   fp.head, s);
     else
-        e = bl::launch_head(cur, w_in, n_samples, n_classes, scores, argmax, planes, fp.head,
-                            bl::kLayoutSlab, s);
+        e = bl::launch_head(cur, w_in, n_samples, n_classes, scores, argmax, dsp_weights, planes,
+                            fp.head, bl::kLayoutSlab, s);
     if (e == hipSuccess)
         e = mark(n_layers + 2);
     return hip_status(e, "forward: head launch");
@@ -350,7 +356,42 @@ int bitlogic_forward(const uint8_t *x, int64_t n_samples, int32_t n_features,
                      void *stream)
 {
     return forward_impl(x, n_samples, n_features, thresholds, n_thresholds, layers, n_layers,
-                        n_classes, scores, argmax, workspace, workspace_bytes, stream, nullptr, 0);
+                        n_classes, nullptr, scores, argmax, workspace, workspace_bytes, stream,
+                        nullptr, 0);
+}
+
+int bitlogic_forward_grouped_dsp(const uint8_t *x, int64_t n_samples, int32_t n_features,
+                                 const uint8_t *thresholds, int32_t n_thresholds,
+                                 const bitlogic_layer *layers, int32_t n_layers,
+                                 int32_t n_classes, const int8_t *weights, int32_t *logits,
+                                 int32_t *argmax, void *workspace, size_t workspace_bytes,
+                                 void *stream)
+{
+    if (!weights)
+        return fail(BITLOGIC_ERR_NULL, "forward_grouped_dsp: NULL weights");
+    return forward_impl(x, n_samples, n_features, thresholds, n_thresholds, layers, n_layers,
+                        n_classes, weights, logits, argmax, workspace, workspace_bytes, stream,
+                        nullptr, 0);
+}
+
+int bitlogic_grouped_dsp_head(const int32_t *counts, int64_t n_samples, int32_t n_classes,
+                              const int8_t *weights, int32_t *logits, int32_t *argmax,
+                              void *stream)
+{
+    if (!counts || !weights || (!logits && !argmax))
+        return fail(BITLOGIC_ERR_NULL, "grouped_dsp_head: NULL counts/weights or both outputs");
+    if (n_samples < 0 || n_classes < 1 || n_samples > ((int64_t)1 << 40))
+        return fail(BITLOGIC_ERR_SHAPE, "grouped_dsp_head: need n_samples >= 0, n_classes >= 1");
+    if (n_classes > kDspMaxClasses)
+        return fail(BITLOGIC_ERR_UNSUPPORTED, "grouped_dsp_head: n_classes %d > %d", n_classes,
+                    kDspMaxClasses);
+    if (!aligned(counts, 4) || (logits && !aligned(logits, 4)) || (argmax && !aligned(argmax, 4)))
+        return fail(BITLOGIC_ERR_ALIGN, "grouped_dsp_head: misaligned buffer");
+    if (n_samples == 0)
+        return ok();
+    return hip_status(bl::launch_grouped_dsp(counts, n_samples, n_classes, weights, logits, argmax,
+                                             (hipStream_t)stream),
+                      "grouped_dsp_head launch");
 }
 
 int bitlogic_forward_timed(const uint8_t *x, int64_t n_samples, int32_t n_features,
@@ -363,8 +404,8 @@ int bitlogic_forward_timed(const uint8_t *x, int64_t n_samples, int32_t n_featur
     if (!events)
         return fail(BITLOGIC_ERR_NULL, "forward_timed: NULL event array");
     return forward_impl(x, n_samples, n_features, thresholds, n_thresholds, layers, n_layers,
-                        n_classes, scores, argmax, workspace, workspace_bytes, stream, events,
-                        n_events);
+                        n_classes, nullptr, scores, argmax, workspace, workspace_bytes, stream,
+                        events, n_events);
 }
 
 const char *bitlogic_status_string(int status)

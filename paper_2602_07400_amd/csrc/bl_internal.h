@@ -79,12 +79,19 @@ struct HeadPlan {
 HeadPlan plan_head(int32_t w, int64_t n, int32_t c);
 // Plan of the fused last layer + head: splits = g / nb, planes = bit length of nb.
 HeadPlan plan_fused_head(int32_t w, int64_t n, int32_t c, int32_t nb);
-// Finish step only (planes -> scores, argmax).
+// Finish step only (planes -> scores, argmax).  With dsp_weights (int8
+// [c][c], c <= 128) the quantized head's logits replace the scores.
 hipError_t launch_head_finish(const uint64_t *planes, int64_t n, int32_t c, int32_t *scores,
-                              int32_t *argmax, const HeadPlan &plan, hipStream_t stream);
+                              int32_t *argmax, const int8_t *dsp_weights, const HeadPlan &plan,
+                              hipStream_t stream);
 
 hipError_t launch_head(const uint64_t *bits, int32_t w, int64_t n, int32_t c,
-                       int32_t *scores, int32_t *argmax, void *ws,
+                       int32_t *scores, int32_t *argmax, const int8_t *dsp_weights, void *ws,
                        const HeadPlan &plan, int layout, hipStream_t stream);
+
+// Quantized head on counts [n][c] (0..65535 each), c <= 128.
+hipError_t launch_grouped_dsp(const int32_t *counts, int64_t n, int32_t c,
+                              const int8_t *weights, int32_t *logits, int32_t *argmax,
+                              hipStream_t stream);
 
 }  // namespace bl

@@ -15,14 +15,30 @@
 // class score bit by bit from the column's planes (wave-uniform scalar loads)
 // and sum the splits into an LDS score tile, from which the argmax is taken
 // and the scores are written as one contiguous block.
+//
+// Quantized head (Sec. 3 "Encoders and heads"; Sec. 5 "Head", the DSP-backed
+// head): logit i = sum_j Q[i][j] * count[j] with Q a c x c matrix of signed
+// 8-bit weights.  Per 64-sample column this is a [64 x c] x [c x c] integer
+// product, done on the matrix cores with v_mfma_i32_16x16x32_i8: a count
+// (0..65535) is split into two offset bytes, count = 256 (h + 128) + (l + 128)
+// with h, l in [-128, 127], so logit = 256 (Q h) + (Q l) + 32896 rowsum(Q),
+// exact in 32-bit integers for c <= 128.
 #include "bl_internal.h"
 
 namespace bl {
+
+template <int P>
+hipError_t launch_finish_p(const uint64_t *planes, int64_t n, int32_t c, int32_t *scores,
+                           int32_t *argmax, const int8_t *dsp_weights, const HeadPlan &plan,
+                           hipStream_t stream);
+
 namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
 constexpr int kMaxPlanes = 16;
+constexpr int kDspMaxClasses = 128;   // logits stay below 2^31; tiles fit in LDS
+constexpr int64_t kDspBlocks = 1024;  // blocks of the quantized head (4 per CU)
 
 __device__ __forceinline__ void csa(uint64_t &h, uint64_t &l, uint64_t a, uint64_t b,
                                     uint64_t c)
@@ -166,10 +182,331 @@ __global__ __launch_bounds__(kThreads) void k_head_finish(
         argmax[s0 + lane] = besti;
 }
 
+// ---------------------------------------------------------------------------
+// Quantized head on the matrix cores.
+
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+
+// LDS of the quantized head for c classes: Q padded to [cn][ckp] bytes
+// (cn = c rounded up to 16 output classes, ck = c rounded up to the 32-deep
+// K step, ckp = ck + 8 to spread the banks) and its row sums, kept for the
+// block's whole run of 64-sample tiles; the two offset byte planes of a
+// tile's counts [64][ckp], whose bytes the logit tile [64][c] reuses once
+// the products are in registers; and the argmax partials.
+struct DspLayout {
+    int cn, ck, ckp;
+    size_t off_q, off_rs, off_lo, off_hi, off_tile, off_part, bytes;
+};
+
+__host__ __device__ inline DspLayout dsp_layout(int c)
+{
+    DspLayout L;
+    L.cn = (c + 15) / 16 * 16;
+    L.ck = (c + 31) / 32 * 32;
+    L.ckp = L.ck + 8;
+    L.off_q = 0;
+    L.off_rs = (size_t)L.cn * L.ckp;
+    L.off_lo = L.off_rs + (size_t)L.cn * 4;
+    L.off_hi = L.off_lo + (size_t)kWave * L.ckp;
+    const size_t planes_end = L.off_hi + (size_t)kWave * L.ckp;
+    L.off_tile = L.off_lo;
+    const size_t tile_end = L.off_tile + (size_t)kWave * c * 4;
+    L.off_part = ((planes_end > tile_end ? planes_end : tile_end) + 15) / 16 * 16;
+    L.bytes = L.off_part + 2 * kWaves * kWave * 4;
+    return L;
+}
+
+// Stage Q (zero padded) and its row sums in LDS, once per block.  All
+// threads; ends with a barrier.  Q is read as whole dwords when c*c is a
+// multiple of 4 and the matrix is 4-byte aligned.
+__device__ __forceinline__ void dsp_stage_q(const int8_t *__restrict__ weights, int c,
+                                            const DspLayout &L, uint8_t *smem)
+{
+    int8_t *q = reinterpret_cast<int8_t *>(smem + L.off_q);
+    int32_t *rs = reinterpret_cast<int32_t *>(smem + L.off_rs);
+    uint32_t *q32 = reinterpret_cast<uint32_t *>(smem + L.off_q);
+    for (int e = threadIdx.x; e < L.cn * L.ckp / 4; e += kThreads)
+        q32[e] = 0;
+    __syncthreads();
+    const int cc = c * c;
+    if (cc % 4 == 0 && ((uintptr_t)weights % 4) == 0) {
+        const uint32_t *w32 = reinterpret_cast<const uint32_t *>(weights);
+        for (int e = threadIdx.x; e < cc / 4; e += kThreads) {
+            const uint32_t v = w32[e];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int f = 4 * e + u;
+                q[(f / c) * L.ckp + f % c] = (int8_t)(v >> (8 * u));
+            }
+        }
+    } else {
+        for (int f = threadIdx.x; f < cc; f += kThreads)
+            q[(f / c) * L.ckp + f % c] = weights[f];
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < L.cn; i += kThreads) {
+        int32_t sum = 0;
+        for (int k = 0; k < c; ++k)
+            sum += q[i * L.ckp + k];
+        rs[i] = sum;
+    }
+    __syncthreads();
+}
+
+// Count of (sample row r, class k) into the two offset byte planes.
+__device__ __forceinline__ void dsp_put_count(uint8_t *smem, const DspLayout &L, int r, int k,
+                                              int32_t cnt)
+{
+    smem[L.off_lo + (size_t)r * L.ckp + k] = (uint8_t)((cnt & 0xFF) ^ 0x80);
+    smem[L.off_hi + (size_t)r * L.ckp + k] = (uint8_t)(((cnt >> 8) & 0xFF) ^ 0x80);
+}
+
+// Logit tile [64][c] from the byte planes and Q (after a barrier; ends with
+// one).  The 4 waves share the (16-sample, 16-class) output tiles, at most
+// kDspTilesPerWave each; v_mfma_i32_16x16x32_i8 takes in lane l the 8
+// K-consecutive bytes of row l % 16 at K offset 8 * (l / 16) of A (counts)
+// and of B^T (rows of Q), and returns D[4 * (l / 16) + r][l % 16] in
+// accumulator r.  The results wait in registers until every wave is done
+// with the staging bytes, which the tile then overwrites.
+constexpr int kDspTilesPerWave = 4 * (kDspMaxClasses / 16) / kWaves;
+
+__device__ __forceinline__ void dsp_logits(uint8_t *smem, const DspLayout &L, int c)
+{
+    const int8_t *q = reinterpret_cast<const int8_t *>(smem + L.off_q);
+    const int32_t *rs = reinterpret_cast<const int32_t *>(smem + L.off_rs);
+    const int lane = threadIdx.x % kWave;
+    const int wave = threadIdx.x / kWave;
+    const int row = lane % 16, kq = 8 * (lane / 16);
+    const int n_t = 4 * (L.cn / 16);
+    i32x4 res[kDspTilesPerWave];
+#pragma unroll
+    for (int j = 0; j < kDspTilesPerWave; ++j) {
+        const int t = wave + kWaves * j;
+        if (t >= n_t)
+            break;
+        const int mt = t % 4, nt = t / 4;
+        i32x4 acc_lo = {0, 0, 0, 0}, acc_hi = {0, 0, 0, 0};
+        for (int k0 = 0; k0 < L.ck; k0 += 32) {
+            const size_t a_off = (size_t)(16 * mt + row) * L.ckp + k0 + kq;
+            const long a_lo = *reinterpret_cast<const long *>(smem + L.off_lo + a_off);
+            const long a_hi = *reinterpret_cast<const long *>(smem + L.off_hi + a_off);
+            const long b = *reinterpret_cast<const long *>(q + (size_t)(16 * nt + row) * L.ckp +
+                                                           k0 + kq);
+            acc_lo = __builtin_amdgcn_mfma_i32_16x16x32_i8(a_lo, b, acc_lo, 0, 0, 0);
+            acc_hi = __builtin_amdgcn_mfma_i32_16x16x32_i8(a_hi, b, acc_hi, 0, 0, 0);
+        }
+        const uint32_t corr = 32896u * (uint32_t)rs[16 * nt + row];
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            res[j][r] = (int32_t)(256u * (uint32_t)acc_hi[r] + (uint32_t)acc_lo[r] + corr);
+    }
+    __syncthreads();
+    int32_t *tile = reinterpret_cast<int32_t *>(smem + L.off_tile);
+#pragma unroll
+    for (int j = 0; j < kDspTilesPerWave; ++j) {
+        const int t = wave + kWaves * j;
+        if (t >= n_t)
+            break;
+        const int mt = t % 4, cls = 16 * (t / 4) + row;
+        if (cls < c)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                tile[(16 * mt + kq / 2 + r) * c + cls] = res[j][r];   // row 4 * (l / 16) + r
+    }
+    __syncthreads();
+}
+
+// Argmax (lowest index) and coalesced logit store of the tile; ends with a
+// barrier.  Each wave scans a quarter of the classes of every sample, then
+// wave 0 merges the four partial maxima (in class order, so ties keep the
+// lowest index).
+__device__ __forceinline__ void dsp_emit(uint8_t *smem, const DspLayout &L, int c, int64_t s0,
+                                         int64_t n, int32_t *__restrict__ logits,
+                                         int32_t *__restrict__ argmax)
+{
+    const int32_t *tile = reinterpret_cast<const int32_t *>(smem + L.off_tile);
+    int32_t *part = reinterpret_cast<int32_t *>(smem + L.off_part);   // [2][kWaves][64]
+    const int lane = threadIdx.x % kWave;
+    const int wave = threadIdx.x / kWave;
+    if (argmax) {
+        const int per = (c + kWaves - 1) / kWaves;
+        const int i0 = wave * per, i1 = min(c, i0 + per);
+        int32_t best = INT32_MIN, besti = c;
+        for (int i = i0; i < i1; ++i) {
+            const int32_t v = tile[lane * c + i];
+            if (v > best) {
+                best = v;
+                besti = i;
+            }
+        }
+        part[wave * kWave + lane] = best;
+        part[(kWaves + wave) * kWave + lane] = besti;
+    }
+    if (logits)
+        for (int e = threadIdx.x; e < kWave * c; e += kThreads) {
+            const int64_t ss = s0 + e / c;
+            if (ss < n)
+                logits[ss * c + e % c] = tile[e];
+        }
+    __syncthreads();
+    if (argmax && wave == 0 && s0 + lane < n) {
+        int32_t best = part[lane], besti = part[kWaves * kWave + lane];
+        for (int w = 1; w < kWaves; ++w) {
+            const int32_t v = part[w * kWave + lane];
+            const int32_t vi = part[(kWaves + w) * kWave + lane];
+            if (vi < c && (besti >= c || v > best)) {
+                best = v;
+                besti = vi;
+            }
+        }
+        argmax[s0 + lane] = besti;
+    }
+}
+
+// Fused finish of the quantized head: class counts of a 64-sample column from
+// the bit planes (as k_head_finish), then the logits on the matrix cores.
+template <int P>
+__global__ __launch_bounds__(kThreads) void k_head_finish_dsp(
+    const uint64_t *__restrict__ planes, int64_t n, int32_t c, int32_t S,
+    const int8_t *__restrict__ weights, int32_t *__restrict__ logits,
+    int32_t *__restrict__ argmax)
+{
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+    const DspLayout L = dsp_layout(c);
+    const int lane = threadIdx.x % kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int64_t W = (n + kWave - 1) / kWave;
+    dsp_stage_q(weights, c, L, smem);
+    for (int64_t col = blockIdx.x; col < W; col += gridDim.x) {
+        const uint64_t *pc = planes + col * (int64_t)c * S * P;
+        for (int i = wave; i < c; i += kWaves) {
+            int32_t cnt = 0;
+            for (int q = 0; q < S; ++q) {
+                const uint64_t *pl = pc + ((int64_t)i * S + q) * P;
+                int32_t part = 0;
+#pragma unroll
+                for (int p = 0; p < P; ++p)
+                    part |= (int32_t)((pl[p] >> lane) & 1u) << p;
+                cnt += part;
+            }
+            dsp_put_count(smem, L, lane, i, cnt);
+        }
+        __syncthreads();
+        dsp_logits(smem, L, c);
+        dsp_emit(smem, L, c, col * kWave, n, logits, argmax);
+    }
+}
+
+// Standalone quantized head on counts [n][c] in device memory.  Only Q
+// lives in LDS: each wave takes 16-sample M-tiles and builds its A operands
+// (8 counts per lane and K step, split into the two offset bytes) straight
+// from global memory; each output tile is stored from the accumulators, and
+// the argmax of a sample -- spread over the 16 lanes of a row and over the
+// N tiles -- is a running maximum per lane followed by a 16-lane xor
+// reduction that prefers the lower class on ties.
+constexpr int kDspMaxK = kDspMaxClasses / 32;      // K steps of 32 classes
+
+__device__ __forceinline__ uint32_t dsp_byte_pack(const int32_t (&v)[4], int shift)
+{
+    uint32_t r = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+        r |= (((uint32_t)v[u] >> shift) & 0xFFu) << (8 * u);
+    return r ^ 0x80808080u;
+}
+
+__global__ __launch_bounds__(kThreads) void k_grouped_dsp(
+    const int32_t *__restrict__ counts, int64_t n, int32_t c,
+    const int8_t *__restrict__ weights, int32_t *__restrict__ logits,
+    int32_t *__restrict__ argmax)
+{
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+    const DspLayout L = dsp_layout(c);
+    dsp_stage_q(weights, c, L, smem);
+    const int8_t *q = reinterpret_cast<const int8_t *>(smem + L.off_q);
+    const int32_t *rs = reinterpret_cast<const int32_t *>(smem + L.off_rs);
+    const int lane = threadIdx.x % kWave;
+    const int row = lane % 16, kg = lane / 16, kq = 8 * kg;
+    const int nks = L.ck / 32, n_nt = L.cn / 16;
+    const int64_t n_mt = (n + 15) / 16;
+    const int64_t stride = (int64_t)gridDim.x * kWaves;
+    for (int64_t mt = (int64_t)blockIdx.x * kWaves + threadIdx.x / kWave; mt < n_mt;
+         mt += stride) {
+        const int64_t sa = 16 * mt + row;                 // this lane's A row
+        long a_lo[kDspMaxK], a_hi[kDspMaxK];
+#pragma unroll
+        for (int ks = 0; ks < kDspMaxK; ++ks) {
+            if (ks >= nks)
+                break;
+            int32_t v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int k = 32 * ks + kq + j;
+                v[j] = (sa < n && k < c) ? counts[sa * c + k] : 0;
+            }
+            const int32_t v0[4] = {v[0], v[1], v[2], v[3]}, v1[4] = {v[4], v[5], v[6], v[7]};
+            a_lo[ks] = (long)(((uint64_t)dsp_byte_pack(v1, 0) << 32) | dsp_byte_pack(v0, 0));
+            a_hi[ks] = (long)(((uint64_t)dsp_byte_pack(v1, 8) << 32) | dsp_byte_pack(v0, 8));
+        }
+        int32_t best[4], besti[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            best[r] = INT32_MIN;
+            besti[r] = c;
+        }
+        for (int nt = 0; nt < n_nt; ++nt) {
+            i32x4 acc_lo = {0, 0, 0, 0}, acc_hi = {0, 0, 0, 0};
+#pragma unroll
+            for (int ks = 0; ks < kDspMaxK; ++ks) {
+                if (ks >= nks)
+                    break;
+                const long b = *reinterpret_cast<const long *>(
+                    q + (size_t)(16 * nt + row) * L.ckp + 32 * ks + kq);
+                acc_lo = __builtin_amdgcn_mfma_i32_16x16x32_i8(a_lo[ks], b, acc_lo, 0, 0, 0);
+                acc_hi = __builtin_amdgcn_mfma_i32_16x16x32_i8(a_hi[ks], b, acc_hi, 0, 0, 0);
+            }
+            const int cls = 16 * nt + row;               // output column of this lane
+            if (cls < c) {
+                const uint32_t corr = 32896u * (uint32_t)rs[cls];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int32_t v =
+                        (int32_t)(256u * (uint32_t)acc_hi[r] + (uint32_t)acc_lo[r] + corr);
+                    const int64_t smp = 16 * mt + 4 * kg + r;
+                    if (logits && smp < n)
+                        logits[smp * c + cls] = v;
+                    if (v > best[r]) {                   // classes ascend with nt
+                        best[r] = v;
+                        besti[r] = cls;
+                    }
+                }
+            }
+        }
+        if (argmax) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+#pragma unroll
+                for (int m = 1; m < 16; m <<= 1) {
+                    const int32_t ov = __shfl_xor(best[r], m);
+                    const int32_t oi = __shfl_xor(besti[r], m);
+                    if (oi < c && (besti[r] >= c || ov > best[r] ||
+                                   (ov == best[r] && oi < besti[r]))) {
+                        best[r] = ov;
+                        besti[r] = oi;
+                    }
+                }
+                const int64_t smp = 16 * mt + 4 * kg + r;
+                if (row == 0 && smp < n)
+                    argmax[smp] = besti[r];
+            }
+        }
+    }
+}
+
 template <int P>
 hipError_t launch_p(const uint64_t *bits, int32_t w, int64_t n, int32_t c,
-                    int32_t *scores, int32_t *argmax, uint64_t *planes,
-                    const HeadPlan &plan, int layout, hipStream_t stream)
+                    int32_t *scores, int32_t *argmax, const int8_t *dsp_weights,
+                    uint64_t *planes, const HeadPlan &plan, int layout, hipStream_t stream)
 {
     const int64_t W = (n + 63) / 64;
     const int64_t n_cb = (W + kWave - 1) / kWave;
@@ -188,10 +525,7 @@ hipError_t launch_p(const uint64_t *bits, int32_t w, int64_t n, int32_t c,
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
-    const size_t lds = (size_t)kWave * (c < kFinishClasses ? c : kFinishClasses) * sizeof(int32_t);
-    hipLaunchKernelGGL(k_head_finish<P>, dim3((unsigned)W), dim3(kThreads), lds, stream,
-                       planes, W, n, c, plan.splits, scores, argmax);
-    return hipGetLastError();
+    return launch_finish_p<P>(planes, n, c, scores, argmax, dsp_weights, plan, stream);
 }
 
 int bit_length(int64_t v)
@@ -249,11 +583,22 @@ HeadPlan plan_fused_head(int32_t w, int64_t n, int32_t c, int32_t nb)
 
 template <int P>
 hipError_t launch_finish_p(const uint64_t *planes, int64_t n, int32_t c, int32_t *scores,
-                           int32_t *argmax, const HeadPlan &plan, hipStream_t stream)
+                           int32_t *argmax, const int8_t *dsp_weights, const HeadPlan &plan,
+                           hipStream_t stream)
 {
     const int64_t W = (n + 63) / 64;
     if (W > 0x7fffffff)
         return hipErrorInvalidConfiguration;
+    if (dsp_weights) {
+        if (c > kDspMaxClasses)
+            return hipErrorInvalidValue;
+        // Q is staged once per block and reused for a run of columns
+        const int64_t blocks = W < kDspBlocks ? W : kDspBlocks;
+        hipLaunchKernelGGL(k_head_finish_dsp<P>, dim3((unsigned)blocks), dim3(kThreads),
+                           dsp_layout(c).bytes, stream, planes, n, c, plan.splits, dsp_weights,
+                           scores, argmax);
+        return hipGetLastError();
+    }
     const size_t lds = (size_t)kWave * (c < kFinishClasses ? c : kFinishClasses) * sizeof(int32_t);
     hipLaunchKernelGGL(k_head_finish<P>, dim3((unsigned)W), dim3(kThreads), lds, stream,
                        planes, W, n, c, plan.splits, scores, argmax);
@@ -261,11 +606,12 @@ hipError_t launch_finish_p(const uint64_t *planes, int64_t n, int32_t c, int32_t
 }
 
 hipError_t launch_head_finish(const uint64_t *planes, int64_t n, int32_t c, int32_t *scores,
-                              int32_t *argmax, const HeadPlan &plan, hipStream_t stream)
+                              int32_t *argmax, const int8_t *dsp_weights, const HeadPlan &plan,
+                              hipStream_t stream)
 {
     switch (plan.planes) {
 #define BL_CASE(P) \
-    case P: return launch_finish_p<P>(planes, n, c, scores, argmax, plan, stream);
+    case P: return launch_finish_p<P>(planes, n, c, scores, argmax, dsp_weights, plan, stream);
     BL_CASE(1) BL_CASE(2) BL_CASE(3) BL_CASE(4) BL_CASE(5) BL_CASE(6) BL_CASE(7) BL_CASE(8)
     BL_CASE(9) BL_CASE(10) BL_CASE(11) BL_CASE(12) BL_CASE(13) BL_CASE(14) BL_CASE(15)
     BL_CASE(16)
@@ -275,13 +621,14 @@ hipError_t launch_head_finish(const uint64_t *planes, int64_t n, int32_t c, int3
 }
 
 hipError_t launch_head(const uint64_t *bits, int32_t w, int64_t n, int32_t c,
-                       int32_t *scores, int32_t *argmax, void *ws, const HeadPlan &plan,
-                       int layout, hipStream_t stream)
+                       int32_t *scores, int32_t *argmax, const int8_t *dsp_weights, void *ws,
+                       const HeadPlan &plan, int layout, hipStream_t stream)
 {
     uint64_t *planes = static_cast<uint64_t *>(ws);
     switch (plan.planes) {
 #define BL_CASE(P) \
-    case P: return launch_p<P>(bits, w, n, c, scores, argmax, planes, plan, layout, stream);
+    case P: return launch_p<P>(bits, w, n, c, scores, argmax, dsp_weights, planes, plan, \
+                               layout, stream);
     BL_CASE(1) BL_CASE(2) BL_CASE(3) BL_CASE(4) BL_CASE(5) BL_CASE(6) BL_CASE(7) BL_CASE(8)
     BL_CASE(9) BL_CASE(10) BL_CASE(11) BL_CASE(12) BL_CASE(13) BL_CASE(14) BL_CASE(15)
     BL_CASE(16)
@@ -291,5 +638,21 @@ hipError_t launch_head(const uint64_t *bits, int32_t w, int64_t n, int32_t c,
 }
 
 static_assert(kMaxPlanes == 16, "plane count switch covers 1..16");
+
+hipError_t launch_grouped_dsp(const int32_t *counts, int64_t n, int32_t c,
+                              const int8_t *weights, int32_t *logits, int32_t *argmax,
+                              hipStream_t stream)
+{
+    const int64_t mtiles = (n + 15) / 16;
+    const int64_t want = (mtiles + kWaves - 1) / kWaves;
+    const int64_t blocks = want < kDspBlocks ? want : kDspBlocks;
+    if (c < 1 || c > kDspMaxClasses)
+        return hipErrorInvalidConfiguration;
+    // only Q and its row sums in LDS
+    const DspLayout L = dsp_layout(c);
+    hipLaunchKernelGGL(k_grouped_dsp, dim3((unsigned)blocks), dim3(kThreads), L.off_lo, stream,
+                       counts, n, c, weights, logits, argmax);
+    return hipGetLastError();
+}
 
 }  // namespace bl

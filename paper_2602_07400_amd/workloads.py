@@ -112,6 +112,7 @@ class Workload:
     layers: List[Tuple[np.ndarray, np.ndarray]]   # [(conn int32 [w][k], tables uint64 [w])]
     labels: Optional[np.ndarray] = None
     seed: int = 0
+    dsp_weights: Optional[np.ndarray] = None   # int8 [c][c], quantized head weights
 
     @property
     def n_classes(self) -> int:
@@ -123,8 +124,10 @@ class Workload:
 
 
 def _streams(seed: int, name: str, n_layers: int):
+    # slots: pixels, prototypes, training split, (conn, tables) per layer, then
+    # the quantized head's weights (appended last, so the others keep their draws)
     root = np.random.SeedSequence([seed, zlib.crc32(name.encode())])
-    return root.spawn(_S_LAYERS + 2 * n_layers)
+    return root.spawn(_S_LAYERS + 2 * n_layers + 1)
 
 
 def uniform_thresholds(d: int, b: int) -> np.ndarray:
@@ -210,6 +213,12 @@ def draw_tables(rng: np.random.Generator, w: int, k: int) -> np.ndarray:
     return t
 
 
+def draw_dsp_weights(rng: np.random.Generator, c: int) -> np.ndarray:
+    """c x c weights of the quantized head, uniform on the signed 8-bit grid
+    [-127, 127] that trained weights are snapped to."""
+    return rng.integers(-127, 128, size=(c, c)).astype(np.int8)
+
+
 def make_workload(name_or_cfg, seed: int = 0, n: Optional[int] = None) -> Workload:
     """Draw the inputs of one configuration.
 
@@ -238,4 +247,5 @@ def make_workload(name_or_cfg, seed: int = 0, n: Optional[int] = None) -> Worklo
         tables = draw_tables(rngs[_S_LAYERS + 2 * l + 1], w, cfg.k)
         layers.append((conn, tables))
         w_in = w
-    return Workload(cfg, x, th, layers, labels, seed)
+    dsp = draw_dsp_weights(rngs[_S_LAYERS + 2 * L], cfg.n_classes)
+    return Workload(cfg, x, th, layers, labels, seed, dsp)

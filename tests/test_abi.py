@@ -189,3 +189,30 @@ def test_forward_plan(lib, monkeypatch):
     assert lib.bitlogic_forward_plan(4096, 784, 1, p, 2, 10, None) == ENULL
     assert lib.bitlogic_forward_plan(4096, 784, 1, p, 2, 7, ref) == ESHAPE
     assert lib.bitlogic_forward_plan(4096, 784, 1, None, 2, 10, ref) == ENULL
+
+
+def test_grouped_dsp_validation(lib):
+    f = lib.bitlogic_grouped_dsp_head
+    assert f(None, 64, 10, FAKE, FAKE, FAKE, None) == ENULL
+    assert f(FAKE, 64, 10, None, FAKE, FAKE, None) == ENULL
+    assert f(FAKE, 64, 10, FAKE, None, None, None) == ENULL
+    assert f(FAKE, -1, 10, FAKE, FAKE, FAKE, None) == ESHAPE
+    assert f(FAKE, 64, 0, FAKE, FAKE, FAKE, None) == ESHAPE
+    assert f(FAKE, 64, 129, FAKE, FAKE, FAKE, None) == EUNSUP
+    assert "128" in _err(lib)
+    assert f(FAKE + 2, 64, 10, FAKE, FAKE, FAKE, None) == EALIGN
+    assert f(FAKE, 0, 10, FAKE, FAKE, FAKE, None) == OK        # nothing to do
+
+
+def test_forward_grouped_dsp_validation(lib):
+    p, keep = _layers([(1000, 6), (1000, 6)])
+    need = lib.bitlogic_forward_workspace_bytes(4096, 784, 1, p, 2, 10)
+    args = lambda **o: [FAKE, o.get("n", 4096), 784, FAKE, 1, p, 2, o.get("c", 10),
+                        o.get("w", FAKE), FAKE, FAKE, FAKE * 16, need, None]
+    f = lib.bitlogic_forward_grouped_dsp
+    assert f(*args(w=None)) == ENULL
+    assert f(*args(c=7)) == ESHAPE                      # 1000 nodes do not split into 7 groups
+    p2, keep2 = _layers([(1000, 6), (250 * 4 * 129 // 129 * 129, 6)])
+    assert f(FAKE, 4096, 784, FAKE, 1, p2, 2, 129, FAKE, FAKE, FAKE, FAKE * 16, 1 << 40,
+             None) == EUNSUP
+    assert f(*args(n=0)) == OK
