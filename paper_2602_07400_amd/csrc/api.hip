@@ -158,10 +158,14 @@ int plan_forward(int64_t n, int32_t d, int32_t b, const bitlogic_layer *layers, 
     const int32_t nb = bl::fused_head_nodes(w_last / c);
     fp->fused = nb > 0 && fused_head_enabled();
     fp->head = fp->fused ? bl::plan_fused_head(w_last, n, c, nb) : bl::plan_head(w_last, n, c);
+    // layer l writes activation buffer l % 2, except a last layer fused with
+    // the head, which writes nothing: allocate only the buffers some layer writes
+    const int32_t stored = fp->fused ? L - 1 : L;     // layers whose bits are stored
+    const bool need_a = stored >= 1, need_b = stored >= 2;
     fp->off_enc = 0;
     fp->off_a = round_up(enc);
-    fp->off_b = fp->off_a + round_up(act);
-    fp->off_head = fp->off_b + (L > 1 ? round_up(act) : 0);
+    fp->off_b = fp->off_a + (need_a ? round_up(act) : 0);
+    fp->off_head = fp->off_b + (need_b ? round_up(act) : 0);
     fp->total = fp->off_head + round_up(fp->head.ws_bytes);
     return BITLOGIC_OK;
 }
