@@ -2,8 +2,10 @@
 
 Python front end of ``bitlogic_oracle.c``: a plain per-sample C implementation
 of the paper's forward pass (thermometer encoder, LUT layers, GroupSum head and
-argmax; Sec. 3 Eq. 1, App. C.1) on unpacked bytes, and of the quantized
-(DSP-backed) class head on the group sums (Sec. 3; Sec. 5 "Head").  Only ``tests/``,
+argmax; Sec. 3 Eq. 1, App. C.1) on unpacked bytes, of the quantized
+(DSP-backed) class head on the group sums (Sec. 3; Sec. 5 "Head"), of the
+binary-coded encoder (Sec. 3; Sec. 5 "Encoder") and of quantile-threshold
+fitting (Sec. 4 "Initialization"; App. B).  Only ``tests/``,
 ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of ``bench.py`` may
 import it.  The product library (``paper_2602_07400_amd``) never imports,
 links or calls anything here, and the two share no code.
@@ -50,9 +52,14 @@ def _load():
         lib.oracle_forward.argtypes = [P, i64, i32, P, i32, i32, P, P, P, P,
                                        i32, P, P, i32]
         lib.oracle_grouped_dsp.argtypes = [P, i64, i32, P, P, P]
+        lib.oracle_encode_binary.argtypes = [P, i64, i32, i32, P]
+        lib.oracle_fit_quantiles.argtypes = [P, i64, i32, i32, i32, P]
+        lib.oracle_forward_binary.argtypes = [P, i64, i32, i32, i32, P, P, P, P, i32, P, P, i32]
         lib.oracle_max_threads.argtypes = []
         for f in (lib.oracle_encode, lib.oracle_lut_layer, lib.oracle_groupsum,
-                  lib.oracle_grouped_dsp, lib.oracle_forward, lib.oracle_max_threads):
+                  lib.oracle_grouped_dsp, lib.oracle_forward, lib.oracle_max_threads,
+                  lib.oracle_encode_binary, lib.oracle_fit_quantiles,
+                  lib.oracle_forward_binary):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -108,6 +115,27 @@ def groupsum(v: np.ndarray, n_classes: int):
     return scores, pred
 
 
+def encode_binary(x: np.ndarray, n_bits: int) -> np.ndarray:
+    """Binary-coded encoder: x uint8 [n][d] -> wires uint8 [n][d*b], wire f*b+t = bit t
+    of round(x * (2^b - 1) / 255)."""
+    x = np.ascontiguousarray(x, dtype=np.uint8)
+    n, d = x.shape
+    e = np.empty((n, d * n_bits), dtype=np.uint8)
+    _check(_load().oracle_encode_binary(_ptr(x), n, d, n_bits, _ptr(e)), "encode_binary")
+    return e
+
+
+def fit_quantiles(x: np.ndarray, n_bits: int, n_groups: int = 1) -> np.ndarray:
+    """Quantile thermometer thresholds fitted from x uint8 [n][d]: th uint8 [d][b], one
+    ladder per contiguous group of d / n_groups features."""
+    x = np.ascontiguousarray(x, dtype=np.uint8)
+    n, d = x.shape
+    th = np.empty((d, n_bits), dtype=np.uint8)
+    _check(_load().oracle_fit_quantiles(_ptr(x), n, d, n_bits, n_groups, _ptr(th)),
+           "fit_quantiles")
+    return th
+
+
 def grouped_dsp(counts: np.ndarray, weights: np.ndarray):
     """Quantized head: counts int32 [n][c], weights int8 [c][c] ->
     (logits int64 [n][c], pred int32 [n]); logit i = sum_j weights[i][j] * counts[j]."""
@@ -122,16 +150,21 @@ def grouped_dsp(counts: np.ndarray, weights: np.ndarray):
     return logits, pred
 
 
-def forward(x: np.ndarray, thresholds: np.ndarray, layers, n_classes: int,
-            n_threads: int = 0):
+def forward(x: np.ndarray, thresholds, layers, n_classes: int,
+            n_threads: int = 0, binary_bits: int = 0):
     """Whole forward, per sample.  layers = [(conn int32 [w][k], tables uint64 [w]), ...].
+    With binary_bits > 0 the binary-coded encoder replaces the thermometer
+    (thresholds is then ignored).
 
     Returns (scores int32 [n][c], pred int32 [n]).
     """
     x = np.ascontiguousarray(x, dtype=np.uint8)
-    th = np.ascontiguousarray(thresholds, dtype=np.uint8)
     n, d = x.shape
-    b = th.shape[1]
+    if binary_bits:
+        th, b = None, int(binary_bits)
+    else:
+        th = np.ascontiguousarray(thresholds, dtype=np.uint8)
+        b = th.shape[1]
     conns = [np.ascontiguousarray(c, dtype=np.int32) for c, _ in layers]
     tabs = [np.ascontiguousarray(t, dtype=np.uint64) for _, t in layers]
     L = len(layers)
@@ -141,11 +174,13 @@ def forward(x: np.ndarray, thresholds: np.ndarray, layers, n_classes: int,
     ks = (ctypes.c_int32 * L)(*[c.shape[1] for c in conns])
     scores = np.empty((n, n_classes), dtype=np.int32)
     pred = np.empty((n,), dtype=np.int32)
-    _check(_load().oracle_forward(_ptr(x), n, d, _ptr(th), b, L,
-                                  ctypes.cast(conn_p, ctypes.c_void_p),
-                                  ctypes.cast(tab_p, ctypes.c_void_p),
-                                  ctypes.cast(w_out, ctypes.c_void_p),
-                                  ctypes.cast(ks, ctypes.c_void_p),
-                                  n_classes, _ptr(scores), _ptr(pred), n_threads),
-           "forward")
+    ptrs = [ctypes.cast(conn_p, ctypes.c_void_p), ctypes.cast(tab_p, ctypes.c_void_p),
+            ctypes.cast(w_out, ctypes.c_void_p), ctypes.cast(ks, ctypes.c_void_p)]
+    if th is None:
+        rc = _load().oracle_forward_binary(_ptr(x), n, d, b, L, *ptrs, n_classes, _ptr(scores),
+                                           _ptr(pred), n_threads)
+    else:
+        rc = _load().oracle_forward(_ptr(x), n, d, _ptr(th), b, L, *ptrs, n_classes,
+                                    _ptr(scores), _ptr(pred), n_threads)
+    _check(rc, "forward")
     return scores, pred

@@ -23,6 +23,12 @@
  *             and heads"; Sec. 5 "Head")
  *   DSP head  c x c signed 8-bit matrix on the group sums  (Sec. 3, "Encoders
  *             and heads"; Sec. 5 "Head", head sweep table)
+ *   Binary    uniform fixed-point code, 2^b levels on b    (Sec. 3, "Encoders
+ *   encoder   wires                                        and heads"; Sec. 5
+ *                                                          "Encoder")
+ *   Quantile  thresholds fitted from the data's quantiles  (Sec. 4
+ *   fitting                                                "Initialization";
+ *                                                          App. B)
  *   Argmax    predicted class index                        (App. C.2 "HDL
  *             export and emission modes": the top module outputs it)
  *
@@ -60,6 +66,22 @@ static void encode_one(const uint8_t *x_row, int32_t d, const uint8_t *theta,
     for (int32_t f = 0; f < d; ++f)
         for (int32_t t = 0; t < b; ++t)
             e[(int64_t)f * b + t] = (x_row[f] > theta[(int64_t)f * b + t]) ? 1 : 0;
+}
+
+/* Binary-coded uniform fixed-point encoder of one sample (Sec. 3 "Encoders and
+ * heads": the integer quantizer with 2^b levels on b wires; Sec. 5 "Encoder",
+ * the encoder sweep table).  The pixel v/255 in [0, 1] is quantized to the
+ * nearest of the 2^b equispaced levels q/(2^b - 1), q = round(v (2^b-1) / 255)
+ * (no ties occur: 255 is odd), and wire (f, t) carries bit t of q, least
+ * significant first. */
+static void encode_binary_one(const uint8_t *x_row, int32_t d, int32_t b, uint8_t *e)
+{
+    const int64_t top = ((int64_t)1 << b) - 1;
+    for (int32_t f = 0; f < d; ++f) {
+        const int64_t q = (2 * (int64_t)x_row[f] * top + 255) / 510;
+        for (int32_t t = 0; t < b; ++t)
+            e[(int64_t)f * b + t] = (uint8_t)((q >> t) & 1);
+    }
 }
 
 /* One LUT layer on one sample (Sec. 3, connection map M_j and the 2^n-entry
@@ -182,6 +204,53 @@ int oracle_groupsum(const uint8_t *v, int64_t n, int32_t w, int32_t c,
     return ORACLE_OK;
 }
 
+/* e [n][d*b] bytes, binary-coded encoder, 1 <= b <= 16 */
+int oracle_encode_binary(const uint8_t *x, int64_t n, int32_t d, int32_t b, uint8_t *e)
+{
+    if (!x || !e || n < 0 || d <= 0 || b < 1 || b > 16)
+        return ORACLE_ERR_ARG;
+    for (int64_t s = 0; s < n; ++s)
+        encode_binary_one(x + s * d, d, b, e + s * (int64_t)d * b);
+    return ORACLE_OK;
+}
+
+/* Quantile thermometer thresholds fitted from data (Sec. 4 "Initialization":
+ * fitted once from the empirical pixel quantiles of the training split;
+ * App. B: over the flattened pixel distribution).  The d features are cut
+ * into n_groups contiguous groups of d / n_groups features (1 group: the
+ * whole flattened distribution; one group per colour channel for CHW
+ * images); in each group, with cum(v) = number of pixels <= v among the
+ * group's n * d / n_groups pixels, threshold i (i = 1..b) is the smallest v
+ * with cum(v) / total >= i / (b + 1), compared exactly in integers.  Every
+ * feature of the group receives the group's b thresholds: th [d][b]. */
+int oracle_fit_quantiles(const uint8_t *x, int64_t n, int32_t d, int32_t b, int32_t n_groups,
+                         uint8_t *th)
+{
+    if (!x || !th || n <= 0 || d <= 0 || b < 1 || b > 64 || n_groups < 1 || d % n_groups != 0)
+        return ORACLE_ERR_ARG;
+    const int32_t per = d / n_groups;
+    for (int32_t grp = 0; grp < n_groups; ++grp) {
+        int64_t hist[256];
+        memset(hist, 0, sizeof hist);
+        for (int64_t s = 0; s < n; ++s)
+            for (int32_t f = grp * per; f < (grp + 1) * per; ++f)
+                hist[x[s * d + f]] += 1;
+        const int64_t total = n * per;
+        for (int32_t i = 1; i <= b; ++i) {
+            int64_t cum = 0;
+            int32_t v = 0;
+            for (v = 0; v < 256; ++v) {
+                cum += hist[v];
+                if (cum * (b + 1) >= (int64_t)i * total)
+                    break;
+            }
+            for (int32_t f = grp * per; f < (grp + 1) * per; ++f)
+                th[(int64_t)f * b + (i - 1)] = (uint8_t)v;
+        }
+    }
+    return ORACLE_OK;
+}
+
 /* counts [n][c] int32, q [c][c] int8 -> logits [n][c] int64, pred [n] */
 int oracle_grouped_dsp(const int32_t *counts, int64_t n, int32_t c, const int8_t *q,
                        int64_t *logits, int32_t *pred)
@@ -196,13 +265,44 @@ int oracle_grouped_dsp(const int32_t *counts, int64_t n, int32_t c, const int8_t
 /* Whole forward, one sample at a time, OpenMP over samples.
  * conn[l] [w_out[l]][k[l]], tables[l] [w_out[l]]; layer 0 reads the d*b
  * encoder wires, layer l > 0 reads layer l-1. */
+static int forward_impl(const uint8_t *x, int64_t n, int32_t d, const uint8_t *theta,
+                        int32_t b, int binary, int32_t n_layers, const int32_t *const *conn,
+                        const uint64_t *const *tables, const int32_t *w_out,
+                        const int32_t *k, int32_t c, int32_t *scores, int32_t *pred,
+                        int32_t n_threads);
+
 int oracle_forward(const uint8_t *x, int64_t n, int32_t d, const uint8_t *theta,
                    int32_t b, int32_t n_layers, const int32_t *const *conn,
                    const uint64_t *const *tables, const int32_t *w_out,
                    const int32_t *k, int32_t c, int32_t *scores, int32_t *pred,
                    int32_t n_threads)
 {
-    if (!x || !theta || !conn || !tables || !w_out || !k || !scores || !pred ||
+    if (!theta)
+        return ORACLE_ERR_ARG;
+    return forward_impl(x, n, d, theta, b, 0, n_layers, conn, tables, w_out, k, c, scores,
+                        pred, n_threads);
+}
+
+/* The forward with the binary-coded encoder (b code bits per feature). */
+int oracle_forward_binary(const uint8_t *x, int64_t n, int32_t d, int32_t b,
+                          int32_t n_layers, const int32_t *const *conn,
+                          const uint64_t *const *tables, const int32_t *w_out,
+                          const int32_t *k, int32_t c, int32_t *scores, int32_t *pred,
+                          int32_t n_threads)
+{
+    if (b > 16)
+        return ORACLE_ERR_ARG;
+    return forward_impl(x, n, d, NULL, b, 1, n_layers, conn, tables, w_out, k, c, scores, pred,
+                        n_threads);
+}
+
+static int forward_impl(const uint8_t *x, int64_t n, int32_t d, const uint8_t *theta,
+                        int32_t b, int binary, int32_t n_layers, const int32_t *const *conn,
+                        const uint64_t *const *tables, const int32_t *w_out,
+                        const int32_t *k, int32_t c, int32_t *scores, int32_t *pred,
+                        int32_t n_threads)
+{
+    if (!x || !conn || !tables || !w_out || !k || !scores || !pred ||
         n < 0 || d <= 0 || b <= 0 || n_layers < 1 || c <= 0)
         return ORACLE_ERR_ARG;
     int32_t w_in = d * b, widest = d * b;
@@ -230,7 +330,10 @@ int oracle_forward(const uint8_t *x, int64_t n, int32_t d, const uint8_t *theta,
         } else {
 #pragma omp for schedule(dynamic, 16)
             for (int64_t s = 0; s < n; ++s) {
-                encode_one(x + s * d, d, theta, b, cur);
+                if (binary)
+                    encode_binary_one(x + s * d, d, b, cur);
+                else
+                    encode_one(x + s * d, d, theta, b, cur);
                 for (int32_t l = 0; l < n_layers; ++l) {
                     layer_one(cur, conn[l], tables[l], w_out[l], k[l], nxt);
                     uint8_t *t = cur; cur = nxt; nxt = t;

@@ -392,3 +392,111 @@ def test_grouped_dsp_extremes_exact():
     ln, pred = oracle.grouped_dsp(counts, np.full((c, c), -128, np.int8))
     assert (lp == 100 * 127 * 65535).all() and (ln == -100 * 128 * 65535).all()
     assert (pred == 0).all()          # all logits equal: lowest index
+
+
+# ---------------------------------------------------------------------------
+# Binary-coded uniform fixed-point encoder (Sec. 3 "Encoders and heads";
+# Sec. 5 "Encoder") and quantile-threshold fitting (Sec. 4 "Initialization";
+# App. B)
+
+def _binary_golden():
+    rows = []
+    for line in open(os.path.join(GOLDEN, "binary_encoder.txt")):
+        line = line.strip()
+        if not line or line.startswith("#"):
+            continue
+        b, v, bits = line.split()
+        rows.append((int(b), int(v), [int(ch) for ch in bits]))
+    return rows
+
+
+def test_binary_encoder_golden():
+    rows = _binary_golden()
+    assert len(rows) >= 18
+    for b, v, bits in rows:
+        e = oracle.encode_binary(np.array([[v]], np.uint8), b)
+        assert e[0].tolist() == bits, (b, v)
+
+
+@pytest.mark.parametrize("b", range(1, 9))
+def test_binary_encoder_levels_and_exact_rounding(b):
+    from fractions import Fraction
+    v = np.arange(256, dtype=np.uint8)[:, None]
+    e = oracle.encode_binary(v, b)                       # [256][b]
+    q = (e.astype(np.int64) << np.arange(b)).sum(axis=1)
+    # the paper's count: 2^b distinct levels, in order, from 0 to 2^b - 1
+    assert len(set(q.tolist())) == 2 ** b
+    assert (np.diff(q) >= 0).all() and q[0] == 0 and q[255] == 2 ** b - 1
+    top = 2 ** b - 1
+    for val in range(256):
+        exact = Fraction(val * top, 255)
+        lo = exact.numerator // exact.denominator
+        assert exact - lo != Fraction(1, 2)                 # no ties
+        assert q[val] == (lo + 1 if exact - lo > Fraction(1, 2) else lo)
+
+
+def test_binary_encoder_special_cases():
+    rng = np.random.default_rng(7)
+    x = rng.integers(0, 256, size=(50, 13), dtype=np.uint8)
+    # b = 8 is the pixel's own binary expansion
+    e8 = oracle.encode_binary(x, 8).reshape(50, 13, 8)
+    assert np.array_equal((e8.astype(np.int64) << np.arange(8)).sum(axis=2), x)
+    # b = 1 is the thermometer bit x > 127
+    assert np.array_equal(oracle.encode_binary(x, 1),
+                          oracle.encode(x, np.full((13, 1), 127, np.uint8)))
+
+
+def test_forward_binary_equals_staged():
+    rng = np.random.default_rng(8)
+    n, d, b, c = 300, 20, 3, 4
+    x = rng.integers(0, 256, size=(n, d), dtype=np.uint8)
+    layers, w_in = [], d * b
+    for w in (40, 24):
+        conn = np.stack([rng.choice(w_in, 6, replace=False) for _ in range(w)]).astype(np.int32)
+        layers.append((conn, rng.integers(0, 2**63, size=w).astype(np.uint64)))
+        w_in = w
+    s, p = oracle.forward(x, None, layers, c, binary_bits=b)
+    v = oracle.encode_binary(x, b)
+    for conn, tab in layers:
+        v = oracle.lut_layer(v, conn, tab)
+    s2, p2 = oracle.groupsum(v, c)
+    assert np.array_equal(s, s2) and np.array_equal(p, p2)
+
+
+@pytest.mark.parametrize("b", [1, 3, 4, 7, 8, 15])
+def test_fit_quantiles_uniform_closed_form(b):
+    # every pixel value equally often: the smallest v with (v+1)/256 >= i/(b+1)
+    x = np.tile(np.arange(256, dtype=np.uint8), 12).reshape(-1, 4)    # 768 x 4
+    th = oracle.fit_quantiles(x, b)
+    want = [-(-256 * i // (b + 1)) - 1 for i in range(1, b + 1)]
+    assert (th == np.array(want, np.uint8)).all()
+
+
+def test_fit_quantiles_mnist_collapse():
+    # App. B: on MNIST's pixels a point mass at 0 exceeds the 88 % quantile; at
+    # b = 4 all thresholds are 0, at b = 8 seven are 0 and the last ~0.706
+    # (180 on the 0..255 scale).  Synthetic data with that shape: 88.5 % zeros,
+    # the rest at 180.
+    n = 2000
+    x = np.zeros((n, 100), np.uint8)
+    flat = x.reshape(-1)
+    flat[: int(0.115 * flat.size)] = 180
+    np.random.default_rng(0).shuffle(flat)
+    assert (oracle.fit_quantiles(x, 4) == 0).all()
+    th8 = oracle.fit_quantiles(x, 8)
+    assert (th8[:, :7] == 0).all() and (th8[:, 7] == 180).all()
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_fit_quantiles_order_statistics(seed):
+    rng = np.random.default_rng(seed)
+    n, d, groups, b = 37, 12, 3, 5
+    x = rng.integers(0, 256, size=(n, d), dtype=np.uint8)
+    th = oracle.fit_quantiles(x, b, groups)
+    per = d // groups
+    for g in range(groups):
+        vals = np.sort(x[:, g * per:(g + 1) * per].ravel())
+        for i in range(1, b + 1):
+            k = -(-i * vals.size // (b + 1))                  # ceil(i * total / (b+1))
+            assert (th[g * per:(g + 1) * per, i - 1] == vals[k - 1]).all()
+    assert (np.diff(th.astype(int), axis=1) >= 0).all()
