@@ -58,16 +58,21 @@ def parse():
     ap.add_argument("--head", choices=["groupsum", "dsp"], default="groupsum",
                     help="class head of the timed forward: the popcount GroupSum, or the "
                          "quantized c x c head on the group sums (bitlogic_forward_grouped_dsp)")
+    ap.add_argument("--encoder", choices=["thermometer", "binary"], default="thermometer",
+                    help="input encoder: the configuration's thermometer, or the binary-coded "
+                         "uniform fixed-point code (layer 1 is redrawn if the wire count changes)")
+    ap.add_argument("--bits", type=int, default=None,
+                    help="code width of the binary encoder (default: the configuration's b)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run a write-only fill and a read-only sum over this many MiB "
                          "(reference kernels for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     return ap.parse_args()
 
 
-def algorithmic(cfg, n, fused_head):
+def algorithmic(cfg, n, fused_head, binary_bits=0):
     """Compulsory bytes and algorithmic 32-bit lane-ops per stage of one forward."""
     W = (n + 63) // 64
-    D0 = cfg.d * cfg.b
+    D0 = cfg.d * (binary_bits or cfg.b)
     st = {"encode": {"bytes": n * cfg.d + D0 * W * 8, "ops": n * D0}}
     w_in = D0
     L = len(cfg.widths)
@@ -136,23 +141,31 @@ def main():
     print(f"[bench] {cfg.name}: generated inputs in {time.time() - t0:.1f}s", file=sys.stderr,
           flush=True)
     n = wl.n
-    model = bl.BitlogicModel.from_numpy(wl.thresholds, wl.layers, wl.n_classes, device=dev)
+    binary_bits = 0
+    if args.encoder == "binary":
+        binary_bits = args.bits or cfg.b
+        if cfg.d * binary_bits != cfg.wires:
+            # another wire count: layer 1 reads the binary wires (seeded redraw)
+            from paper_2602_07400_amd.workloads import draw_connectivity
+            rng = np.random.default_rng([args.seed, binary_bits, 1])
+            conn0, tab0 = wl.layers[0]
+            wl.layers[0] = (draw_connectivity(rng, conn0.shape[0], cfg.k, cfg.d * binary_bits),
+                            tab0)
+    dsp_np = wl.dsp_weights if args.head == "dsp" else None
+    model = bl.BitlogicModel.from_numpy(None if binary_bits else wl.thresholds, wl.layers,
+                                        wl.n_classes, device=dev,
+                                        encoder="binary" if binary_bits else "thermometer",
+                                        n_features=cfg.d, n_bits=binary_bits or None,
+                                        head_weights=dsp_np)
+    dsp_w = model.head_weights
     x = torch.from_numpy(wl.x).to(dev)
     ws = torch.empty(model.workspace_bytes(n), dtype=torch.uint8, device=dev)
     scores = torch.empty((n, cfg.n_classes), dtype=torch.int32, device=dev)
     argmax = torch.empty((n,), dtype=torch.int32, device=dev)
     stream = torch.cuda.current_stream(dev)
 
-    dsp_w = torch.from_numpy(wl.dsp_weights).to(dev) if args.head == "dsp" else None
-
-    def step():
-        if dsp_w is None:
-            bl.bitlogic_forward(x, model.thresholds, model.layers, model.n_classes,
-                                scores=scores, argmax=argmax, workspace=ws, stream=stream)
-        else:
-            bl.bitlogic_forward_grouped_dsp(x, model.thresholds, model.layers, model.n_classes,
-                                            dsp_w, logits=scores, argmax=argmax, workspace=ws,
-                                            stream=stream)
+    def step(events=None):
+        model.forward(x, out=scores, argmax=argmax, workspace=ws, stream=stream, events=events)
 
     if args.calibrate_copy_mib:
         # reference kernels of known traffic for scaling rocprofv3's
@@ -193,8 +206,7 @@ def main():
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
         for e in ev:
             e.record(stream)          # creates the HIP event handles
-        bl.bitlogic_forward_timed(x, model.thresholds, model.layers, model.n_classes, ev,
-                                  scores=scores, argmax=argmax, workspace=ws, stream=stream)
+        step(ev)
         torch.cuda.synchronize()
         if it >= 2:                   # two untimed passes first
             sums += [ev[i].elapsed_time(ev[i + 1]) for i in range(len(names))]
@@ -205,8 +217,9 @@ def main():
         # the quantized head alone, on the group sums of this batch: HIP events
         # on the launch stream around repeated calls
         counts = torch.empty((n, cfg.n_classes), dtype=torch.int32, device=dev)
-        bl.bitlogic_forward(x, model.thresholds, model.layers, model.n_classes, scores=counts,
-                            argmax=argmax, workspace=ws, stream=stream)
+        plain = bl.BitlogicModel(model.thresholds, model.layers, model.n_classes, model.n_features,
+                                 model.encoder, model.n_bits)
+        plain.forward(x, out=counts, argmax=argmax, workspace=ws, stream=stream)
         lg = torch.empty_like(counts)
         reps = max(ksteps, 10)
         for _ in range(3):
@@ -228,9 +241,33 @@ def main():
                       "frac_of_hbm_peak": round(hb / (t_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
                       "achieved_int8_TOPs": round(hops / (t_ms * 1e-3) / 1e12, 3)}
 
+    # quantile-threshold fitting on the device over this batch: HBM-bound
+    # (reads N*d pixel bytes); per-channel groups for 3-channel images
+    groups = cfg.channels if cfg.d % max(cfg.channels, 1) == 0 else 1
+    th_fit = torch.empty((cfg.d, cfg.b), dtype=torch.uint8, device=dev)
+    fit_ws = torch.empty(max(8, groups * 256 * 8), dtype=torch.uint8, device=dev)
+    for _ in range(2):
+        bl.bitlogic_fit_quantile_thresholds(x, cfg.b, groups, out=th_fit, workspace=fit_ws,
+                                            stream=stream)
+    f0 = torch.cuda.Event(enable_timing=True)
+    f1 = torch.cuda.Event(enable_timing=True)
+    f0.record(stream)
+    for _ in range(5):
+        bl.bitlogic_fit_quantile_thresholds(x, cfg.b, groups, out=th_fit, workspace=fit_ws,
+                                            stream=stream)
+    f1.record(stream)
+    torch.cuda.synchronize()
+    fit_ms = f0.elapsed_time(f1) / 5
+    fit_detail = {"kernels": "k_fit_clear + k_fit_hist + k_fit_select "
+                             "(bitlogic_fit_quantile_thresholds)",
+                  "groups": groups, "thresholds": cfg.b, "ms": round(fit_ms, 4),
+                  "bytes": n * cfg.d,
+                  "achieved_GBs": round(n * cfg.d / (fit_ms * 1e-3) / 1e9, 1),
+                  "frac_of_hbm_peak": round(n * cfg.d / (fit_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+
     plan = model.plan(n)
     fused = plan["fused_head"]
-    alg = algorithmic(cfg, n, fused)
+    alg = algorithmic(cfg, n, fused, binary_bits)
     roof_sum = sum(v["roof_ms"] for v in alg.values())
     # dominant kernel: the stage with the longest launch
     dom = max(names, key=lambda k: stage_ms[k])
@@ -268,7 +305,9 @@ def main():
         "staged_sum_ms": round(sum(stage_ms.values()), 4),
         "fused_head": fused,
         "head": args.head,
+        "encoder": args.encoder + (f" ({binary_bits} bits)" if binary_bits else ""),
         "grouped_dsp_head": dsp_detail,
+        "fit_quantile_thresholds": fit_detail,
         "layer_frac_of_valu_peak": {k: round(alg[k]["ops"] / (stage_ms[k] * 1e-3) / 1e12
                                              / PEAK_VALU_TOPS, 4) for k in layer_names},
         "gpu": torch.cuda.get_device_name(dev),
@@ -284,14 +323,16 @@ def main():
         threads = oracle.max_threads()
         probe = min(n, 2048)
         t0 = time.perf_counter()
-        oracle.forward(wl.x[:probe], wl.thresholds, wl.layers, wl.n_classes)
+        oracle.forward(wl.x[:probe], wl.thresholds, wl.layers, wl.n_classes,
+                       binary_bits=binary_bits)
         per = (time.perf_counter() - t0) / probe
         m = int(min(n, max(probe, args.cpu_seconds / max(per, 1e-9))))
         idx = np.random.default_rng(1).choice(n, size=m, replace=False)
         idx.sort()
         xs = np.ascontiguousarray(wl.x[idx])
         t0 = time.perf_counter()
-        rs, rp = oracle.forward(xs, wl.thresholds, wl.layers, wl.n_classes)
+        rs, rp = oracle.forward(xs, wl.thresholds, wl.layers, wl.n_classes,
+                                binary_bits=binary_bits)
         if dsp_w is not None:
             rs, rp = oracle.grouped_dsp(rs, wl.dsp_weights)
         cpu_s = time.perf_counter() - t0
@@ -318,9 +359,12 @@ def main():
         "vs_baseline": None,
         "dtype": "u64 (bitwise on packed 64-sample words; u8 pixels, i32 scores)",
         "data": "synthetic",
-        "config": {"workload": cfg.description + ("" if dsp_w is None else
-                                                     "; quantized c x c head on the group sums"),
-                   "name": cfg.name, "head": args.head, "n_samples": n,
+        "config": {"workload": cfg.description
+                   + ("" if not binary_bits else
+                      f"; binary-coded {binary_bits}-bit encoder instead of the thermometer")
+                   + ("" if dsp_w is None else "; quantized c x c head on the group sums"),
+                   "name": cfg.name, "head": args.head, "encoder": args.encoder,
+                   "n_samples": n,
                    "features": cfg.d, "thresholds": cfg.b, "widths": list(cfg.widths),
                    "k": cfg.k, "classes": cfg.n_classes, "seed": args.seed},
         "roofline": roofline,

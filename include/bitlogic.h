@@ -216,6 +216,82 @@ int bitlogic_forward_grouped_dsp(const uint8_t *x, int64_t n_samples, int32_t n_
                                  int32_t *argmax, void *workspace, size_t workspace_bytes,
                                  void *stream);
 
+/* ---- Encoder family and quantile fitting -------------------------------- */
+
+/* Binary-coded uniform fixed-point encoder (Sec. 3 "Encoders and heads": the
+ * integer quantizer with 2^b levels on b wires; Sec. 5 "Encoder", the encoder
+ * sweep table).  Pixel v (0..255, read as v/255 in [0, 1]) is quantized to
+ * the nearest of 2^b equispaced levels, q = round(v * (2^b - 1) / 255) (no
+ * ties occur), and wire f * n_bits + t carries bit t of q, least significant
+ * first:
+ *     bit (s % 64) of bits_out[f * n_bits + t][s / 64] = (q(x[s][f]) >> t) & 1
+ * Layout, padding and alignment as bitlogic_encode; 1 <= n_bits <= 8. */
+int bitlogic_encode_binary(const uint8_t *x, int64_t n_samples, int32_t n_features,
+                           int32_t n_bits, uint64_t *bits_out, void *stream);
+
+/* Quantile thermometer thresholds fitted from data (Sec. 4 "Initialization":
+ * fitted once from the empirical pixel quantiles of the training split;
+ * App. B: over the flattened pixel distribution).  The n_features features
+ * are cut into n_groups contiguous groups of n_features / n_groups (1: the
+ * whole flattened distribution; 3 for CHW colour images: one ladder per
+ * channel).  For each group, with cum(v) = number of its pixels <= v and
+ * total = n_samples * n_features / n_groups, threshold i (i = 1..b) is the
+ * smallest v with (b + 1) * cum(v) >= i * total, and every feature of the
+ * group gets that ladder:
+ *   x               [n_samples][n_features] uint8 pixels (device)
+ *   thresholds_out  [n_features][n_thresholds] uint8 (device), ready for
+ *                   bitlogic_encode / bitlogic_forward
+ *   workspace       bitlogic_fit_quantile_thresholds_workspace_bytes(n_groups)
+ *                   bytes of device memory, 8-byte aligned (a histogram)
+ * Needs n_samples >= 1, 1 <= n_thresholds <= 64, 1 <= n_groups <= 32,
+ * n_features % n_groups == 0 and n_samples * n_features <= 2^56. */
+size_t bitlogic_fit_quantile_thresholds_workspace_bytes(int32_t n_groups);
+int bitlogic_fit_quantile_thresholds(const uint8_t *x, int64_t n_samples, int32_t n_features,
+                                     int32_t n_thresholds, int32_t n_groups,
+                                     uint8_t *thresholds_out, void *workspace,
+                                     size_t workspace_bytes, void *stream);
+
+/* ---- Network descriptor: any encoder, any head --------------------------- */
+
+enum { BITLOGIC_ENCODER_THERMOMETER = 0, BITLOGIC_ENCODER_BINARY = 1 };
+enum { BITLOGIC_HEAD_GROUPSUM = 0, BITLOGIC_HEAD_GROUPED_DSP = 1 };
+
+/* A whole network (Sec. 3, Eq. 1): encoder -> n_layers LUT layers -> head.
+ * Host struct; its pointers are device memory except `layers` (a host array
+ * of n_layers descriptors, as for bitlogic_forward). */
+typedef struct bitlogic_network {
+    int32_t n_features;             /* d                                          */
+    int32_t encoder;                /* BITLOGIC_ENCODER_*                         */
+    int32_t n_bits;                 /* b: thresholds per feature (thermometer,
+                                       1..64) or code bits (binary, 1..8)         */
+    const uint8_t *thresholds;      /* [d][b], thermometer only (else ignored)    */
+    const bitlogic_layer *layers;   /* host array; layer 0 reads the d * b wires  */
+    int32_t n_layers;
+    int32_t n_classes;              /* c; the last width is a multiple of c       */
+    int32_t head;                   /* BITLOGIC_HEAD_*                            */
+    const int8_t *head_weights;     /* [c][c] int8, GROUPED_DSP only (c <= 128)   */
+} bitlogic_network;
+
+/* Workspace bytes of bitlogic_network_forward for n_samples (0 if the
+ * descriptor is invalid). */
+size_t bitlogic_network_workspace_bytes(const bitlogic_network *net, int64_t n_samples);
+
+/* bitlogic_forward_plan for a network descriptor. */
+int bitlogic_network_plan(const bitlogic_network *net, int64_t n_samples,
+                          bitlogic_forward_info *info);
+
+/* The forward of a network descriptor: out [n_samples][c] int32 receives the
+ * GroupSum scores or, with the quantized head, its logits; argmax [n_samples]
+ * the lowest class holding the largest value (either may be NULL, not both).
+ * events: NULL, or n_layers + 3 HIP events recorded as in
+ * bitlogic_forward_timed.  Conventions and errors as bitlogic_forward, plus
+ * BITLOGIC_ERR_UNSUPPORTED for an unknown encoder or head kind, a binary code
+ * wider than 8 bits or a quantized head with more than 128 classes. */
+int bitlogic_network_forward(const bitlogic_network *net, const uint8_t *x, int64_t n_samples,
+                             int32_t *out, int32_t *argmax, void *workspace,
+                             size_t workspace_bytes, void *stream, void *const *events,
+                             int32_t n_events);
+
 /* Static description of a status code. */
 const char *bitlogic_status_string(int status);
 

@@ -23,6 +23,7 @@ __all__ = [
     "BitlogicError", "bitlogic_encode", "bitlogic_lut_layer", "bitlogic_groupsum_head",
     "bitlogic_forward", "bitlogic_forward_timed", "bitlogic_forward_workspace_bytes",
     "bitlogic_forward_plan", "bitlogic_grouped_dsp_head", "bitlogic_forward_grouped_dsp",
+    "bitlogic_encode_binary", "bitlogic_fit_quantile_thresholds", "bitlogic_network_forward",
     "bitlogic_groupsum_head_workspace_bytes", "bitlogic_status_string", "bitlogic_version",
     "BitlogicModel", "library_path", "load_library", "words",
 ]
@@ -51,6 +52,18 @@ class _Layer(ctypes.Structure):
                 ("w_out", ctypes.c_int32), ("k", ctypes.c_int32)]
 
 
+ENCODER_THERMOMETER, ENCODER_BINARY = 0, 1
+HEAD_GROUPSUM, HEAD_GROUPED_DSP = 0, 1
+
+
+class _Network(ctypes.Structure):
+    _fields_ = [("n_features", ctypes.c_int32), ("encoder", ctypes.c_int32),
+                ("n_bits", ctypes.c_int32), ("thresholds", ctypes.c_void_p),
+                ("layers", ctypes.c_void_p), ("n_layers", ctypes.c_int32),
+                ("n_classes", ctypes.c_int32), ("head", ctypes.c_int32),
+                ("head_weights", ctypes.c_void_p)]
+
+
 def library_path() -> str:
     return _LIB_PATH
 
@@ -74,6 +87,12 @@ def load_library():
         "bitlogic_forward_workspace_bytes": ([i64, i32, i32, P, i32, i32], sz),
         "bitlogic_forward_plan": ([i64, i32, i32, P, i32, i32, P], ctypes.c_int),
         "bitlogic_grouped_dsp_head": ([P, i64, i32, P, P, P, P], ctypes.c_int),
+        "bitlogic_encode_binary": ([P, i64, i32, i32, P, P], ctypes.c_int),
+        "bitlogic_fit_quantile_thresholds_workspace_bytes": ([i32], sz),
+        "bitlogic_fit_quantile_thresholds": ([P, i64, i32, i32, i32, P, P, sz, P], ctypes.c_int),
+        "bitlogic_network_workspace_bytes": ([P, i64], sz),
+        "bitlogic_network_plan": ([P, i64, P], ctypes.c_int),
+        "bitlogic_network_forward": ([P, P, i64, P, P, P, sz, P, P, i32], ctypes.c_int),
         "bitlogic_forward_grouped_dsp": ([P, i64, i32, P, i32, P, i32, i32, P, P, P, P, sz, P],
                                          ctypes.c_int),
         "bitlogic_forward": ([P, i64, i32, P, i32, P, i32, i32, P, P, P, sz, P], ctypes.c_int),
@@ -230,6 +249,38 @@ def bitlogic_forward_plan(n_samples: int, n_features: int, n_thresholds: int,
 _I8 = (torch.int8,)
 
 
+def bitlogic_encode_binary(x: torch.Tensor, n_bits: int,
+                           bits_out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Binary-coded encoder: pixels uint8 [N][d] -> packed int64 [d*n_bits][ceil(N/64)];
+    wire f*n_bits+t = bit t of round(x * (2^n_bits - 1) / 255)."""
+    n, d = x.shape
+    if bits_out is None:
+        bits_out = torch.empty((d * n_bits, words(n)), dtype=torch.int64, device=x.device)
+    _check(load_library().bitlogic_encode_binary(_dev(x, "x", _U8), n, d, int(n_bits),
+                                                 _dev(bits_out, "bits_out", _U64),
+                                                 _stream(stream, x.device)))
+    return bits_out
+
+
+def bitlogic_fit_quantile_thresholds(x: torch.Tensor, n_thresholds: int, n_groups: int = 1,
+                                     out: Optional[torch.Tensor] = None,
+                                     workspace: Optional[torch.Tensor] = None,
+                                     stream=None) -> torch.Tensor:
+    """Quantile thermometer thresholds fitted from pixels uint8 [N][d]: uint8
+    [d][n_thresholds], one ladder per contiguous group of d / n_groups features."""
+    n, d = x.shape
+    dev = x.device
+    if out is None:
+        out = torch.empty((d, n_thresholds), dtype=torch.uint8, device=dev)
+    lib = load_library()
+    need = int(lib.bitlogic_fit_quantile_thresholds_workspace_bytes(int(n_groups)))
+    ws_ptr, ws_bytes = _workspace(max(need, 8), dev, workspace)
+    _check(lib.bitlogic_fit_quantile_thresholds(_dev(x, "x", _U8), n, d, int(n_thresholds),
+                                                int(n_groups), _dev(out, "out", _U8), ws_ptr,
+                                                ws_bytes, _stream(stream, dev)))
+    return out
+
+
 def bitlogic_grouped_dsp_head(counts: torch.Tensor, weights: torch.Tensor,
                               logits: Optional[torch.Tensor] = None,
                               argmax: Optional[torch.Tensor] = None, stream=None,
@@ -334,19 +385,43 @@ def bitlogic_forward_timed(x: torch.Tensor, thresholds: torch.Tensor,
 
 @dataclass
 class BitlogicModel:
-    """A network resident in device memory: thresholds, per-layer conn/tables."""
-    thresholds: torch.Tensor
+    """A network resident in device memory: encoder (thermometer thresholds, or
+    the binary code width), per-layer conn/tables, and the class head."""
+    thresholds: Optional[torch.Tensor]
     layers: List[Tuple[torch.Tensor, torch.Tensor]]
     n_classes: int
+    n_features: int = 0
+    encoder: int = ENCODER_THERMOMETER
+    n_bits: int = 0
+    head: int = HEAD_GROUPSUM
+    head_weights: Optional[torch.Tensor] = None
+
+    def __post_init__(self):
+        if self.thresholds is not None and self.encoder == ENCODER_THERMOMETER:
+            self.n_features, self.n_bits = (int(v) for v in self.thresholds.shape)
 
     @classmethod
-    def from_numpy(cls, thresholds: np.ndarray, layers, n_classes: int,
-                   device="cuda") -> "BitlogicModel":
-        """Copy a host model to the GPU, checking every connection index."""
-        th = np.ascontiguousarray(thresholds, dtype=np.uint8)
-        if th.ndim != 2:
-            raise ValueError("thresholds must be [d][b]")
-        w_in = th.shape[0] * th.shape[1]
+    def from_numpy(cls, thresholds, layers, n_classes: int, device="cuda",
+                   encoder: str = "thermometer", n_features: Optional[int] = None,
+                   n_bits: Optional[int] = None, head_weights=None) -> "BitlogicModel":
+        """Copy a host model to the GPU, checking every connection index.
+        encoder "thermometer" takes thresholds uint8 [d][b]; "binary" takes
+        n_features and n_bits (thresholds None).  head_weights int8 [c][c]
+        selects the quantized head."""
+        if encoder == "thermometer":
+            th = np.ascontiguousarray(thresholds, dtype=np.uint8)
+            if th.ndim != 2:
+                raise ValueError("thresholds must be [d][b]")
+            d, b = th.shape
+            th_dev, kind = torch.from_numpy(th).to(device), ENCODER_THERMOMETER
+        elif encoder == "binary":
+            if n_features is None or n_bits is None:
+                raise ValueError("the binary encoder needs n_features and n_bits")
+            d, b = int(n_features), int(n_bits)
+            th_dev, kind = None, ENCODER_BINARY
+        else:
+            raise ValueError(f"unknown encoder {encoder!r}")
+        w_in = d * b
         dev_layers = []
         for l, (conn, tables) in enumerate(layers):
             conn = np.ascontiguousarray(conn, dtype=np.int32)
@@ -360,16 +435,75 @@ class BitlogicModel:
             w_in = conn.shape[0]
         if w_in % n_classes != 0:
             raise ValueError("last width must be a multiple of n_classes")
-        return cls(torch.from_numpy(th).to(device), dev_layers, int(n_classes))
+        hw, head = None, HEAD_GROUPSUM
+        if head_weights is not None:
+            q = np.ascontiguousarray(head_weights, dtype=np.int8)
+            if q.shape != (n_classes, n_classes):
+                raise ValueError("head_weights must be [c][c]")
+            hw, head = torch.from_numpy(q).to(device), HEAD_GROUPED_DSP
+        return cls(th_dev, dev_layers, int(n_classes), d, kind, b, head, hw)
+
+    def _net(self):
+        arr = _layer_array(self.layers)
+        net = _Network()
+        net.n_features, net.encoder, net.n_bits = self.n_features, self.encoder, self.n_bits
+        net.thresholds = (_dev(self.thresholds, "thresholds", _U8)
+                          if self.thresholds is not None else None)
+        net.layers = ctypes.cast(arr, ctypes.c_void_p)
+        net.n_layers = len(self.layers)
+        net.n_classes = self.n_classes
+        net.head = self.head
+        net.head_weights = (_dev(self.head_weights, "head_weights", _I8)
+                            if self.head_weights is not None else None)
+        return net, arr
 
     def workspace_bytes(self, n_samples: int) -> int:
-        return bitlogic_forward_workspace_bytes(n_samples, self.thresholds.shape[0],
-                                                self.thresholds.shape[1], self.layers,
-                                                self.n_classes)
+        net, keep = self._net()
+        return int(load_library().bitlogic_network_workspace_bytes(ctypes.byref(net),
+                                                                   n_samples))
 
     def plan(self, n_samples: int) -> dict:
-        return bitlogic_forward_plan(n_samples, self.thresholds.shape[0],
-                                     self.thresholds.shape[1], self.layers, self.n_classes)
+        net, keep = self._net()
+        info = _ForwardInfo()
+        _check(load_library().bitlogic_network_plan(ctypes.byref(net), n_samples,
+                                                    ctypes.byref(info)))
+        return {"workspace_bytes": int(info.workspace_bytes), "slab_words": int(info.slab_words),
+                "fused_head": bool(info.fused_head), "head_splits": int(info.head_splits),
+                "head_planes": int(info.head_planes)}
 
-    def forward(self, x: torch.Tensor, **kw):
-        return bitlogic_forward(x, self.thresholds, self.layers, self.n_classes, **kw)
+    def forward(self, x: torch.Tensor, out: Optional[torch.Tensor] = None,
+                argmax: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                stream=None, events=None, want_scores: bool = True):
+        """pixels uint8 [N][d] -> (scores or logits int32 [N][c], argmax int32 [N])."""
+        return bitlogic_network_forward(self, x, out, argmax, workspace, stream, events,
+                                        want_scores)
+
+
+def bitlogic_network_forward(model: BitlogicModel, x: torch.Tensor,
+                             out: Optional[torch.Tensor] = None,
+                             argmax: Optional[torch.Tensor] = None,
+                             workspace: Optional[torch.Tensor] = None, stream=None,
+                             events=None, want_scores: bool = True):
+    """Forward of a BitlogicModel through bitlogic_network_forward."""
+    n, d = x.shape
+    if d != model.n_features:
+        raise ValueError(f"x has {d} features, the model {model.n_features}")
+    dev = x.device
+    net, keep = model._net()
+    lib = load_library()
+    need = int(lib.bitlogic_network_workspace_bytes(ctypes.byref(net), n))
+    if out is None and want_scores:
+        out = torch.empty((n, model.n_classes), dtype=torch.int32, device=dev)
+    if argmax is None:
+        argmax = torch.empty((n,), dtype=torch.int32, device=dev)
+    ws_ptr, ws_bytes = _workspace(need, dev, workspace)
+    if events is None:
+        ev_ptr, n_ev = None, 0
+    else:
+        handles = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
+        ev_ptr, n_ev = ctypes.cast(handles, ctypes.c_void_p), len(events)
+    _check(lib.bitlogic_network_forward(
+        ctypes.byref(net), _dev(x, "x", _U8), n,
+        _dev(out, "out", _I32) if out is not None else None, _dev(argmax, "argmax", _I32),
+        ws_ptr, ws_bytes, _stream(stream, dev), ev_ptr, n_ev))
+    return out, argmax

@@ -267,21 +267,52 @@ int bitlogic_forward_plan(int64_t n_samples, int32_t n_features, int32_t n_thres
 
 namespace {
 
-int forward_impl(const uint8_t *x, int64_t n_samples, int32_t n_features,
-                 const uint8_t *thresholds, int32_t n_thresholds, const bitlogic_layer *layers,
-                 int32_t n_layers, int32_t n_classes, const int8_t *dsp_weights,
+// Checks of a network descriptor beyond the shapes that plan_forward checks.
+int check_network(const bitlogic_network *net)
+{
+    if (!net)
+        return fail(BITLOGIC_ERR_NULL, "network: NULL descriptor");
+    if (net->encoder == BITLOGIC_ENCODER_THERMOMETER) {
+        if (!net->thresholds)
+            return fail(BITLOGIC_ERR_NULL, "network: thermometer needs thresholds");
+    } else if (net->encoder == BITLOGIC_ENCODER_BINARY) {
+        if (net->n_bits < 1 || net->n_bits > 8)
+            return fail(BITLOGIC_ERR_UNSUPPORTED, "network: binary code of %d bits (1..8)",
+                        net->n_bits);
+    } else {
+        return fail(BITLOGIC_ERR_UNSUPPORTED, "network: unknown encoder %d", net->encoder);
+    }
+    if (net->head == BITLOGIC_HEAD_GROUPED_DSP) {
+        if (!net->head_weights)
+            return fail(BITLOGIC_ERR_NULL, "network: quantized head needs weights");
+        if (net->n_classes > kDspMaxClasses)
+            return fail(BITLOGIC_ERR_UNSUPPORTED, "network: quantized head needs n_classes <= %d",
+                        kDspMaxClasses);
+    } else if (net->head != BITLOGIC_HEAD_GROUPSUM) {
+        return fail(BITLOGIC_ERR_UNSUPPORTED, "network: unknown head %d", net->head);
+    }
+    return BITLOGIC_OK;
+}
+
+int plan_network(const bitlogic_network *net, int64_t n, ForwardPlan *fp)
+{
+    int st = check_network(net);
+    if (st != BITLOGIC_OK)
+        return st;
+    return plan_forward(n, net->n_features, net->n_bits, net->layers, net->n_layers,
+                        net->n_classes, fp);
+}
+
+int forward_impl(const bitlogic_network *net, const uint8_t *x, int64_t n_samples,
                  int32_t *scores, int32_t *argmax, void *workspace, size_t workspace_bytes,
                  void *stream, void *const *events, int32_t n_events)
 {
-    if (!x || !thresholds || (!scores && !argmax))
-        return fail(BITLOGIC_ERR_NULL, "forward: NULL pixels/thresholds or both outputs NULL");
-    if (dsp_weights && n_classes > kDspMaxClasses)
-        return fail(BITLOGIC_ERR_UNSUPPORTED, "forward: quantized head needs n_classes <= %d",
-                    kDspMaxClasses);
     ForwardPlan fp;
-    int st = plan_forward(n_samples, n_features, n_thresholds, layers, n_layers, n_classes, &fp);
+    int st = plan_network(net, n_samples, &fp);
     if (st != BITLOGIC_OK)
         return st;
+    if (!x || (!scores && !argmax))
+        return fail(BITLOGIC_ERR_NULL, "forward: NULL pixels or both outputs NULL");
     if (!workspace)
         return fail(BITLOGIC_ERR_NULL, "forward: NULL workspace");
     if (workspace_bytes < fp.total)
@@ -291,6 +322,7 @@ int forward_impl(const uint8_t *x, int64_t n_samples, int32_t n_features,
         return fail(BITLOGIC_ERR_ALIGN, "forward: workspace not 256-byte aligned");
     if ((scores && !aligned(scores, 4)) || (argmax && !aligned(argmax, 4)))
         return fail(BITLOGIC_ERR_ALIGN, "forward: misaligned output");
+    const int32_t n_layers = net->n_layers;
     if (events) {
         if (n_events != n_layers + 3)
             return fail(BITLOGIC_ERR_SHAPE, "forward_timed: need %d events, got %d",
@@ -302,6 +334,9 @@ int forward_impl(const uint8_t *x, int64_t n_samples, int32_t n_features,
     if (n_samples == 0)
         return ok();
 
+    const bitlogic_layer *layers = net->layers;
+    const int32_t n_classes = net->n_classes;
+    const int8_t *dsp = net->head == BITLOGIC_HEAD_GROUPED_DSP ? net->head_weights : nullptr;
     hipStream_t s = (hipStream_t)stream;
     auto mark = [&](int i) -> hipError_t {
         return events ? hipEventRecord((hipEvent_t)events[i], s) : hipSuccess;
@@ -312,14 +347,16 @@ int forward_impl(const uint8_t *x, int64_t n_samples, int32_t n_features,
                         reinterpret_cast<uint64_t *>(ws + fp.off_b)};
     hipError_t e = mark(0);
     if (e == hipSuccess)
-        e = bl::launch_encode(x, n_samples, n_features, thresholds, n_thresholds, enc,
-                              bl::kLayoutSlab, fp.n_slabs * bl::kSlabWords, s);
+        e = bl::launch_encode(x, n_samples, net->n_features, net->thresholds, net->n_bits, enc,
+                              bl::kLayoutSlab, fp.n_slabs * bl::kSlabWords, s,
+                              net->encoder == BITLOGIC_ENCODER_BINARY ? bl::kEncBinary
+                                                                      : bl::kEncThermometer);
     if (e == hipSuccess)
         e = mark(1);
     if (e != hipSuccess)
         return hip_status(e, "forward: encode launch");
     const uint64_t *cur = enc;
-    int32_t w_in = n_features * n_thresholds;
+    int32_t w_in = net->n_features * net->n_bits;
     uint64_t *planes = reinterpret_cast<uint64_t *>(ws + fp.off_head);
     for (int32_t l = 0; l < n_layers; ++l) {
         const bool last_fused = fp.fused && l == n_layers - 1;
@@ -339,14 +376,31 @@ int forward_impl(const uint8_t *x, int64_t n_samples, int32_t n_features,
         w_in = layers[l].w_out;
     }
     if (fp.fused)
-        e = bl::launch_head_finish(planes, n_samples, n_classes, scores, argmax, dsp_weights,
-                                   fp.head, s);
+        e = bl::launch_head_finish(planes, n_samples, n_classes, scores, argmax, dsp, fp.head, s);
     else
-        e = bl::launch_head(cur, w_in, n_samples, n_classes, scores, argmax, dsp_weights, planes,
+        e = bl::launch_head(cur, w_in, n_samples, n_classes, scores, argmax, dsp, planes,
                             fp.head, bl::kLayoutSlab, s);
     if (e == hipSuccess)
         e = mark(n_layers + 2);
     return hip_status(e, "forward: head launch");
+}
+
+// The descriptor of the legacy entry points' arguments.
+bitlogic_network legacy_net(int32_t n_features, const uint8_t *thresholds, int32_t n_thresholds,
+                            const bitlogic_layer *layers, int32_t n_layers, int32_t n_classes,
+                            const int8_t *dsp_weights)
+{
+    bitlogic_network net;
+    net.n_features = n_features;
+    net.encoder = BITLOGIC_ENCODER_THERMOMETER;
+    net.n_bits = n_thresholds;
+    net.thresholds = thresholds;
+    net.layers = layers;
+    net.n_layers = n_layers;
+    net.n_classes = n_classes;
+    net.head = dsp_weights ? BITLOGIC_HEAD_GROUPED_DSP : BITLOGIC_HEAD_GROUPSUM;
+    net.head_weights = dsp_weights;
+    return net;
 }
 
 }  // namespace
@@ -359,8 +413,11 @@ int bitlogic_forward(const uint8_t *x, int64_t n_samples, int32_t n_features,
                      int32_t *scores, int32_t *argmax, void *workspace, size_t workspace_bytes,
                      void *stream)
 {
-    return forward_impl(x, n_samples, n_features, thresholds, n_thresholds, layers, n_layers,
-                        n_classes, nullptr, scores, argmax, workspace, workspace_bytes, stream,
+    if (!thresholds)
+        return fail(BITLOGIC_ERR_NULL, "forward: NULL thresholds");
+    const bitlogic_network net =
+        legacy_net(n_features, thresholds, n_thresholds, layers, n_layers, n_classes, nullptr);
+    return forward_impl(&net, x, n_samples, scores, argmax, workspace, workspace_bytes, stream,
                         nullptr, 0);
 }
 
@@ -373,8 +430,11 @@ int bitlogic_forward_grouped_dsp(const uint8_t *x, int64_t n_samples, int32_t n_
 {
     if (!weights)
         return fail(BITLOGIC_ERR_NULL, "forward_grouped_dsp: NULL weights");
-    return forward_impl(x, n_samples, n_features, thresholds, n_thresholds, layers, n_layers,
-                        n_classes, weights, logits, argmax, workspace, workspace_bytes, stream,
+    if (!thresholds)
+        return fail(BITLOGIC_ERR_NULL, "forward: NULL thresholds");
+    const bitlogic_network net =
+        legacy_net(n_features, thresholds, n_thresholds, layers, n_layers, n_classes, weights);
+    return forward_impl(&net, x, n_samples, logits, argmax, workspace, workspace_bytes, stream,
                         nullptr, 0);
 }
 
@@ -407,9 +467,97 @@ int bitlogic_forward_timed(const uint8_t *x, int64_t n_samples, int32_t n_featur
 {
     if (!events)
         return fail(BITLOGIC_ERR_NULL, "forward_timed: NULL event array");
-    return forward_impl(x, n_samples, n_features, thresholds, n_thresholds, layers, n_layers,
-                        n_classes, nullptr, scores, argmax, workspace, workspace_bytes, stream,
+    if (!thresholds)
+        return fail(BITLOGIC_ERR_NULL, "forward: NULL thresholds");
+    const bitlogic_network net =
+        legacy_net(n_features, thresholds, n_thresholds, layers, n_layers, n_classes, nullptr);
+    return forward_impl(&net, x, n_samples, scores, argmax, workspace, workspace_bytes, stream,
                         events, n_events);
+}
+
+size_t bitlogic_network_workspace_bytes(const bitlogic_network *net, int64_t n_samples)
+{
+    ForwardPlan fp;
+    if (plan_network(net, n_samples, &fp) != BITLOGIC_OK)
+        return 0;
+    return fp.total;
+}
+
+int bitlogic_network_plan(const bitlogic_network *net, int64_t n_samples,
+                          bitlogic_forward_info *info)
+{
+    if (!info)
+        return fail(BITLOGIC_ERR_NULL, "network_plan: NULL info");
+    ForwardPlan fp;
+    int st = plan_network(net, n_samples, &fp);
+    if (st != BITLOGIC_OK)
+        return st;
+    info->workspace_bytes = fp.total;
+    info->slab_words = bl::kSlabWords;
+    info->fused_head = fp.fused ? 1 : 0;
+    info->head_splits = fp.head.splits;
+    info->head_planes = fp.head.planes;
+    return ok();
+}
+
+int bitlogic_network_forward(const bitlogic_network *net, const uint8_t *x, int64_t n_samples,
+                             int32_t *out, int32_t *argmax, void *workspace,
+                             size_t workspace_bytes, void *stream, void *const *events,
+                             int32_t n_events)
+{
+    return forward_impl(net, x, n_samples, out, argmax, workspace, workspace_bytes, stream,
+                        events, events ? n_events : 0);
+}
+
+int bitlogic_encode_binary(const uint8_t *x, int64_t n_samples, int32_t n_features,
+                           int32_t n_bits, uint64_t *bits_out, void *stream)
+{
+    if (!x || !bits_out)
+        return fail(BITLOGIC_ERR_NULL, "encode_binary: NULL pointer");
+    if (n_samples < 0 || n_features <= 0 || n_bits < 1 || n_bits > 8)
+        return fail(BITLOGIC_ERR_SHAPE, "encode_binary: need n >= 0, d > 0, 1 <= n_bits <= 8");
+    if ((int64_t)n_features * n_bits > kMaxRows)
+        return fail(BITLOGIC_ERR_SHAPE, "encode_binary: d * n_bits exceeds int32");
+    if (!aligned(bits_out, 8))
+        return fail(BITLOGIC_ERR_ALIGN, "encode_binary: bits_out not 8-byte aligned");
+    if (n_samples == 0)
+        return ok();
+    return hip_status(bl::launch_encode(x, n_samples, n_features, nullptr, n_bits, bits_out,
+                                        bl::kLayoutRowMajor, words_of(n_samples),
+                                        (hipStream_t)stream, bl::kEncBinary),
+                      "encode_binary launch");
+}
+
+size_t bitlogic_fit_quantile_thresholds_workspace_bytes(int32_t n_groups)
+{
+    if (n_groups < 1 || n_groups > bl::kFitMaxGroups)
+        return 0;
+    return (size_t)n_groups * 256 * sizeof(uint64_t);
+}
+
+int bitlogic_fit_quantile_thresholds(const uint8_t *x, int64_t n_samples, int32_t n_features,
+                                     int32_t n_thresholds, int32_t n_groups,
+                                     uint8_t *thresholds_out, void *workspace,
+                                     size_t workspace_bytes, void *stream)
+{
+    if (!x || !thresholds_out || !workspace)
+        return fail(BITLOGIC_ERR_NULL, "fit_quantiles: NULL pointer");
+    if (n_samples < 1 || n_features < 1 || n_thresholds < 1 || n_thresholds > 64)
+        return fail(BITLOGIC_ERR_SHAPE, "fit_quantiles: need n >= 1, d >= 1, 1 <= b <= 64");
+    if (n_groups < 1 || n_groups > bl::kFitMaxGroups || n_features % n_groups != 0)
+        return fail(BITLOGIC_ERR_SHAPE, "fit_quantiles: %d groups of %d features", n_groups,
+                    n_features);
+    if (n_samples > ((int64_t)1 << 56) / n_features)
+        return fail(BITLOGIC_ERR_SHAPE, "fit_quantiles: n * d exceeds 2^56");
+    if (workspace_bytes < bitlogic_fit_quantile_thresholds_workspace_bytes(n_groups))
+        return fail(BITLOGIC_ERR_WORKSPACE, "fit_quantiles: workspace too small");
+    if (!aligned(workspace, 8))
+        return fail(BITLOGIC_ERR_ALIGN, "fit_quantiles: workspace not 8-byte aligned");
+    return hip_status(bl::launch_fit_quantiles(x, n_samples, n_features, n_thresholds, n_groups,
+                                               thresholds_out,
+                                               static_cast<uint64_t *>(workspace),
+                                               (hipStream_t)stream),
+                      "fit_quantiles launch");
 }
 
 const char *bitlogic_status_string(int status)
@@ -428,6 +576,6 @@ const char *bitlogic_status_string(int status)
 
 const char *bitlogic_last_error(void) { return g_last_error; }
 
-int bitlogic_version(void) { return 100; }
+int bitlogic_version(void) { return 200; }
 
 }  // extern "C"

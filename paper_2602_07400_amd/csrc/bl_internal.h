@@ -46,9 +46,20 @@ __device__ __forceinline__ int local_of(int bid) { return bid / kXcds; }
 // Encoder into either layout; W_cols = columns (words) to write: W for the
 // row-major layout, W rounded up to whole slabs for the slab layout (columns
 // past the batch get zero bits).
+// kind: kEncThermometer (thresholds [d][b]) or kEncBinary (b <= 8, thresholds
+// unused).
+constexpr int kEncThermometer = 0;
+constexpr int kEncBinary = 1;
 hipError_t launch_encode(const uint8_t *x, int64_t n, int32_t d,
                          const uint8_t *thresholds, int32_t b, uint64_t *out, int layout,
-                         int64_t W_cols, hipStream_t stream);
+                         int64_t W_cols, hipStream_t stream, int kind = kEncThermometer);
+
+// Quantile thresholds from data: histograms of n_groups contiguous feature
+// groups (ws: n_groups * 256 uint64, cleared here), then per group the
+// smallest v with (b + 1) * cum(v) >= i * total for i = 1..b into th [d][b].
+constexpr int kFitMaxGroups = 32;
+hipError_t launch_fit_quantiles(const uint8_t *x, int64_t n, int32_t d, int32_t b,
+                                int32_t n_groups, uint8_t *th, uint64_t *ws, hipStream_t stream);
 
 // Slab-layout LUT layer over n_slabs slabs (bitlogic_forward's intermediates).
 hipError_t launch_lut_layer_slab(const uint64_t *in, int32_t w_in, int64_t n_slabs,

@@ -29,6 +29,10 @@
 //
 // Both write either the row-major layout [wires][W] of bitlogic_encode or the
 // slab layout [Wp/S][wires][S] of bitlogic_forward's intermediates.
+//
+// The binary-coded uniform fixed-point encoder (Sec. 3 "Encoders and heads":
+// 2^b levels on b wires; Sec. 5 "Encoder") is the same kernel with another
+// code table: code[f][v] = round(v (2^b - 1) / 255), wire t = bit t.
 #include "bl_internal.h"
 
 namespace bl {
@@ -142,7 +146,7 @@ template <int B, int LAYOUT>
 __global__ __launch_bounds__(kThreads) void k_encode_t(
     const uint8_t *__restrict__ x, int64_t n, int32_t d, const uint8_t *__restrict__ th,
     uint64_t *__restrict__ out, int64_t W, int64_t W_cols, int32_t n_ftiles,
-    int32_t tiles_per_block, int64_t n_tiles, int64_t n_tgroups, int aligned4)
+    int32_t tiles_per_block, int64_t n_tiles, int64_t n_tgroups, int aligned4, int kind)
 {
     using G = EncGeom<B>;
     constexpr int kWires = G::kG * G::kWPG;              // wire rows of one output tile
@@ -165,20 +169,27 @@ __global__ __launch_bounds__(kThreads) void k_encode_t(
     // ---- code table for this feature tile: dword e holds the codes of values
     // 4*(e%64) .. +3 of tile feature e/64 (one feature per wave); bit t of a
     // code is set from byte position p on, p = clamp(theta_t - v0 + 1, 0, 4)
-    for (int q = threadIdx.x; q < nf * B; q += kThreads)
-        ths[q] = th[(int64_t)f0 * B + q];
+    if (kind == kEncThermometer)
+        for (int q = threadIdx.x; q < nf * B; q += kThreads)
+            ths[q] = th[(int64_t)f0 * B + q];
     __syncthreads();
     for (int e = threadIdx.x; e < G::kFT * 64; e += kThreads) {
         const int f = e >> 6;
         const int v0 = 4 * (e & 63);
         uint32_t codes = 0;
-        if (f < nf) {
+        if (f < nf && kind == kEncThermometer) {
 #pragma unroll
             for (int t = 0; t < B; ++t) {
                 const int p = min(max((int)ths[f * B + t] - v0 + 1, 0), 4);
                 const uint32_t m = (p >= 4) ? 0u : (0xFFFFFFFFu << (8 * p));
                 codes |= m & (0x01010101u << t);
             }
+        } else if (f < nf) {
+            // binary code: q = round(v (2^B - 1) / 255), no ties since 255 is odd
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                codes |= (uint32_t)((2u * (uint32_t)(v0 + u) * ((1u << B) - 1u) + 255u) / 510u)
+                         << (8 * u);
         }
         reinterpret_cast<uint32_t *>(lut)[e] = codes;
     }
@@ -369,7 +380,7 @@ __global__ __launch_bounds__(kThreads) void k_encode_ballot(
 
 template <int B, int LAYOUT>
 hipError_t launch_t(const uint8_t *x, int64_t n, int32_t d, const uint8_t *th, uint64_t *out,
-                    int64_t W_cols, hipStream_t stream)
+                    int64_t W_cols, int kind, hipStream_t stream)
 {
     using G = EncGeom<B>;
     const int64_t W = (n + 63) / 64;
@@ -388,7 +399,7 @@ hipError_t launch_t(const uint8_t *x, int64_t n, int32_t d, const uint8_t *th, u
     const int aligned4 = (d % 4 == 0) && ((uintptr_t)x % 4 == 0);
     hipLaunchKernelGGL((k_encode_t<B, LAYOUT>), dim3((unsigned)blocks), dim3(kThreads), 0, stream,
                        x, n, d, th, out, W, W_cols, n_ftiles, (int32_t)tpb, n_tiles, n_tg,
-                       aligned4);
+                       aligned4, kind);
     return hipGetLastError();
 }
 
@@ -416,18 +427,21 @@ hipError_t launch_ballot(const uint8_t *x, int64_t n, int32_t d, const uint8_t *
 
 template <int LAYOUT>
 hipError_t launch_layout(const uint8_t *x, int64_t n, int32_t d, const uint8_t *th, int32_t b,
-                         uint64_t *out, int64_t W_cols, hipStream_t stream)
+                         uint64_t *out, int64_t W_cols, int kind, hipStream_t stream)
 {
     switch (b) {
-    case 1: return launch_t<1, LAYOUT>(x, n, d, th, out, W_cols, stream);
-    case 2: return launch_t<2, LAYOUT>(x, n, d, th, out, W_cols, stream);
-    case 3: return launch_t<3, LAYOUT>(x, n, d, th, out, W_cols, stream);
-    case 4: return launch_t<4, LAYOUT>(x, n, d, th, out, W_cols, stream);
-    case 5: return launch_t<5, LAYOUT>(x, n, d, th, out, W_cols, stream);
-    case 6: return launch_t<6, LAYOUT>(x, n, d, th, out, W_cols, stream);
-    case 7: return launch_t<7, LAYOUT>(x, n, d, th, out, W_cols, stream);
-    case 8: return launch_t<8, LAYOUT>(x, n, d, th, out, W_cols, stream);
-    default: return launch_ballot<LAYOUT>(x, n, d, th, b, out, W_cols, stream);
+    case 1: return launch_t<1, LAYOUT>(x, n, d, th, out, W_cols, kind, stream);
+    case 2: return launch_t<2, LAYOUT>(x, n, d, th, out, W_cols, kind, stream);
+    case 3: return launch_t<3, LAYOUT>(x, n, d, th, out, W_cols, kind, stream);
+    case 4: return launch_t<4, LAYOUT>(x, n, d, th, out, W_cols, kind, stream);
+    case 5: return launch_t<5, LAYOUT>(x, n, d, th, out, W_cols, kind, stream);
+    case 6: return launch_t<6, LAYOUT>(x, n, d, th, out, W_cols, kind, stream);
+    case 7: return launch_t<7, LAYOUT>(x, n, d, th, out, W_cols, kind, stream);
+    case 8: return launch_t<8, LAYOUT>(x, n, d, th, out, W_cols, kind, stream);
+    default:
+        if (kind != kEncThermometer)
+            return hipErrorInvalidValue;          // binary codes have at most 8 bits
+        return launch_ballot<LAYOUT>(x, n, d, th, b, out, W_cols, stream);
     }
 }
 
@@ -435,11 +449,11 @@ hipError_t launch_layout(const uint8_t *x, int64_t n, int32_t d, const uint8_t *
 
 hipError_t launch_encode(const uint8_t *x, int64_t n, int32_t d, const uint8_t *thresholds,
                          int32_t b, uint64_t *out, int layout, int64_t W_cols,
-                         hipStream_t stream)
+                         hipStream_t stream, int kind)
 {
     if (layout == kLayoutSlab)
-        return launch_layout<kLayoutSlab>(x, n, d, thresholds, b, out, W_cols, stream);
-    return launch_layout<kLayoutRowMajor>(x, n, d, thresholds, b, out, W_cols, stream);
+        return launch_layout<kLayoutSlab>(x, n, d, thresholds, b, out, W_cols, kind, stream);
+    return launch_layout<kLayoutRowMajor>(x, n, d, thresholds, b, out, W_cols, kind, stream);
 }
 
 }  // namespace bl

@@ -26,6 +26,11 @@ def _declared():
 
 @pytest.fixture(scope="module")
 def lib():
+    # the fake pointers below must never reach a device: if a check were
+    # missing, a launch would dereference them
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("fake-pointer argument checks run only where no GPU is visible")
     return bl.load_library()
 
 
@@ -216,3 +221,68 @@ def test_forward_grouped_dsp_validation(lib):
     assert f(FAKE, 4096, 784, FAKE, 1, p2, 2, 129, FAKE, FAKE, FAKE, FAKE * 16, 1 << 40,
              None) == EUNSUP
     assert f(*args(n=0)) == OK
+
+
+def test_encode_binary_validation(lib):
+    f = lib.bitlogic_encode_binary
+    assert f(None, 64, 4, 2, FAKE, None) == ENULL
+    assert f(FAKE, 64, 4, 0, FAKE, None) == ESHAPE
+    assert f(FAKE, 64, 4, 9, FAKE, None) == ESHAPE
+    assert f(FAKE, -1, 4, 2, FAKE, None) == ESHAPE
+    assert f(FAKE, 64, 4, 2, FAKE + 4, None) == EALIGN
+    assert f(FAKE, 0, 4, 2, FAKE, None) == OK
+
+
+def test_fit_quantiles_validation(lib):
+    ws = lib.bitlogic_fit_quantile_thresholds_workspace_bytes
+    assert ws(1) == 256 * 8 and ws(3) == 3 * 256 * 8
+    assert ws(0) == 0 and ws(33) == 0
+    f = lib.bitlogic_fit_quantile_thresholds
+    good = [FAKE, 100, 12, 3, 3, FAKE, FAKE * 16, ws(3), None]
+    bad = lambda i, v: f(*(good[:i] + [v] + good[i + 1:]))
+    assert bad(0, None) == ENULL and bad(5, None) == ENULL and bad(6, None) == ENULL
+    assert bad(1, 0) == ESHAPE                   # no samples to fit on
+    assert bad(3, 0) == ESHAPE and bad(3, 65) == ESHAPE
+    assert bad(4, 5) == ESHAPE                   # 12 features do not split into 5 groups
+    assert bad(4, 33) == ESHAPE
+    assert bad(7, ws(3) - 1) == EWS
+    assert bad(6, FAKE * 16 + 4) == EALIGN
+    assert bad(1, 1 << 55) == ESHAPE             # n * d beyond 2^56
+
+
+def _net(p, **o):
+    net = bl._Network()
+    net.n_features, net.encoder, net.n_bits = o.get("d", 784), o.get("enc", 0), o.get("b", 1)
+    net.thresholds = o.get("th", FAKE)
+    net.layers, net.n_layers, net.n_classes = p, o.get("L", 2), o.get("c", 10)
+    net.head, net.head_weights = o.get("head", 0), o.get("w", None)
+    return net
+
+
+def test_network_validation(lib):
+    p, keep = _layers([(1000, 6), (1000, 6)])
+    ws = lambda net: lib.bitlogic_network_workspace_bytes(ctypes.byref(net), 4096)
+    # same plan as the legacy call
+    assert ws(_net(p)) == lib.bitlogic_forward_workspace_bytes(4096, 784, 1, p, 2, 10)
+    pb, keepb = _layers([(1000, 6), (1000, 6)])
+    assert ws(_net(pb, enc=1, b=4, th=None)) == lib.bitlogic_forward_workspace_bytes(
+        4096, 784, 4, pb, 2, 10)
+    fwd = lambda net, **o: lib.bitlogic_network_forward(
+        ctypes.byref(net), o.get("x", FAKE), o.get("n", 4096), FAKE, FAKE, FAKE * 16,
+        o.get("wsb", 1 << 40), None, None, 0)
+    assert lib.bitlogic_network_forward(None, FAKE, 64, FAKE, FAKE, FAKE * 16, 1 << 40, None,
+                                        None, 0) == ENULL
+    assert fwd(_net(p, th=None)) == ENULL                    # thermometer without thresholds
+    assert fwd(_net(p, enc=2)) == EUNSUP                     # unknown encoder
+    assert fwd(_net(p, enc=1, b=9, th=None)) == EUNSUP       # binary code wider than 8 bits
+    assert fwd(_net(p, head=2)) == EUNSUP                    # unknown head
+    assert fwd(_net(p, head=1)) == ENULL                     # quantized head without weights
+    p2, keep2 = _layers([(1000, 6), (129000, 6)])
+    assert fwd(_net(p2, head=1, w=FAKE, c=129)) == EUNSUP
+    assert fwd(_net(p), x=None) == ENULL
+    assert fwd(_net(p), wsb=0) == EWS
+    assert fwd(_net(p), n=0) == OK
+    assert fwd(_net(p, enc=1, b=8, th=None), n=0) == OK
+    info = bl._ForwardInfo()
+    assert lib.bitlogic_network_plan(ctypes.byref(_net(p)), 4096, ctypes.byref(info)) == OK
+    assert info.workspace_bytes == ws(_net(p))

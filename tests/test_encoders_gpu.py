@@ -1,0 +1,124 @@
+"""The encoder family on the GPU against the oracle, bit-exact.
+
+Binary-coded uniform fixed-point encoder (Sec. 3 "Encoders and heads";
+Sec. 5 "Encoder"): every code width 1..8, ragged sample counts, rows that
+are not whole dwords and misaligned pixel pointers.  Quantile-threshold
+fitting (Sec. 4 "Initialization"; App. B): one and several feature groups,
+threshold counts up to 64, skewed and mixture pixel distributions, the App. B
+collapse case, rows that are not whole dwords, a single sample.  Whole
+networks: the binary encoder with both heads, and the thermometer with
+thresholds fitted on the device.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2602_07400_amd import bitlogic as bl
+from paper_2602_07400_amd.workloads import make_workload
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0")
+
+
+def unpack(bits: torch.Tensor, n: int) -> np.ndarray:
+    b = bits.cpu().numpy().view(np.uint8)
+    v = np.unpackbits(b, axis=1, bitorder="little")
+    return np.ascontiguousarray(v[:, :n].T)
+
+
+@pytest.mark.parametrize("n,d,b", [(64, 4, 1), (64 * 3 + 5, 37, 3), (4096 + 17, 784, 8),
+                                   (1000, 100, 2), (2048, 3072, 7), (300, 13, 5), (129, 8, 4),
+                                   (777, 60, 6)])
+def test_encode_binary_parity(n, d, b):
+    rng = np.random.default_rng(n + 7 * d + b)
+    x = rng.integers(0, 256, size=(n, d), dtype=np.uint8)
+    x[:3] = 0
+    x[3:6] = 255
+    bits = bl.bitlogic_encode_binary(torch.from_numpy(x).to(DEV), b)
+    assert np.array_equal(unpack(bits, n), oracle.encode_binary(x, b))
+
+
+def test_encode_binary_unaligned_rows():
+    rng = np.random.default_rng(3)
+    buf = torch.from_numpy(rng.integers(0, 256, size=(1 + 500 * 12,), dtype=np.uint8)).to(DEV)
+    x = buf[1:].view(500, 12)                    # pixel rows start at an odd address
+    bits = bl.bitlogic_encode_binary(x, 3)
+    assert np.array_equal(unpack(bits, 500), oracle.encode_binary(x.cpu().numpy(), 3))
+
+
+def _fit_check(x, b, groups):
+    th = bl.bitlogic_fit_quantile_thresholds(torch.from_numpy(x).to(DEV), b, groups)
+    torch.cuda.synchronize()
+    assert np.array_equal(th.cpu().numpy(), oracle.fit_quantiles(x, b, groups))
+
+
+@pytest.mark.parametrize("n,d,groups,b", [(5000, 3072, 3, 3), (5000, 3072, 1, 4), (1, 12, 3, 7),
+                                          (3000, 784, 1, 8), (2000, 30, 3, 64), (4097, 64, 32, 5),
+                                          (700, 15, 5, 1)])
+def test_fit_quantiles_parity(n, d, groups, b):
+    rng = np.random.default_rng(n + d + groups + b)
+    # skewed values: many ties and empty bins
+    x = np.minimum(rng.exponential(40.0, size=(n, d)), 255).astype(np.uint8)
+    _fit_check(x, b, groups)
+
+
+def test_fit_quantiles_collapse_and_mixture():
+    x = np.zeros((2000, 100), np.uint8)
+    flat = x.reshape(-1)
+    flat[: int(0.115 * flat.size)] = 180
+    np.random.default_rng(0).shuffle(flat)
+    for b in (4, 8):
+        _fit_check(x, b, 1)
+    wl = make_workload("c2_fmnist", n=20000)     # the Gaussian-mixture pixels
+    _fit_check(wl.x, 7, 1)
+
+
+def _net_check(wl, model, binary_bits=0, dsp=None):
+    x = torch.from_numpy(wl.x).to(DEV)
+    out, am = model.forward(x)
+    torch.cuda.synchronize()
+    th = None if binary_bits else model.thresholds.cpu().numpy()
+    rs, rp = oracle.forward(wl.x, th, wl.layers, wl.n_classes, binary_bits=binary_bits)
+    if dsp is not None:
+        rs, rp = oracle.grouped_dsp(rs, dsp)
+    assert np.array_equal(out.cpu().numpy().astype(np.int64), rs.astype(np.int64))
+    assert np.array_equal(am.cpu().numpy(), rp)
+
+
+@pytest.mark.parametrize("b,head", [(2, False), (8, False), (3, True)])
+def test_forward_binary_encoder(b, head):
+    # a C4-shaped network (3072 features, 100 classes x 640) fed binary codes
+    from paper_2602_07400_amd.workloads import CONFIGS, Config, draw_connectivity, draw_tables
+    cfg = CONFIGS["c4_cifar100_wide"]
+    n = 64 * 16 * 2 + 64 * 3 + 17
+    wl = make_workload(cfg, n=n)
+    rng = np.random.default_rng(b)
+    w1 = 4000
+    conn1 = draw_connectivity(rng, w1, 6, 3072 * b)
+    conn2 = draw_connectivity(rng, 6400, 6, w1)
+    wl.layers = [(conn1, draw_tables(rng, w1, 6)), (conn2, draw_tables(rng, 6400, 6))]
+    dsp = wl.dsp_weights if head else None
+    model = bl.BitlogicModel.from_numpy(None, wl.layers, wl.n_classes, device=DEV,
+                                        encoder="binary", n_features=3072, n_bits=b,
+                                        head_weights=dsp)
+    assert model.plan(n)["fused_head"]
+    _net_check(wl, model, binary_bits=b, dsp=dsp)
+
+
+def test_forward_with_device_fitted_thresholds():
+    # C3's recipe end to end on the device: fit per-channel quantile thresholds
+    # on a training split, then run the forward with them
+    wl = make_workload("c3_cifar10", n=3000)
+    train = make_workload("c3_cifar10", seed=1, n=4000).x
+    th_dev = bl.bitlogic_fit_quantile_thresholds(torch.from_numpy(train).to(DEV), 3, 3)
+    th_ref = oracle.fit_quantiles(train, 3, 3)
+    assert np.array_equal(th_dev.cpu().numpy(), th_ref)
+    model = bl.BitlogicModel(th_dev, [(torch.from_numpy(c).to(DEV),
+                                       torch.from_numpy(t.view(np.int64)).to(DEV))
+                                      for c, t in wl.layers], wl.n_classes)
+    x = torch.from_numpy(wl.x).to(DEV)
+    s, p = model.forward(x)
+    rs, rp = oracle.forward(wl.x, th_ref, wl.layers, wl.n_classes)
+    assert np.array_equal(s.cpu().numpy(), rs) and np.array_equal(p.cpu().numpy(), rp)
