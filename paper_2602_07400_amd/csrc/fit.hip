@@ -13,8 +13,8 @@
 // k_fit_hist: each block counts a run of rows into an LDS histogram per
 // group (LDS atomics), then adds it into the global 64-bit histogram.  Rows
 // are read as coalesced dwords: a thread keeps its columns (and their
-// groups) and walks the rows.  k_fit_select: one block per group turns the
-// histogram into the ladder.
+// groups) and walks the rows, eight rows' loads at a time.  k_fit_select:
+// one block per group turns the histogram into the ladder.
 #include "bl_internal.h"
 
 namespace bl {
@@ -22,6 +22,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kHistBlocks = 1024;
+constexpr int kRowUnroll = 8;
 
 __global__ __launch_bounds__(kThreads) void k_fit_clear(uint64_t *__restrict__ ws, int32_t n)
 {
@@ -48,7 +49,20 @@ __global__ __launch_bounds__(kThreads) void k_fit_hist(
 #pragma unroll
             for (int u = 0; u < 4; ++u)
                 g[u] = (4 * fq + u) / per * 256;
-            for (int64_t r = r0; r < r1; ++r) {
+            // eight rows' loads in flight before their counts
+            int64_t r = r0;
+            for (; r + kRowUnroll <= r1; r += kRowUnroll) {
+                uint32_t v[kRowUnroll];
+#pragma unroll
+                for (int q = 0; q < kRowUnroll; ++q)
+                    v[q] = x32[(r + q) * d4 + fq];
+#pragma unroll
+                for (int q = 0; q < kRowUnroll; ++q)
+#pragma unroll
+                    for (int u = 0; u < 4; ++u)
+                        atomicAdd(&hist[g[u] + ((v[q] >> (8 * u)) & 0xFFu)], 1u);
+            }
+            for (; r < r1; ++r) {
                 const uint32_t v = x32[r * d4 + fq];
 #pragma unroll
                 for (int u = 0; u < 4; ++u)
@@ -58,7 +72,17 @@ __global__ __launch_bounds__(kThreads) void k_fit_hist(
     } else {
         for (int32_t f = threadIdx.x; f < d; f += kThreads) {
             const int g = f / per * 256;
-            for (int64_t r = r0; r < r1; ++r)
+            int64_t r = r0;
+            for (; r + kRowUnroll <= r1; r += kRowUnroll) {
+                uint32_t v[kRowUnroll];
+#pragma unroll
+                for (int q = 0; q < kRowUnroll; ++q)
+                    v[q] = x[(r + q) * d + f];
+#pragma unroll
+                for (int q = 0; q < kRowUnroll; ++q)
+                    atomicAdd(&hist[g + v[q]], 1u);
+            }
+            for (; r < r1; ++r)
                 atomicAdd(&hist[g + x[r * d + f]], 1u);
         }
     }
