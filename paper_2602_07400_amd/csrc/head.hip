@@ -38,7 +38,11 @@ constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
 constexpr int kMaxPlanes = 16;
 constexpr int kDspMaxClasses = 128;   // logits stay below 2^31; tiles fit in LDS
+#ifndef BL_DSP_FINISH_BLOCKS
+#define BL_DSP_FINISH_BLOCKS 2048
+#endif
 constexpr int64_t kDspBlocks = 1024;  // blocks of the quantized head (4 per CU)
+constexpr int64_t kDspFinishBlocks = BL_DSP_FINISH_BLOCKS;   // measured best on C4: 2048
 
 __device__ __forceinline__ void csa(uint64_t &h, uint64_t &l, uint64_t a, uint64_t b,
                                     uint64_t c)
@@ -593,7 +597,7 @@ hipError_t launch_finish_p(const uint64_t *planes, int64_t n, int32_t c, int32_t
         if (c > kDspMaxClasses)
             return hipErrorInvalidValue;
         // Q is staged once per block and reused for a run of columns
-        const int64_t blocks = W < kDspBlocks ? W : kDspBlocks;
+        const int64_t blocks = W < kDspFinishBlocks ? W : kDspFinishBlocks;
         hipLaunchKernelGGL(k_head_finish_dsp<P>, dim3((unsigned)blocks), dim3(kThreads),
                            dsp_layout(c).bytes, stream, planes, n, c, plan.splits, dsp_weights,
                            scores, argmax);
