@@ -151,6 +151,10 @@ typedef struct bitlogic_forward_info {
                                  written to memory                                */
     int32_t head_splits;      /* partial counters per (sample word, class)       */
     int32_t head_planes;      /* bit planes per partial counter                  */
+    int32_t fused_network;    /* 1: the whole network runs as one kernel, one
+                                 block per 64 samples with every activation in
+                                 LDS (small networks and batches; the workspace
+                                 is then not used)                              */
 } bitlogic_forward_info;
 
 int bitlogic_forward_plan(int64_t n_samples, int32_t n_features, int32_t n_thresholds,

@@ -33,10 +33,13 @@
 // The binary-coded uniform fixed-point encoder (Sec. 3 "Encoders and heads":
 // 2^b levels on b wires; Sec. 5 "Encoder") is the same kernel with another
 // code table: code[f][v] = round(v (2^b - 1) / 255), wire t = bit t.
-#include "bl_internal.h"
+#include "bl_device.h"
 
 namespace bl {
 namespace {
+
+using dev::transpose64;
+using dev::transpose_consts;
 
 constexpr int kThreads = 256;
 
@@ -54,43 +57,6 @@ __device__ __forceinline__ int64_t out_index(int64_t wire, int64_t wb, int64_t W
         return slab_index(wire, wb, rows);
     else
         return wire * W + wb;
-}
-
-// (sel & one) | (~sel & zero) as a single v_bfi_b32 (left to itself the
-// compiler splits it into and/or with an extra inverted-mask register)
-__device__ __forceinline__ uint32_t bfi(uint32_t sel, uint32_t one, uint32_t zero)
-{
-    uint32_t r;
-    asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(sel), "v"(one), "v"(zero));
-    return r;
-}
-
-// One block-swap stage of the 32x32 transpose inside each 32-lane half: lanes
-// l and l^S exchange the S-bit blocks that sit off the diagonal.
-template <int S, int K>
-__device__ __forceinline__ void swap_stage(uint32_t &v, const uint32_t (&amt)[5],
-                                           const uint32_t (&msk)[5])
-{
-    constexpr int kPattern = 0x1F | (S << 10);     // ds_swizzle bit mode: lane ^ S
-    const uint32_t y = (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, kPattern);
-    v = bfi(msk[K], v, __builtin_amdgcn_alignbit(y, y, amt[K]));
-}
-
-// 64x64 bit transpose across a wave.  In: lane l holds bits (lo, hi) = row l.
-// Out: lane p holds column p (bit l of (lo, hi) = old bit p of lane l).
-__device__ __forceinline__ void transpose64(uint32_t &lo, uint32_t &hi,
-                                            const uint32_t (&amt)[5], const uint32_t (&msk)[5])
-{
-    // off-diagonal 32x32 blocks: hi of lanes 0..31 <-> lo of lanes 32..63
-    const auto sw = __builtin_amdgcn_permlane32_swap(lo, hi, false, false);
-    lo = sw[0];
-    hi = sw[1];
-    // each register is now a 32x32 block per 32-lane half: recursive block swap
-    swap_stage<16, 0>(lo, amt, msk); swap_stage<16, 0>(hi, amt, msk);
-    swap_stage<8, 1>(lo, amt, msk);  swap_stage<8, 1>(hi, amt, msk);
-    swap_stage<4, 2>(lo, amt, msk);  swap_stage<4, 2>(hi, amt, msk);
-    swap_stage<2, 3>(lo, amt, msk);  swap_stage<2, 3>(hi, amt, msk);
-    swap_stage<1, 4>(lo, amt, msk);  swap_stage<1, 4>(hi, amt, msk);
 }
 
 template <int B>
@@ -197,16 +163,7 @@ __global__ __launch_bounds__(kThreads) void k_encode_t(
 
     // per-lane constants of the transpose stages
     uint32_t amt[5], msk[5];
-    {
-        const uint32_t low[5] = {0x0000FFFFu, 0x00FF00FFu, 0x0F0F0F0Fu, 0x33333333u, 0x55555555u};
-#pragma unroll
-        for (int k = 0; k < 5; ++k) {
-            const int s = 16 >> k;
-            const bool up = (lane & s) != 0;
-            amt[k] = up ? s : 32 - s;
-            msk[k] = up ? ~low[k] : low[k];
-        }
-    }
+    transpose_consts(lane, amt, msk);
 
     const int64_t t0 = tg * tiles_per_block;
     const int64_t t1 = min(t0 + tiles_per_block, n_tiles);

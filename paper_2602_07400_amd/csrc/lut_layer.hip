@@ -22,37 +22,16 @@
 // window bytes.  Windows are dealt to the 8 XCDs round-robin and each XCD
 // walks all node blocks of one window before the next, so that slab stays in
 // that XCD's L2 while every node reading it runs.
-#include "bl_internal.h"
+#include "bl_device.h"
 
 namespace bl {
 namespace {
 
+using dev::eval_node;
+using dev::mux_tree;
+
 constexpr int kThreads = 256;
 constexpr int kWavesPerBlock = kThreads / kWave;
-
-__device__ __forceinline__ uint32_t bfi(uint32_t sel, uint32_t one, uint32_t zero)
-{
-    return (sel & one) | (~sel & zero);
-}
-
-// Fold 2^K masks with K select words: level i pairs entries that differ in
-// address bit i, so the address bit order is slot 0 = least significant.
-template <int K>
-__device__ __forceinline__ uint32_t mux_tree(const uint32_t (&sel)[K],
-                                             const uint32_t (&m)[1 << K])
-{
-    uint32_t v[1 << (K - 1)];
-#pragma unroll
-    for (int a = 0; a < (1 << (K - 1)); ++a)
-        v[a] = bfi(sel[0], m[2 * a + 1], m[2 * a]);
-#pragma unroll
-    for (int i = 1; i < K; ++i) {
-#pragma unroll
-        for (int a = 0; a < (1 << (K - 1 - i)); ++a)
-            v[a] = bfi(sel[i], v[2 * a + 1], v[2 * a]);
-    }
-    return v[0];
-}
 
 // Access modes: whole windows with 16-byte or 8-byte accesses, or the one
 // ragged last window with per-word guards.  Separate instantiations keep the
@@ -203,52 +182,6 @@ __device__ __forceinline__ void gather(const uint64_t *src, const int32_t *c, in
                 xv[2 * r + 3][i] = a.w;
             }
         }
-    }
-}
-
-// Fold a K-input subtree whose 2^K leaf masks come from bits [base, base + 2^K)
-// of the table word t (a 32-bit half of the table).
-template <int K, int H>
-__device__ __forceinline__ void subtree(uint32_t t, const uint32_t (&xv)[H][6], uint32_t (&o)[H])
-{
-    uint32_t m[1 << K];
-#pragma unroll
-    for (int a = 0; a < (1 << K); ++a)
-        m[a] = 0u - ((t >> a) & 1u);
-#pragma unroll
-    for (int h = 0; h < H; ++h) {
-        uint32_t sel[K];
-#pragma unroll
-        for (int i = 0; i < K; ++i)
-            sel[i] = xv[h][i];
-        o[h] = mux_tree<K>(sel, m);
-    }
-}
-
-// Evaluate one node on 2R half-words (32 samples each).
-template <int K, int R>
-__device__ __forceinline__ void eval_node(uint64_t T, const uint32_t (&xv)[2 * R][K],
-                                          uint32_t (&o)[2 * R])
-{
-    if constexpr (K == 6) {
-        // Shannon split on x5: the two 5-input halves of the table are folded
-        // one after the other, so only 32 masks are live at a time
-        uint32_t lo[2 * R], hi[2 * R];
-        subtree<5, 2 * R>((uint32_t)T, xv, lo);
-        __builtin_amdgcn_sched_barrier(0);   // keep the two halves' masks apart
-        subtree<5, 2 * R>((uint32_t)(T >> 32), xv, hi);
-#pragma unroll
-        for (int h = 0; h < 2 * R; ++h)
-            o[h] = (xv[h][5] & hi[h]) | (~xv[h][5] & lo[h]);
-    } else {
-        const uint32_t t_lo = (uint32_t)T, t_hi = (uint32_t)(T >> 32);
-        uint32_t m[1 << K];
-#pragma unroll
-        for (int a = 0; a < (1 << K); ++a)
-            m[a] = 0u - (((a < 32 ? t_lo : t_hi) >> (a & 31)) & 1u);
-#pragma unroll
-        for (int h = 0; h < 2 * R; ++h)
-            o[h] = mux_tree<K>(xv[h], m);
     }
 }
 

@@ -94,6 +94,16 @@ for _k in (2, 4, 6):
         f"per-channel quantile thresholds, 2 x 64000 nodes, k={_k}, 10 classes x 6400",
         "c5_fanin")
 
+# The network shape the paper deploys (Sec. 7 hardware table; App. C.1): its
+# MNIST "best-of-space" network with a 4-threshold quantile thermometer on 784
+# features (3136 wires), two layers of 4000 nodes of fan-in 4 and a
+# 10-class popcount head, timed there at batches of 1024 and 64.  Random
+# tables and uniform pixels stand in for the trained checkpoint and MNIST.
+CONFIGS["paper_mnist_w4000"] = Config(
+    "paper_mnist_w4000", 1024, 784, 4, "quantile", (4000, 4000), 4, 10, "uniform", 1,
+    "the paper's deployed MNIST network shape: 784 features, 4 quantile thresholds "
+    "(3136 wires), 2 x 4000 nodes, k=4, 10 classes x 400; batch 1024")
+
 #: the order the configurations are listed in
 CONFIG_ORDER = ["c1_mnist_tiny", "c2_fmnist", "c3_cifar10", "c4_cifar100_wide",
                 "c5_fanin_k2", "c5_fanin_k4", "c5_fanin_k6"]
