@@ -117,28 +117,21 @@ struct ForwardPlan {
     bl::NetPlan net;
 };
 
-// Whole-network kernel: used for GroupSum networks whose activations of 64
-// samples fit in LDS, up to kNetAutoWords 64-sample columns (beyond that the
-// layered kernels amortize their node masks better) and up to kNetAutoNodes
-// nodes in all (one block evaluates every node of its column: with more, the
-// layered kernels' extra parallelism wins; measured on MI355X, 2 x 1000 nodes
-// ran 1.6x faster fused, 2 x 4000 nodes 1.2x slower).  BITLOGIC_FUSED_NETWORK
-// = 0 never uses it, = 1 uses it whenever the network fits.
-constexpr int64_t kNetAutoWords = 512;
-constexpr int64_t kNetAutoNodes = 4096;
-
+// Whole-network kernel (net_fused.hip): available for GroupSum networks whose
+// activations of 64 samples fit in LDS, on request only
+// (BITLOGIC_FUSED_NETWORK=1).  Measured on MI355X with HIP-graph replays, the
+// layered kernels were faster at every batch from 64 to 4096 samples (C1:
+// 28-29 us against 36 us; 2 x 4000 nodes: 35-37 us against 52-53 us): one
+// block's serial encode -> layers -> head chain has a higher floor than four
+// short kernels that each spread over many CUs.
 bitlogic_network legacy_net(int32_t n_features, const uint8_t *thresholds, int32_t n_thresholds,
                             const bitlogic_layer *layers, int32_t n_layers, int32_t n_classes,
                             const int8_t *dsp_weights);
 
-int fused_network_mode()
+bool fused_network_requested()
 {
     const char *e = getenv("BITLOGIC_FUSED_NETWORK");
-    if (e && e[0] == '0')
-        return 0;
-    if (e && e[0] == '1')
-        return 1;
-    return -1;
+    return e && e[0] == '1';
 }
 
 int plan_forward(int64_t n, int32_t d, int32_t b, const bitlogic_layer *layers, int32_t L,
@@ -181,7 +174,7 @@ int plan_forward(int64_t n, int32_t d, int32_t b, const bitlogic_layer *layers, 
     const size_t enc = (size_t)d * b * Wp * sizeof(uint64_t);
     const size_t act = (size_t)widest * Wp * sizeof(uint64_t);
     // the last layer and the head run fused when the group size allows it
-    const int32_t nb = bl::fused_head_nodes(w_last / c);
+    const int32_t nb = bl::fused_head_nodes(w_last / c, c, fp->n_slabs);
     fp->fused = nb > 0 && fused_head_enabled();
     fp->head = fp->fused ? bl::plan_fused_head(w_last, n, c, nb) : bl::plan_head(w_last, n, c);
     // layer l writes activation buffer l % 2, except a last layer fused with
@@ -325,12 +318,8 @@ int plan_network(const bitlogic_network *net, int64_t n, ForwardPlan *fp)
                       net->n_classes, fp);
     if (st != BITLOGIC_OK)
         return st;
-    const int mode = fused_network_mode();
-    int64_t nodes = 0;
-    for (int32_t l = 0; l < net->n_layers; ++l)
-        nodes += net->layers[l].w_out;
-    if (mode != 0 && net->head == BITLOGIC_HEAD_GROUPSUM && net->n_layers <= bl::kNetMaxLayers &&
-        (mode == 1 || (fp->W <= kNetAutoWords && nodes <= kNetAutoNodes))) {
+    if (fused_network_requested() && net->head == BITLOGIC_HEAD_GROUPSUM &&
+        net->n_layers <= bl::kNetMaxLayers) {
         int32_t w_out[bl::kNetMaxLayers];
         for (int32_t l = 0; l < net->n_layers; ++l)
             w_out[l] = net->layers[l].w_out;

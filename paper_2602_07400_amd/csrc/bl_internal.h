@@ -72,10 +72,11 @@ hipError_t launch_lut_layer(const uint64_t *in, int32_t w_in, int64_t n_words,
                             hipStream_t stream);
 
 // Last LUT layer fused with the GroupSum head (slab layout): writes the head's
-// bit planes instead of the layer's bits.  fused_head_nodes(g) is the node
-// count of one block (a divisor of the group size g), or 0 when g does not
-// allow the fused kernel.
-int32_t fused_head_nodes(int32_t g);
+// bit planes instead of the layer's bits.  fused_head_nodes(g, c, n_slabs) is the
+// node count of one block (a multiple of 32 dividing the group size g; fewer
+// passes per block for small batches), or 0 when g does not allow the fused
+// kernel.
+int32_t fused_head_nodes(int32_t g, int32_t c, int64_t n_slabs);
 hipError_t launch_lut_slab_head(const uint64_t *in, int32_t w_in, int64_t n_slabs,
                                 const int32_t *conn, const uint64_t *tables, int32_t w_out,
                                 int32_t k, int32_t c, int64_t W, uint64_t *planes, int32_t P,

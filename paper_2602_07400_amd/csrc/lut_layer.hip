@@ -258,22 +258,40 @@ __global__ __launch_bounds__(kThreads, BL_LUT_MINWAVES) void k_lut_slab(
     }
 }
 
+// Nodes per block: 512 (8 passes over one staging of connections and
+// tables) when the launch has blocks to spare; one pass per block when the
+// batch is so small that 512-node blocks would leave most CUs idle and each
+// block's passes would run one gather latency after another.
 constexpr int kSlabNB = 512;
+constexpr int kSlabNBSmall = kThreads / kSlabLanes;     // one pass
+constexpr int64_t kSlabSmallBlocks = 2048;
+
+template <int K, int NB>
+hipError_t launch_slab_kn(const uint64_t *in, int32_t w_in, int64_t n_slabs,
+                          const int32_t *conn, const uint64_t *tables, int32_t w_out,
+                          uint64_t *out, hipStream_t stream)
+{
+    const int32_t n_nblk = (w_out + NB - 1) / NB;
+    const int64_t slabs_pad = (n_slabs + kXcds - 1) / kXcds * kXcds;
+    const int64_t blocks = slabs_pad * n_nblk;
+    if (blocks > 0x7fffffff)
+        return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((k_lut_slab<K, kSlabWords, kSlabLanes, NB>), dim3((unsigned)blocks),
+                       dim3(kThreads), 0, stream, in, w_in, conn, tables, w_out, out, n_nblk,
+                       (int32_t)n_slabs);
+    return hipGetLastError();
+}
 
 template <int K>
 hipError_t launch_slab_k(const uint64_t *in, int32_t w_in, int64_t n_slabs,
                          const int32_t *conn, const uint64_t *tables, int32_t w_out,
                          uint64_t *out, hipStream_t stream)
 {
-    const int32_t n_nblk = (w_out + kSlabNB - 1) / kSlabNB;
-    const int64_t slabs_pad = (n_slabs + kXcds - 1) / kXcds * kXcds;
-    const int64_t blocks = slabs_pad * n_nblk;
-    if (blocks > 0x7fffffff)
-        return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((k_lut_slab<K, kSlabWords, kSlabLanes, kSlabNB>), dim3((unsigned)blocks),
-                       dim3(kThreads), 0, stream, in, w_in, conn, tables, w_out, out, n_nblk,
-                       (int32_t)n_slabs);
-    return hipGetLastError();
+    const int64_t big = n_slabs * ((w_out + kSlabNB - 1) / kSlabNB);
+    if (big < kSlabSmallBlocks)
+        return launch_slab_kn<K, kSlabNBSmall>(in, w_in, n_slabs, conn, tables, w_out, out,
+                                                stream);
+    return launch_slab_kn<K, kSlabNB>(in, w_in, n_slabs, conn, tables, w_out, out, stream);
 }
 
 // ---------------------------------------------------------------------------
@@ -520,12 +538,17 @@ hipError_t launch_lut_layer_slab(const uint64_t *in, int32_t w_in, int64_t n_sla
     }
 }
 
-int32_t fused_head_nodes(int32_t g)
+int32_t fused_head_nodes(int32_t g, int32_t c, int64_t n_slabs)
 {
     if (kSlabWords != 16 || g <= 0 || g % kHeadPassNodes != 0)
         return 0;
     const int32_t units = g / kHeadPassNodes;
-    for (int p = kHeadMaxPasses; p >= 1; --p)
+    // small batches: fewer passes per block until the launch has
+    // kSlabSmallBlocks blocks (n_slabs * c * units / p of them)
+    int max_p = kHeadMaxPasses;
+    while (max_p > 1 && n_slabs * c * (int64_t)(units / max_p) < kSlabSmallBlocks)
+        --max_p;
+    for (int p = max_p; p >= 1; --p)
         if (units % p == 0)
             return p * kHeadPassNodes;
     return 0;
@@ -537,7 +560,7 @@ hipError_t launch_lut_slab_head(const uint64_t *in, int32_t w_in, int64_t n_slab
                                 hipStream_t stream)
 {
     const int32_t g = w_out / c;
-    const int32_t nb = fused_head_nodes(g);
+    const int32_t nb = fused_head_nodes(g, c, n_slabs);
     if (nb == 0)
         return hipErrorInvalidValue;
     switch (k) {

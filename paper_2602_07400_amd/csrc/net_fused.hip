@@ -2,10 +2,10 @@
 // samples fit in LDS (Sec. 3, Eq. 1: encoder -> D LUT layers -> GroupSum
 // head; App. C.1).
 //
-// Small networks at small batches are latency-bound: the layered forward
-// spends most of its time launching and draining one kernel per stage.  Here
-// one block of 512 threads takes a 64-sample column through every stage
-// without leaving the CU:
+// Small networks at small batches are latency-bound, and this kernel tries
+// to remove the stage boundaries: one block of 512 threads takes a 64-sample
+// column through every stage without leaving the CU (used on request; on
+// MI355X the layered kernels measured faster, see the forward's planner):
 //   1. encode: each wave packs 64-wire groups of the column's samples (codes
 //      computed from the thresholds, or the binary code) and transposes them
 //      across the wave (dev::transpose64) into one word per wire in LDS;

@@ -292,20 +292,20 @@ def test_whole_network_plan(lib, monkeypatch):
     info = bl._ForwardInfo()
     ref = ctypes.byref(info)
     p, keep = _layers([(1000, 6), (1000, 6)])
+    # off unless requested
     monkeypatch.delenv("BITLOGIC_FUSED_NETWORK", raising=False)
-    # C1: 784 wires + 2 x 1000 nodes of 64 samples fit in LDS, small batch
     assert lib.bitlogic_forward_plan(4096, 784, 1, p, 2, 10, ref) == OK
-    assert info.fused_network == 1
-    # a large batch takes the layered kernels, unless forced
-    assert lib.bitlogic_forward_plan(1 << 20, 784, 1, p, 2, 10, ref) == OK
     assert info.fused_network == 0
     monkeypatch.setenv("BITLOGIC_FUSED_NETWORK", "1")
+    # C1: 784 wires + 2 x 1000 nodes of 64 samples fit in LDS, at any batch
+    assert lib.bitlogic_forward_plan(4096, 784, 1, p, 2, 10, ref) == OK
+    assert info.fused_network == 1
     assert lib.bitlogic_forward_plan(1 << 20, 784, 1, p, 2, 10, ref) == OK
     assert info.fused_network == 1
-    monkeypatch.setenv("BITLOGIC_FUSED_NETWORK", "0")
-    assert lib.bitlogic_forward_plan(4096, 784, 1, p, 2, 10, ref) == OK
-    assert info.fused_network == 0
-    monkeypatch.delenv("BITLOGIC_FUSED_NETWORK")
+    # the paper's deployed network shape (3136 wires, 2 x 4000 nodes) fits
+    pp, keepp = _layers([(4000, 4), (4000, 4)])
+    assert lib.bitlogic_forward_plan(1024, 784, 4, pp, 2, 10, ref) == OK
+    assert info.fused_network == 1
     # too wide for LDS (C4), more than 8 code bits, or the quantized head: layered
     p4, keep4 = _layers([(64000, 6), (64000, 6)])
     assert lib.bitlogic_forward_plan(4096, 3072, 7, p4, 2, 100, ref) == OK
@@ -314,12 +314,3 @@ def test_whole_network_plan(lib, monkeypatch):
     assert info.fused_network == 0
     assert lib.bitlogic_network_plan(ctypes.byref(_net(p, head=1, w=FAKE)), 4096, ref) == OK
     assert info.fused_network == 0
-    # the paper's deployed network shape (3136 wires, 2 x 4000 nodes, 10 classes)
-    # fits, but with 8000 nodes per block the layered kernels are chosen unless forced
-    pp, keepp = _layers([(4000, 4), (4000, 4)])
-    assert lib.bitlogic_forward_plan(1024, 784, 4, pp, 2, 10, ref) == OK
-    assert info.fused_network == 0
-    monkeypatch.setenv("BITLOGIC_FUSED_NETWORK", "1")
-    assert lib.bitlogic_forward_plan(1024, 784, 4, pp, 2, 10, ref) == OK
-    assert info.fused_network == 1
-    monkeypatch.delenv("BITLOGIC_FUSED_NETWORK")
