@@ -69,14 +69,19 @@ def parse():
                          "uniform fixed-point code (layer 1 is redrawn if the wire count changes)")
     ap.add_argument("--bits", type=int, default=None,
                     help="code width of the binary encoder (default: the configuration's b)")
+    ap.add_argument("--specialize", action="store_true",
+                    help="evaluate the network from its specialized tables (tied and "
+                         "ignored inputs removed, nodes ordered by effective fan-in)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run a write-only fill and a read-only sum over this many MiB "
                          "(reference kernels for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     return ap.parse_args()
 
 
-def algorithmic(cfg, n, fused_head, binary_bits=0):
-    """Compulsory bytes and algorithmic 32-bit lane-ops per stage of one forward."""
+def algorithmic(cfg, n, fused_head, binary_bits=0, fanin_hist=None):
+    """Compulsory bytes and algorithmic 32-bit lane-ops per stage of one forward.
+    fanin_hist: per layer, None or the node count per effective fan-in 0..6 of
+    a specialized layer (its multiplexers: 2^k' - 1 per node)."""
     W = (n + 63) // 64
     D0 = cfg.d * (binary_bits or cfg.b)
     st = {"encode": {"bytes": n * cfg.d + D0 * W * 8, "ops": n * D0}}
@@ -84,10 +89,13 @@ def algorithmic(cfg, n, fused_head, binary_bits=0):
     L = len(cfg.widths)
     for l, w in enumerate(cfg.widths):
         last_fused = fused_head and l == L - 1
+        h = fanin_hist[l] if fanin_hist else None
+        muxes = (((1 << cfg.k) - 1) * w if h is None else
+                 sum(int(c) * ((1 << q) - 1) for q, c in enumerate(h)))
         st[f"layer{l + 1}"] = {
             # a fused last layer reads its input and hands counts to the head
             "bytes": (w_in + (0 if last_fused else w)) * W * 8,
-            "ops": 2 * ((1 << cfg.k) - 1) * w * W + (n * w // 32 if last_fused else 0)}
+            "ops": 2 * muxes * W + (n * w // 32 if last_fused else 0)}
         w_in = w
     out_bytes = 4 * n * cfg.n_classes + 4 * n
     if fused_head:
@@ -163,7 +171,7 @@ def main():
                                         wl.n_classes, device=dev,
                                         encoder="binary" if binary_bits else "thermometer",
                                         n_features=cfg.d, n_bits=binary_bits or None,
-                                        head_weights=dsp_np)
+                                        head_weights=dsp_np, specialize=args.specialize)
     dsp_w = model.head_weights
     x = torch.from_numpy(wl.x).to(dev)
     ws = torch.empty(model.workspace_bytes(n), dtype=torch.uint8, device=dev)
@@ -230,7 +238,8 @@ def main():
         # on the launch stream around repeated calls
         counts = torch.empty((n, cfg.n_classes), dtype=torch.int32, device=dev)
         plain = bl.BitlogicModel(model.thresholds, model.layers, model.n_classes, model.n_features,
-                                 model.encoder, model.n_bits)
+                                 model.encoder, model.n_bits, pass_fanin=model.pass_fanin,
+                                 fanin_histogram=model.fanin_histogram, order=model.order)
         plain.forward(x, out=counts, argmax=argmax, workspace=ws, stream=stream)
         lg = torch.empty_like(counts)
         reps = max(ksteps, 10)
@@ -278,7 +287,7 @@ def main():
                   "frac_of_hbm_peak": round(n * cfg.d / (fit_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
 
     fused = plan["fused_head"]
-    alg = algorithmic(cfg, n, fused, binary_bits)
+    alg = algorithmic(cfg, n, fused, binary_bits, model.fanin_histogram)
     if whole:
         # compulsory traffic of the single kernel: pixels in, scores and argmax out
         ops = sum(v["ops"] for v in alg.values())
@@ -307,6 +316,8 @@ def main():
         kname = STAGE_KERNELS["layer_fused"]
     else:
         kname = STAGE_KERNELS["layer"]
+    if model.pass_fanin and dom in layer_names:
+        kname += ", specialized (one fan-in per pass)"
     roofline = {"bound": a["bound"], "achieved": round(achieved, 3), "peak": round(peak, 3),
                 "unit": unit, "frac": round(achieved / peak, 4),
                 "traffic": measured_traffic(dom) if cfg.name == "c4_cifar100_wide" else None,
@@ -326,6 +337,10 @@ def main():
         "staged_sum_ms": round(sum(stage_ms.values()), 4),
         "fused_head": fused,
         "fused_network": whole,
+        "specialized": bool(args.specialize),
+        "fanin_histogram": ([None if h is None else [int(v) for v in h]
+                             for h in model.fanin_histogram]
+                            if model.fanin_histogram else None),
         "head": args.head,
         "encoder": args.encoder + (f" ({binary_bits} bits)" if binary_bits else ""),
         "grouped_dsp_head": dsp_detail,
@@ -386,7 +401,8 @@ def main():
         "config": {"workload": cfg.description
                    + ("" if not binary_bits else
                       f"; binary-coded {binary_bits}-bit encoder instead of the thermometer")
-                   + ("" if dsp_w is None else "; quantized c x c head on the group sums"),
+                   + ("" if dsp_w is None else "; quantized c x c head on the group sums")
+                   + ("" if not args.specialize else "; table-specialized layers"),
                    "name": cfg.name, "head": args.head, "encoder": args.encoder,
                    "n_samples": n,
                    "features": cfg.d, "thresholds": cfg.b, "widths": list(cfg.widths),

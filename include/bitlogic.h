@@ -257,6 +257,59 @@ int bitlogic_fit_quantile_thresholds(const uint8_t *x, int64_t n_samples, int32_
 
 /* ---- Network descriptor: any encoder, any head --------------------------- */
 
+/* ---- Table specialization ------------------------------------------------ */
+
+/* Table specialization of a layer (host arrays, no HIP call): the collapse
+ * the paper's synthesis flow applies to the per-node tables it emits (Sec. 5
+ * "Connectivity": slots tied to the same wire reduce a table to a function of
+ * fewer effective inputs; App. C.2, one table per node).  For every node j:
+ * connection slots that repeat an earlier slot's wire are merged (only
+ * addresses whose bits agree can occur), slots the table does not depend on
+ * are dropped, and the table is rewritten over the k_eff[j] remaining slots,
+ * which keep their order (k_eff = 0: a constant node, output bit = table
+ * bit 0).  Evaluating conn_out[j][0..k_eff-1] with tables_out[j] gives the
+ * node's output for every input, with 2^k_eff - 1 multiplexers instead of
+ * 2^k - 1.
+ *   conn [w_out][k], tables [w_out] in; k_eff [w_out], conn_out [w_out][k]
+ *   (slots past k_eff are 0), tables_out [w_out] out.
+ * Returns BITLOGIC_ERR_SHAPE if a connection is outside [0, w_in). */
+int bitlogic_specialize_layer(const int32_t *conn, const uint64_t *tables, int32_t w_out,
+                              int32_t k, int32_t w_in, int32_t *k_eff, int32_t *conn_out,
+                              uint64_t *tables_out);
+
+/* Table specialization of a whole network (host arrays, no HIP call), ready
+ * for bitlogic_network_forward.  Every node is specialized as above; then
+ * each layer's nodes are reordered by effective fan-in, largest first
+ * (within each class group of the last layer, so every class keeps its
+ * nodes), the next layer's connections are relabelled to the new order, and
+ * every run of BITLOGIC_SPECIALIZE_PASS positions records its largest
+ * fan-in in fanin_out.  The specialized layer's fan-in k_out[l] is the
+ * largest effective fan-in of its nodes (at least 1).  Slots past a node's
+ * effective fan-in repeat its first wire (wire 0 for a constant node) and
+ * its table is extended over all k_out[l] slots so that it ignores them:
+ * evaluating the first kp slots, for any kp from the node's effective fan-in
+ * up to k_out[l], gives the node's output.  The result computes the same
+ * scores as the original network; its hidden activations are the original
+ * ones permuted.
+ *   w_in: encoder wires (n_features * n_bits); per layer l (host arrays of
+ *   n_layers pointers): conn[l] [w_out[l]][k[l]], tables[l] [w_out[l]] in;
+ *   k_out [n_layers]; conn_out[l] [w_out[l]][k_out[l]] (allocate
+ *   w_out[l] * k[l] entries), tables_out[l] [w_out[l]],
+ *   fanin_out[l] [ceil(w_out[l] / BITLOGIC_SPECIALIZE_PASS)] out;
+ *   order_out: NULL, or per layer [w_out[l]] (the original node at each
+ *   position).  The specialized network for bitlogic_network_forward has
+ *   layers {conn_out[l], tables_out[l], w_out[l], k_out[l]} and pass_fanin
+ *   fanin_out (on the device).
+ * Returns BITLOGIC_ERR_SHAPE if a connection is out of range or the last
+ * width is not a multiple of n_classes. */
+#define BITLOGIC_SPECIALIZE_PASS 32
+int bitlogic_specialize_network(int32_t w_in, const int32_t *const *conn,
+                                const uint64_t *const *tables, const int32_t *w_out,
+                                const int32_t *k, int32_t n_layers, int32_t n_classes,
+                                int32_t *k_out, int32_t *const *conn_out,
+                                uint64_t *const *tables_out, uint8_t *const *fanin_out,
+                                int32_t *const *order_out);
+
 enum { BITLOGIC_ENCODER_THERMOMETER = 0, BITLOGIC_ENCODER_BINARY = 1 };
 enum { BITLOGIC_HEAD_GROUPSUM = 0, BITLOGIC_HEAD_GROUPED_DSP = 1 };
 
@@ -274,6 +327,15 @@ typedef struct bitlogic_network {
     int32_t n_classes;              /* c; the last width is a multiple of c       */
     int32_t head;                   /* BITLOGIC_HEAD_*                            */
     const int8_t *head_weights;     /* [c][c] int8, GROUPED_DSP only (c <= 128)   */
+    const uint8_t *const *pass_fanin;
+                                    /* NULL, or a host array of n_layers device
+                                       pointers: a non-NULL entry marks layer l
+                                       as specialized (bitlogic_specialize_network)
+                                       and holds its fan-in per run of
+                                       BITLOGIC_SPECIALIZE_PASS nodes: each
+                                       node's output is read from its first
+                                       fan-in slots (values above k[l] are
+                                       clamped to it)                            */
 } bitlogic_network;
 
 /* Workspace bytes of bitlogic_network_forward for n_samples (0 if the

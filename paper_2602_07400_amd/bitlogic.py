@@ -25,7 +25,8 @@ __all__ = [
     "bitlogic_forward_plan", "bitlogic_grouped_dsp_head", "bitlogic_forward_grouped_dsp",
     "bitlogic_encode_binary", "bitlogic_fit_quantile_thresholds", "bitlogic_network_forward",
     "bitlogic_groupsum_head_workspace_bytes", "bitlogic_status_string", "bitlogic_version",
-    "BitlogicModel", "library_path", "load_library", "words",
+    "BitlogicModel", "bitlogic_specialize_layer", "bitlogic_specialize_network", "library_path",
+    "load_library", "words",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -61,7 +62,11 @@ class _Network(ctypes.Structure):
                 ("n_bits", ctypes.c_int32), ("thresholds", ctypes.c_void_p),
                 ("layers", ctypes.c_void_p), ("n_layers", ctypes.c_int32),
                 ("n_classes", ctypes.c_int32), ("head", ctypes.c_int32),
-                ("head_weights", ctypes.c_void_p)]
+                ("head_weights", ctypes.c_void_p), ("pass_fanin", ctypes.c_void_p)]
+
+
+MAX_FANIN = 6
+SPECIALIZE_PASS = 32          # nodes per entry of a specialized layer's fan-in array
 
 
 def library_path() -> str:
@@ -98,6 +103,9 @@ def load_library():
         "bitlogic_forward": ([P, i64, i32, P, i32, P, i32, i32, P, P, P, sz, P], ctypes.c_int),
         "bitlogic_forward_timed": ([P, i64, i32, P, i32, P, i32, i32, P, P, P, sz, P, P, i32],
                                    ctypes.c_int),
+        "bitlogic_specialize_layer": ([P, P, i32, i32, i32, P, P, P], ctypes.c_int),
+        "bitlogic_specialize_network": ([i32, P, P, P, P, i32, i32, P, P, P, P, P],
+                                        ctypes.c_int),
         "bitlogic_status_string": ([ctypes.c_int], ctypes.c_char_p),
         "bitlogic_last_error": ([], ctypes.c_char_p),
         "bitlogic_version": ([], ctypes.c_int),
@@ -383,6 +391,52 @@ def bitlogic_forward_timed(x: torch.Tensor, thresholds: torch.Tensor,
                     want_scores, list(events))
 
 
+def bitlogic_specialize_layer(conn, tables, w_in: int):
+    """Table specialization of one layer on the host (bitlogic_specialize_layer):
+    conn int32 [w][k], tables uint64 [w] -> (k_eff int32 [w], conn_eff int32
+    [w][k] with slots past k_eff zero, tables_eff uint64 [w])."""
+    conn = np.ascontiguousarray(conn, dtype=np.int32)
+    tables = np.ascontiguousarray(tables, dtype=np.uint64)
+    if conn.ndim != 2 or tables.shape != (conn.shape[0],):
+        raise ValueError("conn [w][k] and tables [w] expected")
+    w, k = conn.shape
+    k_eff = np.zeros(w, dtype=np.int32)
+    conn_eff = np.zeros_like(conn)
+    tables_eff = np.zeros_like(tables)
+    _check(load_library().bitlogic_specialize_layer(
+        conn.ctypes.data, tables.ctypes.data, w, k, int(w_in), k_eff.ctypes.data,
+        conn_eff.ctypes.data, tables_eff.ctypes.data))
+    return k_eff, conn_eff, tables_eff
+
+
+def bitlogic_specialize_network(layers, w_in: int, n_classes: int):
+    """Table specialization of a whole network on the host
+    (bitlogic_specialize_network): layers [(conn int32 [w][k], tables uint64
+    [w])] -> [(conn, tables, fanin uint8 [ceil(w / 32)], order int32 [w])] per
+    layer, the nodes reordered by effective fan-in; conn has the layer's
+    largest effective fan-in as its width."""
+    conns = [np.ascontiguousarray(c, dtype=np.int32) for c, _ in layers]
+    tabs = [np.ascontiguousarray(t, dtype=np.uint64) for _, t in layers]
+    L = len(layers)
+    outs = [(np.zeros_like(c), np.zeros_like(t),
+             np.zeros((c.shape[0] + SPECIALIZE_PASS - 1) // SPECIALIZE_PASS, np.uint8),
+             np.zeros(c.shape[0], np.int32)) for c, t in zip(conns, tabs)]
+    arr = lambda xs, ty: (ty * L)(*[x.ctypes.data for x in xs])
+    P = ctypes.c_void_p
+    k_out = (ctypes.c_int32 * L)()
+    _check(load_library().bitlogic_specialize_network(
+        int(w_in), arr(conns, P), arr(tabs, P),
+        (ctypes.c_int32 * L)(*[c.shape[0] for c in conns]),
+        (ctypes.c_int32 * L)(*[c.shape[1] for c in conns]), L, int(n_classes), k_out,
+        arr([o[0] for o in outs], P), arr([o[1] for o in outs], P),
+        arr([o[2] for o in outs], P), arr([o[3] for o in outs], P)))
+    res = []
+    for (c, t, f, o), kn in zip(outs, k_out):
+        w = c.shape[0]
+        res.append((np.ascontiguousarray(c.reshape(-1)[:w * kn].reshape(w, kn)), t, f, o))
+    return res
+
+
 @dataclass
 class BitlogicModel:
     """A network resident in device memory: encoder (thermometer thresholds, or
@@ -395,6 +449,12 @@ class BitlogicModel:
     n_bits: int = 0
     head: int = HEAD_GROUPSUM
     head_weights: Optional[torch.Tensor] = None
+    # specialized network: per layer the fan-in of each run of 32 nodes
+    # (device), the node count per effective fan-in 0..6 and the original
+    # node at each position
+    pass_fanin: Optional[List[torch.Tensor]] = None
+    fanin_histogram: Optional[list] = None
+    order: Optional[list] = None
 
     def __post_init__(self):
         if self.thresholds is not None and self.encoder == ENCODER_THERMOMETER:
@@ -403,11 +463,14 @@ class BitlogicModel:
     @classmethod
     def from_numpy(cls, thresholds, layers, n_classes: int, device="cuda",
                    encoder: str = "thermometer", n_features: Optional[int] = None,
-                   n_bits: Optional[int] = None, head_weights=None) -> "BitlogicModel":
+                   n_bits: Optional[int] = None, head_weights=None,
+                   specialize=False) -> "BitlogicModel":
         """Copy a host model to the GPU, checking every connection index.
         encoder "thermometer" takes thresholds uint8 [d][b]; "binary" takes
         n_features and n_bits (thresholds None).  head_weights int8 [c][c]
-        selects the quantized head."""
+        selects the quantized head.  specialize=True evaluates the network
+        from its specialized tables (bitlogic_specialize_network: tied and
+        ignored inputs removed, nodes ordered by effective fan-in)."""
         if encoder == "thermometer":
             th = np.ascontiguousarray(thresholds, dtype=np.uint8)
             if th.ndim != 2:
@@ -422,7 +485,7 @@ class BitlogicModel:
         else:
             raise ValueError(f"unknown encoder {encoder!r}")
         w_in = d * b
-        dev_layers = []
+        dev_layers, host_layers = [], []
         for l, (conn, tables) in enumerate(layers):
             conn = np.ascontiguousarray(conn, dtype=np.int32)
             tables = np.ascontiguousarray(tables, dtype=np.uint64)
@@ -430,18 +493,38 @@ class BitlogicModel:
                 raise ValueError(f"layer {l}: conn [w][k] and tables [w] expected")
             if conn.size and (conn.min() < 0 or conn.max() >= w_in):
                 raise ValueError(f"layer {l}: connection index outside [0, {w_in})")
-            dev_layers.append((torch.from_numpy(conn).to(device),
-                               torch.from_numpy(tables.view(np.int64)).to(device)))
+            host_layers.append((conn, tables))
             w_in = conn.shape[0]
         if w_in % n_classes != 0:
             raise ValueError("last width must be a multiple of n_classes")
+        fanin = hist = order = None
+        if specialize:
+            spec = bitlogic_specialize_network(host_layers, d * b, n_classes)
+            hist, w_prev = [], d * b
+            for conn, tables in host_layers:
+                k_eff, _, _ = bitlogic_specialize_layer(conn, tables, w_prev)
+                hist.append(np.bincount(k_eff, minlength=MAX_FANIN + 1))
+                w_prev = conn.shape[0]
+            host_layers = [(c, t) for c, t, _, _ in spec]
+            fanin = [torch.from_numpy(f).to(device) for _, _, f, _ in spec]
+            order = [o for _, _, _, o in spec]
+        for conn, tables in host_layers:
+            dev_layers.append((torch.from_numpy(conn).to(device),
+                               torch.from_numpy(tables.view(np.int64)).to(device)))
         hw, head = None, HEAD_GROUPSUM
         if head_weights is not None:
             q = np.ascontiguousarray(head_weights, dtype=np.int8)
             if q.shape != (n_classes, n_classes):
                 raise ValueError("head_weights must be [c][c]")
             hw, head = torch.from_numpy(q).to(device), HEAD_GROUPED_DSP
-        return cls(th_dev, dev_layers, int(n_classes), d, kind, b, head, hw)
+        return cls(th_dev, dev_layers, int(n_classes), d, kind, b, head, hw, fanin, hist, order)
+
+    def _fanin_array(self):
+        if not self.pass_fanin:
+            return None, None
+        ptrs = (ctypes.c_void_p * len(self.layers))(
+            *[_dev(f, "pass_fanin", (torch.uint8,)) for f in self.pass_fanin])
+        return ctypes.cast(ptrs, ctypes.c_void_p), ptrs
 
     def _net(self):
         arr = _layer_array(self.layers)
@@ -455,7 +538,8 @@ class BitlogicModel:
         net.head = self.head
         net.head_weights = (_dev(self.head_weights, "head_weights", _I8)
                             if self.head_weights is not None else None)
-        return net, arr
+        net.pass_fanin, keep = self._fanin_array()
+        return net, (arr, keep)
 
     def workspace_bytes(self, n_samples: int) -> int:
         net, keep = self._net()

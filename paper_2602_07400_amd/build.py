@@ -13,7 +13,8 @@ INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 LIB = os.path.join(HERE, "libbitlogic.so")
 OBJ_DIR = os.path.join(HERE, "_build")
 
-SOURCES = ["encode.hip", "lut_layer.hip", "head.hip", "fit.hip", "net_fused.hip", "api.hip"]
+SOURCES = ["encode.hip", "lut_layer.hip", "head.hip", "fit.hip", "net_fused.hip", "specialize.hip",
+           "api.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -319,7 +319,7 @@ int plan_network(const bitlogic_network *net, int64_t n, ForwardPlan *fp)
     if (st != BITLOGIC_OK)
         return st;
     if (fused_network_requested() && net->head == BITLOGIC_HEAD_GROUPSUM &&
-        net->n_layers <= bl::kNetMaxLayers) {
+        net->n_layers <= bl::kNetMaxLayers && !net->pass_fanin) {
         int32_t w_out[bl::kNetMaxLayers];
         for (int32_t l = 0; l < net->n_layers; ++l)
             w_out[l] = net->layers[l].w_out;
@@ -412,13 +412,15 @@ int forward_impl(const bitlogic_network *net, const uint8_t *x, int64_t n_sample
     for (int32_t l = 0; l < n_layers; ++l) {
         const bool last_fused = fp.fused && l == n_layers - 1;
         uint64_t *dst = act[l & 1];
+        const uint8_t *fanin = net->pass_fanin ? net->pass_fanin[l] : nullptr;
         if (last_fused)
             e = bl::launch_lut_slab_head(cur, w_in, fp.n_slabs, layers[l].conn, layers[l].tables,
                                          layers[l].w_out, layers[l].k, n_classes, fp.W, planes,
-                                         fp.head.planes, s);
+                                         fp.head.planes, s, fanin);
         else
             e = bl::launch_lut_layer_slab(cur, w_in, fp.n_slabs, layers[l].conn,
-                                          layers[l].tables, layers[l].w_out, layers[l].k, dst, s);
+                                          layers[l].tables, layers[l].w_out, layers[l].k, dst, s,
+                                          fanin);
         if (e == hipSuccess)
             e = mark(2 + l);
         if (e != hipSuccess)
@@ -451,6 +453,7 @@ bitlogic_network legacy_net(int32_t n_features, const uint8_t *thresholds, int32
     net.n_classes = n_classes;
     net.head = dsp_weights ? BITLOGIC_HEAD_GROUPED_DSP : BITLOGIC_HEAD_GROUPSUM;
     net.head_weights = dsp_weights;
+    net.pass_fanin = nullptr;
     return net;
 }
 
@@ -578,6 +581,65 @@ int bitlogic_encode_binary(const uint8_t *x, int64_t n_samples, int32_t n_featur
                                         bl::kLayoutRowMajor, words_of(n_samples),
                                         (hipStream_t)stream, bl::kEncBinary),
                       "encode_binary launch");
+}
+
+int bitlogic_specialize_layer(const int32_t *conn, const uint64_t *tables, int32_t w_out,
+                              int32_t k, int32_t w_in, int32_t *k_eff, int32_t *conn_out,
+                              uint64_t *tables_out)
+{
+    if (!conn || !tables || !k_eff || !conn_out || !tables_out)
+        return fail(BITLOGIC_ERR_NULL, "specialize_layer: NULL pointer");
+    if (k < 1 || k > 6)
+        return fail(BITLOGIC_ERR_UNSUPPORTED, "specialize_layer: fan-in %d outside 1..6", k);
+    if (w_out < 0 || w_in <= 0)
+        return fail(BITLOGIC_ERR_SHAPE, "specialize_layer: need w_out >= 0, w_in > 0");
+    for (int64_t q = 0; q < (int64_t)w_out * k; ++q)
+        if (conn[q] < 0 || conn[q] >= w_in)
+            return fail(BITLOGIC_ERR_SHAPE, "specialize_layer: connection %lld = %d outside [0, %d)",
+                        (long long)q, conn[q], w_in);
+    for (int32_t j = 0; j < w_out; ++j) {
+        int32_t *co = conn_out + (int64_t)j * k;
+        k_eff[j] = bl::specialize_node(conn + (int64_t)j * k, tables[j], k, co, &tables_out[j]);
+        for (int i = k_eff[j]; i < k; ++i)
+            co[i] = 0;
+    }
+    return ok();
+}
+
+int bitlogic_specialize_network(int32_t w_in, const int32_t *const *conn,
+                                const uint64_t *const *tables, const int32_t *w_out,
+                                const int32_t *k, int32_t n_layers, int32_t n_classes,
+                                int32_t *k_out, int32_t *const *conn_out,
+                                uint64_t *const *tables_out, uint8_t *const *fanin_out,
+                                int32_t *const *order_out)
+{
+    if (!conn || !tables || !w_out || !k || !k_out || !conn_out || !tables_out || !fanin_out)
+        return fail(BITLOGIC_ERR_NULL, "specialize_network: NULL pointer");
+    if (n_layers < 1 || w_in <= 0 || n_classes < 1)
+        return fail(BITLOGIC_ERR_SHAPE, "specialize_network: need n_layers, w_in, n_classes > 0");
+    int32_t wi = w_in;
+    for (int32_t l = 0; l < n_layers; ++l) {
+        if (!conn[l] || !tables[l] || !conn_out[l] || !tables_out[l] || !fanin_out[l] ||
+            (order_out && !order_out[l]))
+            return fail(BITLOGIC_ERR_NULL, "specialize_network: layer %d NULL pointer", l);
+        if (k[l] < 1 || k[l] > 6)
+            return fail(BITLOGIC_ERR_UNSUPPORTED, "specialize_network: layer %d fan-in %d", l,
+                        k[l]);
+        if (w_out[l] <= 0)
+            return fail(BITLOGIC_ERR_SHAPE, "specialize_network: layer %d width %d", l, w_out[l]);
+        for (int64_t q = 0; q < (int64_t)w_out[l] * k[l]; ++q)
+            if (conn[l][q] < 0 || conn[l][q] >= wi)
+                return fail(BITLOGIC_ERR_SHAPE,
+                            "specialize_network: layer %d connection %lld = %d outside [0, %d)",
+                            l, (long long)q, conn[l][q], wi);
+        wi = w_out[l];
+    }
+    if (wi % n_classes != 0)
+        return fail(BITLOGIC_ERR_SHAPE, "specialize_network: last width %d not a multiple of %d",
+                    wi, n_classes);
+    bl::specialize_network(w_in, n_layers, w_out, k, conn, tables, n_classes, k_out, conn_out,
+                           tables_out, fanin_out, order_out);
+    return ok();
 }
 
 size_t bitlogic_fit_quantile_thresholds_workspace_bytes(int32_t n_groups)

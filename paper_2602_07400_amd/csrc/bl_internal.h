@@ -61,15 +61,40 @@ constexpr int kFitMaxGroups = 32;
 hipError_t launch_fit_quantiles(const uint8_t *x, int64_t n, int32_t d, int32_t b,
                                 int32_t n_groups, uint8_t *th, uint64_t *ws, hipStream_t stream);
 
+// Nodes per entry of a specialized layer's fan-in array.
+constexpr int kSpecPass = 32;
+
 // Slab-layout LUT layer over n_slabs slabs (bitlogic_forward's intermediates).
+// fanin: NULL, or a specialized layer's evaluated fan-in per kSpecPass nodes
+// (device; connections [w_out][k] then use the first fan-in slots).
 hipError_t launch_lut_layer_slab(const uint64_t *in, int32_t w_in, int64_t n_slabs,
                                  const int32_t *conn, const uint64_t *tables, int32_t w_out,
-                                 int32_t k, uint64_t *out, hipStream_t stream);
+                                 int32_t k, uint64_t *out, hipStream_t stream,
+                                 const uint8_t *fanin = nullptr);
 
 hipError_t launch_lut_layer(const uint64_t *in, int32_t w_in, int64_t n_words,
                             const int32_t *conn, const uint64_t *tables,
                             int32_t w_out, int32_t k, uint64_t *out,
                             hipStream_t stream);
+
+// Table specialization of one node (host): merges tied slots and drops
+// inputs the table ignores; returns the effective fan-in k' and writes the
+// k' remaining connections and the table over them.
+int specialize_node(const int32_t *conn, uint64_t T, int k, int32_t *conn_out, uint64_t *T_out);
+
+// Table specialization of a network (host): every node specialized, each
+// layer's nodes reordered by effective fan-in (within class groups for the
+// last layer, of c classes), the next layer's connections relabelled, and per
+// kSpecPass nodes the largest fan-in, to which the pass's nodes are padded.
+// w[l], k[l]: layer widths and fan-ins; conn/tables: the network (host);
+// outputs per layer: k_out (the largest effective fan-in, at least 1),
+// conn_out [w][k_out], tables_out [w] (over k_out slots), fanin_out
+// [ceil(w / kSpecPass)], order_out [w] (original node at each position; may
+// be NULL).  Connections must be in range (the caller checks).
+void specialize_network(int32_t w_in, int32_t L, const int32_t *w, const int32_t *k,
+                        const int32_t *const *conn, const uint64_t *const *tables, int32_t c,
+                        int32_t *k_out, int32_t *const *conn_out, uint64_t *const *tables_out,
+                        uint8_t *const *fanin_out, int32_t *const *order_out);
 
 // Last LUT layer fused with the GroupSum head (slab layout): writes the head's
 // bit planes instead of the layer's bits.  fused_head_nodes(g, c, n_slabs) is the
@@ -80,7 +105,7 @@ int32_t fused_head_nodes(int32_t g, int32_t c, int64_t n_slabs);
 hipError_t launch_lut_slab_head(const uint64_t *in, int32_t w_in, int64_t n_slabs,
                                 const int32_t *conn, const uint64_t *tables, int32_t w_out,
                                 int32_t k, int32_t c, int64_t W, uint64_t *planes, int32_t P,
-                                hipStream_t stream);
+                                hipStream_t stream, const uint8_t *fanin = nullptr);
 
 struct HeadPlan {
     int32_t splits;        // row splits per class group

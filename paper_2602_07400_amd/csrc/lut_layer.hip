@@ -185,12 +185,9 @@ __device__ __forceinline__ void gather(const uint64_t *src, const int32_t *c, in
     }
 }
 
-template <int K, int R>
-__device__ __forceinline__ void eval_store(uint64_t T, const uint32_t (&xv)[2 * R][K],
-                                           uint64_t *q, bool ok)
+template <int R>
+__device__ __forceinline__ void store_out(const uint32_t (&o)[2 * R], uint64_t *q, bool ok)
 {
-    uint32_t o[2 * R];
-    eval_node<K, R>(T, xv, o);
     if (ok) {
         if constexpr (R == 1) {
             const uint64_t v = (uint64_t)o[1] << 32 | o[0];
@@ -211,15 +208,68 @@ __device__ __forceinline__ void eval_store(uint64_t T, const uint32_t (&xv)[2 * 
     }
 }
 
+template <int K, int R>
+__device__ __forceinline__ void eval_store(uint64_t T, const uint32_t (&xv)[2 * R][K],
+                                           uint64_t *q, bool ok)
+{
+    uint32_t o[2 * R];
+    eval_node<K, R>(T, xv, o);
+    store_out<R>(o, q, ok);
+}
+
+// Specialized layers (table specialization, see specialize.hip): the nodes of
+// a pass share one evaluated fan-in kp <= K, read per pass from the layer's
+// fan-in array (one entry per kSpecPass nodes; a pass spanning several
+// entries takes their maximum).  kp is uniform over the block, so the
+// dispatch below is a scalar branch: the pass gathers kp wires and runs the
+// 2^kp - 1 multiplexer tree; kp = 0 is a constant node (table bit 0).
+template <int KQ, int K, int R>
+__device__ __forceinline__ void spec_eval(int kp, const uint64_t *src, const int32_t *c, int S,
+                                          uint64_t T, uint32_t (&o)[2 * R])
+{
+    if constexpr (KQ == 0) {
+        if (kp == 0) {
+            const uint32_t m = 0u - (uint32_t)(T & 1u);
+#pragma unroll
+            for (int h = 0; h < 2 * R; ++h)
+                o[h] = m;
+            return;
+        }
+    } else {
+        if (kp == KQ) {
+            uint32_t xv[2 * R][KQ];
+            gather<KQ, R>(src, c, S, xv);
+            eval_node<KQ, R>(T, xv, o);
+            return;
+        }
+    }
+    if constexpr (KQ < K)
+        spec_eval<KQ + 1, K, R>(kp, src, c, S, T, o);
+}
+
+// evaluated fan-in of the PN nodes from node n0 (a multiple of kSpecPass)
+template <int PN, int K>
+__device__ __forceinline__ int pass_fanin(const uint8_t *fanin, int32_t n_fanin, int n0)
+{
+    static_assert(PN % kSpecPass == 0, "passes are whole fan-in entries");
+    const int e0 = n0 / kSpecPass;
+    int kp = 0;
+#pragma unroll
+    for (int e = 0; e < PN / kSpecPass; ++e)
+        if (e0 + e < n_fanin)
+            kp = max(kp, (int)fanin[e0 + e]);
+    return __builtin_amdgcn_readfirstlane(min(kp, K));
+}
+
 #ifndef BL_LUT_MINWAVES
 #define BL_LUT_MINWAVES 1
 #endif
 
-template <int K, int S, int LPN, int NB>
+template <int K, int S, int LPN, int NB, bool SPEC>
 __global__ __launch_bounds__(kThreads, BL_LUT_MINWAVES) void k_lut_slab(
     const uint64_t *__restrict__ in, int32_t w_in, const int32_t *__restrict__ conn,
     const uint64_t *__restrict__ tables, int32_t w_out, uint64_t *__restrict__ out,
-    int32_t n_nblk, int32_t n_slabs)
+    int32_t n_nblk, int32_t n_slabs, const uint8_t *__restrict__ fanin)
 {
     constexpr int R = S / LPN;                         // words per lane
     constexpr int kPassNodes = kThreads / LPN;
@@ -252,9 +302,17 @@ __global__ __launch_bounds__(kThreads, BL_LUT_MINWAVES) void k_lut_slab(
 #pragma unroll 1
     for (int pass = 0; pass < npass; ++pass) {
         const int jl = pass * kPassNodes + lnode;
-        uint32_t xv[2 * R][K];
-        gather<K, R>(src, &s_conn[jl * K], S, xv);
-        eval_store<K, R>(s_tab[jl], xv, dst + (int64_t)jl * S, jl < nodes);
+        if constexpr (SPEC) {
+            const int kp = pass_fanin<kPassNodes, K>(fanin, (w_out + kSpecPass - 1) / kSpecPass,
+                                                     node0 + pass * kPassNodes);
+            uint32_t o[2 * R];
+            spec_eval<0, K, R>(kp, src, &s_conn[jl * K], S, s_tab[jl], o);
+            store_out<R>(o, dst + (int64_t)jl * S, jl < nodes);
+        } else {
+            uint32_t xv[2 * R][K];
+            gather<K, R>(src, &s_conn[jl * K], S, xv);
+            eval_store<K, R>(s_tab[jl], xv, dst + (int64_t)jl * S, jl < nodes);
+        }
     }
 }
 
@@ -269,29 +327,35 @@ constexpr int64_t kSlabSmallBlocks = 2048;
 template <int K, int NB>
 hipError_t launch_slab_kn(const uint64_t *in, int32_t w_in, int64_t n_slabs,
                           const int32_t *conn, const uint64_t *tables, int32_t w_out,
-                          uint64_t *out, hipStream_t stream)
+                          uint64_t *out, const uint8_t *fanin, hipStream_t stream)
 {
     const int32_t n_nblk = (w_out + NB - 1) / NB;
     const int64_t slabs_pad = (n_slabs + kXcds - 1) / kXcds * kXcds;
     const int64_t blocks = slabs_pad * n_nblk;
     if (blocks > 0x7fffffff)
         return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((k_lut_slab<K, kSlabWords, kSlabLanes, NB>), dim3((unsigned)blocks),
-                       dim3(kThreads), 0, stream, in, w_in, conn, tables, w_out, out, n_nblk,
-                       (int32_t)n_slabs);
+    if (fanin)
+        hipLaunchKernelGGL((k_lut_slab<K, kSlabWords, kSlabLanes, NB, true>),
+                           dim3((unsigned)blocks), dim3(kThreads), 0, stream, in, w_in, conn,
+                           tables, w_out, out, n_nblk, (int32_t)n_slabs, fanin);
+    else
+        hipLaunchKernelGGL((k_lut_slab<K, kSlabWords, kSlabLanes, NB, false>),
+                           dim3((unsigned)blocks), dim3(kThreads), 0, stream, in, w_in, conn,
+                           tables, w_out, out, n_nblk, (int32_t)n_slabs, fanin);
     return hipGetLastError();
 }
 
 template <int K>
 hipError_t launch_slab_k(const uint64_t *in, int32_t w_in, int64_t n_slabs,
                          const int32_t *conn, const uint64_t *tables, int32_t w_out,
-                         uint64_t *out, hipStream_t stream)
+                         uint64_t *out, const uint8_t *fanin, hipStream_t stream)
 {
     const int64_t big = n_slabs * ((w_out + kSlabNB - 1) / kSlabNB);
     if (big < kSlabSmallBlocks)
         return launch_slab_kn<K, kSlabNBSmall>(in, w_in, n_slabs, conn, tables, w_out, out,
-                                                stream);
-    return launch_slab_kn<K, kSlabNB>(in, w_in, n_slabs, conn, tables, w_out, out, stream);
+                                                fanin, stream);
+    return launch_slab_kn<K, kSlabNB>(in, w_in, n_slabs, conn, tables, w_out, out, fanin,
+                                      stream);
 }
 
 // ---------------------------------------------------------------------------
@@ -328,11 +392,12 @@ __device__ __forceinline__ void bs_add(uint32_t (&acc)[NP], const uint32_t (&v)[
     }
 }
 
-template <int K, int P>
+template <int K, int P, bool SPEC>
 __global__ __launch_bounds__(kThreads) void k_lut_slab_head(
     const uint64_t *__restrict__ in, int32_t w_in, const int32_t *__restrict__ conn,
     const uint64_t *__restrict__ tables, int32_t g, int32_t nb, int32_t n_nblk,
-    int32_t n_slabs, int64_t W, int32_t c, int32_t splits, uint64_t *__restrict__ planes)
+    int32_t n_slabs, int64_t W, int32_t c, int32_t splits, uint64_t *__restrict__ planes,
+    const uint8_t *__restrict__ fanin)
 {
     static_assert(kSlabWords == 16 && kSlabWords == kHeadLPN * kHeadR, "slab of 16 words");
     static_assert(P >= kHeadCP, "final planes hold the per-lane counters");
@@ -375,10 +440,16 @@ __global__ __launch_bounds__(kThreads) void k_lut_slab_head(
 #pragma unroll 1
     for (int pass = 0; pass < passes; ++pass) {
         const int jl = pass * kHeadPassNodes + lnode;
-        uint32_t xv[2 * kHeadR][K];
-        gather<K, kHeadR>(src, &s_conn[jl * K], kSlabWords, xv);
         uint32_t o[2 * kHeadR];
-        eval_node<K, kHeadR>(s_tab[jl], xv, o);
+        if constexpr (SPEC) {
+            const int kp = pass_fanin<kHeadPassNodes, K>(fanin, (g * c) / kSpecPass,
+                                                         node0 + pass * kHeadPassNodes);
+            spec_eval<0, K, kHeadR>(kp, src, &s_conn[jl * K], kSlabWords, s_tab[jl], o);
+        } else {
+            uint32_t xv[2 * kHeadR][K];
+            gather<K, kHeadR>(src, &s_conn[jl * K], kSlabWords, xv);
+            eval_node<K, kHeadR>(s_tab[jl], xv, o);
+        }
 #pragma unroll
         for (int h = 0; h < 2 * kHeadR; ++h) {
             uint32_t carry = o[h];
@@ -450,16 +521,21 @@ template <int K, int P>
 hipError_t launch_slab_head_kp(const uint64_t *in, int32_t w_in, int64_t n_slabs,
                                const int32_t *conn, const uint64_t *tables, int32_t w_out,
                                int32_t g, int32_t nb, int64_t W, int32_t c, uint64_t *planes,
-                               hipStream_t stream)
+                               const uint8_t *fanin, hipStream_t stream)
 {
     const int32_t n_nblk = w_out / nb;
     const int64_t slabs_pad = (n_slabs + kXcds - 1) / kXcds * kXcds;
     const int64_t blocks = slabs_pad * n_nblk;
     if (blocks > 0x7fffffff)
         return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((k_lut_slab_head<K, P>), dim3((unsigned)blocks), dim3(kThreads), 0,
-                       stream, in, w_in, conn, tables, g, nb, n_nblk, (int32_t)n_slabs, W, c,
-                       g / nb, planes);
+    if (fanin)
+        hipLaunchKernelGGL((k_lut_slab_head<K, P, true>), dim3((unsigned)blocks), dim3(kThreads),
+                           0, stream, in, w_in, conn, tables, g, nb, n_nblk, (int32_t)n_slabs, W,
+                           c, g / nb, planes, fanin);
+    else
+        hipLaunchKernelGGL((k_lut_slab_head<K, P, false>), dim3((unsigned)blocks),
+                           dim3(kThreads), 0, stream, in, w_in, conn, tables, g, nb, n_nblk,
+                           (int32_t)n_slabs, W, c, g / nb, planes, fanin);
     return hipGetLastError();
 }
 
@@ -467,14 +543,14 @@ template <int K>
 hipError_t launch_slab_head_k(const uint64_t *in, int32_t w_in, int64_t n_slabs,
                               const int32_t *conn, const uint64_t *tables, int32_t w_out,
                               int32_t g, int32_t nb, int32_t P, int64_t W, int32_t c,
-                              uint64_t *planes, hipStream_t stream)
+                              uint64_t *planes, const uint8_t *fanin, hipStream_t stream)
 {
     switch (P) {
-    case 6: return launch_slab_head_kp<K, 6>(in, w_in, n_slabs, conn, tables, w_out, g, nb, W, c, planes, stream);
-    case 7: return launch_slab_head_kp<K, 7>(in, w_in, n_slabs, conn, tables, w_out, g, nb, W, c, planes, stream);
-    case 8: return launch_slab_head_kp<K, 8>(in, w_in, n_slabs, conn, tables, w_out, g, nb, W, c, planes, stream);
-    case 9: return launch_slab_head_kp<K, 9>(in, w_in, n_slabs, conn, tables, w_out, g, nb, W, c, planes, stream);
-    case 10: return launch_slab_head_kp<K, 10>(in, w_in, n_slabs, conn, tables, w_out, g, nb, W, c, planes, stream);
+    case 6: return launch_slab_head_kp<K, 6>(in, w_in, n_slabs, conn, tables, w_out, g, nb, W, c, planes, fanin, stream);
+    case 7: return launch_slab_head_kp<K, 7>(in, w_in, n_slabs, conn, tables, w_out, g, nb, W, c, planes, fanin, stream);
+    case 8: return launch_slab_head_kp<K, 8>(in, w_in, n_slabs, conn, tables, w_out, g, nb, W, c, planes, fanin, stream);
+    case 9: return launch_slab_head_kp<K, 9>(in, w_in, n_slabs, conn, tables, w_out, g, nb, W, c, planes, fanin, stream);
+    case 10: return launch_slab_head_kp<K, 10>(in, w_in, n_slabs, conn, tables, w_out, g, nb, W, c, planes, fanin, stream);
     default: return hipErrorInvalidValue;
     }
 }
@@ -525,15 +601,16 @@ hipError_t launch_k(const uint64_t *in, int64_t W, const int32_t *conn,
 
 hipError_t launch_lut_layer_slab(const uint64_t *in, int32_t w_in, int64_t n_slabs,
                                  const int32_t *conn, const uint64_t *tables, int32_t w_out,
-                                 int32_t k, uint64_t *out, hipStream_t stream)
+                                 int32_t k, uint64_t *out, hipStream_t stream,
+                                 const uint8_t *fanin)
 {
     switch (k) {
-    case 1: return launch_slab_k<1>(in, w_in, n_slabs, conn, tables, w_out, out, stream);
-    case 2: return launch_slab_k<2>(in, w_in, n_slabs, conn, tables, w_out, out, stream);
-    case 3: return launch_slab_k<3>(in, w_in, n_slabs, conn, tables, w_out, out, stream);
-    case 4: return launch_slab_k<4>(in, w_in, n_slabs, conn, tables, w_out, out, stream);
-    case 5: return launch_slab_k<5>(in, w_in, n_slabs, conn, tables, w_out, out, stream);
-    case 6: return launch_slab_k<6>(in, w_in, n_slabs, conn, tables, w_out, out, stream);
+    case 1: return launch_slab_k<1>(in, w_in, n_slabs, conn, tables, w_out, out, fanin, stream);
+    case 2: return launch_slab_k<2>(in, w_in, n_slabs, conn, tables, w_out, out, fanin, stream);
+    case 3: return launch_slab_k<3>(in, w_in, n_slabs, conn, tables, w_out, out, fanin, stream);
+    case 4: return launch_slab_k<4>(in, w_in, n_slabs, conn, tables, w_out, out, fanin, stream);
+    case 5: return launch_slab_k<5>(in, w_in, n_slabs, conn, tables, w_out, out, fanin, stream);
+    case 6: return launch_slab_k<6>(in, w_in, n_slabs, conn, tables, w_out, out, fanin, stream);
     default: return hipErrorInvalidValue;
     }
 }
@@ -557,19 +634,19 @@ int32_t fused_head_nodes(int32_t g, int32_t c, int64_t n_slabs)
 hipError_t launch_lut_slab_head(const uint64_t *in, int32_t w_in, int64_t n_slabs,
                                 const int32_t *conn, const uint64_t *tables, int32_t w_out,
                                 int32_t k, int32_t c, int64_t W, uint64_t *planes, int32_t P,
-                                hipStream_t stream)
+                                hipStream_t stream, const uint8_t *fanin)
 {
     const int32_t g = w_out / c;
     const int32_t nb = fused_head_nodes(g, c, n_slabs);
     if (nb == 0)
         return hipErrorInvalidValue;
     switch (k) {
-    case 1: return launch_slab_head_k<1>(in, w_in, n_slabs, conn, tables, w_out, g, nb, P, W, c, planes, stream);
-    case 2: return launch_slab_head_k<2>(in, w_in, n_slabs, conn, tables, w_out, g, nb, P, W, c, planes, stream);
-    case 3: return launch_slab_head_k<3>(in, w_in, n_slabs, conn, tables, w_out, g, nb, P, W, c, planes, stream);
-    case 4: return launch_slab_head_k<4>(in, w_in, n_slabs, conn, tables, w_out, g, nb, P, W, c, planes, stream);
-    case 5: return launch_slab_head_k<5>(in, w_in, n_slabs, conn, tables, w_out, g, nb, P, W, c, planes, stream);
-    case 6: return launch_slab_head_k<6>(in, w_in, n_slabs, conn, tables, w_out, g, nb, P, W, c, planes, stream);
+    case 1: return launch_slab_head_k<1>(in, w_in, n_slabs, conn, tables, w_out, g, nb, P, W, c, planes, fanin, stream);
+    case 2: return launch_slab_head_k<2>(in, w_in, n_slabs, conn, tables, w_out, g, nb, P, W, c, planes, fanin, stream);
+    case 3: return launch_slab_head_k<3>(in, w_in, n_slabs, conn, tables, w_out, g, nb, P, W, c, planes, fanin, stream);
+    case 4: return launch_slab_head_k<4>(in, w_in, n_slabs, conn, tables, w_out, g, nb, P, W, c, planes, fanin, stream);
+    case 5: return launch_slab_head_k<5>(in, w_in, n_slabs, conn, tables, w_out, g, nb, P, W, c, planes, fanin, stream);
+    case 6: return launch_slab_head_k<6>(in, w_in, n_slabs, conn, tables, w_out, g, nb, P, W, c, planes, fanin, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -21,7 +21,13 @@ Readings of the paper used here:
 * fixed random routing drawn once per layer, each node's k inputs distinct
   (Sec. 3 "Connectivity"; App. A "Initialization");
 * random truth tables, 2^k entries in the low bits of a uint64 (bits >= 2^k
-  are zero).
+  are zero);
+* collapsed routing (the "collapsed" configurations only): each node's k
+  slots are drawn with repetition from a pool of 3 distinct wires of its own,
+  so every node reads at most 3 distinct wires.  This stands in for the
+  mode-collapsed full-pool router of Sec. 5 "Connectivity", where many slots
+  converge on the same wires and a node's table reduces to a function of at
+  most 3 effective inputs; it is the workload of table specialization.
 """
 from __future__ import annotations
 
@@ -35,7 +41,7 @@ import zlib
 import numpy as np
 
 __all__ = ["Config", "CONFIGS", "CONFIG_ORDER", "Workload", "make_workload", "draw_connectivity",
-           "draw_tables", "uniform_thresholds"]
+           "draw_pooled_connectivity", "draw_tables", "uniform_thresholds"]
 
 
 @dataclass(frozen=True)
@@ -52,6 +58,7 @@ class Config:
     channels: int = 1      # colour channels (quantile fit is per channel)
     description: str = ""
     family: str = ""       # configs of one family share their pixel and threshold draws
+    pool: int = 0          # 0: distinct random routing; p > 0: collapsed routing from p wires
 
     @property
     def seed_key(self) -> str:
@@ -103,6 +110,13 @@ CONFIGS["paper_mnist_w4000"] = Config(
     "paper_mnist_w4000", 1024, 784, 4, "quantile", (4000, 4000), 4, 10, "uniform", 1,
     "the paper's deployed MNIST network shape: 784 features, 4 quantile thresholds "
     "(3136 wires), 2 x 4000 nodes, k=4, 10 classes x 400; batch 1024")
+
+# Collapsed routing on the CIFAR-100 wide shape (every node reads at most 3
+# distinct wires); the workload table specialization is measured on.
+CONFIGS["c4_collapsed"] = Config(
+    "c4_collapsed", 1 << 18, 3072, 7, "uniform", (64000, 64000), 6, 100, "uniform", 3,
+    "CIFAR-100 wide shape with collapsed routing: each node's 6 slots drawn from 3 "
+    "wires of its own", "c4_cifar100_wide", 3)
 
 #: the order the configurations are listed in
 CONFIG_ORDER = ["c1_mnist_tiny", "c2_fmnist", "c3_cifar10", "c4_cifar100_wide",
@@ -215,6 +229,17 @@ def draw_connectivity(rng: np.random.Generator, w: int, k: int, w_in: int) -> np
     return conn.astype(np.int32)
 
 
+def draw_pooled_connectivity(rng: np.random.Generator, w: int, k: int, w_in: int,
+                             pool: int) -> np.ndarray:
+    """Each node draws `pool` distinct wires of [0, w_in), then its k slots
+    uniformly with repetition from them."""
+    if pool > w_in:
+        raise ValueError("pool larger than the layer input")
+    base = draw_connectivity(rng, w, pool, w_in)
+    pick = rng.integers(0, pool, size=(w, k))
+    return np.take_along_axis(base, pick, axis=1).astype(np.int32)
+
+
 def draw_tables(rng: np.random.Generator, w: int, k: int) -> np.ndarray:
     """Random 2^k-entry truth tables, entry a = bit a; unused high bits zero."""
     t = rng.integers(0, np.iinfo(np.uint64).max, size=w, dtype=np.uint64, endpoint=True)
@@ -253,7 +278,10 @@ def make_workload(name_or_cfg, seed: int = 0, n: Optional[int] = None) -> Worklo
     layers = []
     w_in = cfg.wires
     for l, w in enumerate(cfg.widths):
-        conn = draw_connectivity(rngs[_S_LAYERS + 2 * l], w, cfg.k, w_in)
+        if cfg.pool:
+            conn = draw_pooled_connectivity(rngs[_S_LAYERS + 2 * l], w, cfg.k, w_in, cfg.pool)
+        else:
+            conn = draw_connectivity(rngs[_S_LAYERS + 2 * l], w, cfg.k, w_in)
         tables = draw_tables(rngs[_S_LAYERS + 2 * l + 1], w, cfg.k)
         layers.append((conn, tables))
         w_in = w

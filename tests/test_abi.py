@@ -314,3 +314,28 @@ def test_whole_network_plan(lib, monkeypatch):
     assert info.fused_network == 0
     assert lib.bitlogic_network_plan(ctypes.byref(_net(p, head=1, w=FAKE)), 4096, ref) == OK
     assert info.fused_network == 0
+
+
+
+def test_pass_fanin_plan(lib, monkeypatch):
+    # a specialized network keeps the fused head and the workspace; the
+    # whole-network kernel is not used for it
+    p, keep = _layers([(1280, 6), (1280, 6)])     # g = 128 per class: fused head
+    info = bl._ForwardInfo()
+    ref = ctypes.byref(info)
+    assert lib.bitlogic_network_plan(ctypes.byref(_net(p)), 4096, ref) == OK
+    plain_ws, plain_fused = info.workspace_bytes, info.fused_head
+    assert plain_fused == 1
+    arr = (ctypes.c_void_p * 2)(FAKE, FAKE)
+    net = _net(p)
+    net.pass_fanin = ctypes.cast(arr, ctypes.c_void_p)
+    assert lib.bitlogic_network_plan(ctypes.byref(net), 4096, ref) == OK
+    assert info.fused_head == 1 and info.workspace_bytes == plain_ws
+    monkeypatch.setenv("BITLOGIC_FUSED_NETWORK", "1")
+    pc, keepc = _layers([(1000, 6), (1000, 6)])
+    net = _net(pc)
+    assert lib.bitlogic_network_plan(ctypes.byref(net), 4096, ref) == OK
+    assert info.fused_network == 1
+    net.pass_fanin = ctypes.cast(arr, ctypes.c_void_p)
+    assert lib.bitlogic_network_plan(ctypes.byref(net), 4096, ref) == OK
+    assert info.fused_network == 0

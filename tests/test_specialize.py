@@ -1,0 +1,185 @@
+"""Table specialization (bitlogic_specialize_layer, host code) against brute force.
+
+A specialized node must compute the same function of the layer's wires as
+the original node: every assignment of 0/1 to the node's distinct wires is
+tried, the original table is read at the address its k slots form and the
+specialized table at the address its k_eff remaining slots form.  The
+specialized node must also be minimal: its remaining wires are distinct and
+the function depends on each of them.  Hand-derived cases follow the paper's
+tied-input remark (Sec. 5 "Connectivity": a 16-entry table whose slots tie
+to the same wire reduces to a function of at most 3 inputs).
+
+Host-only: the entry point makes no HIP call, so these run without a GPU.
+"""
+import numpy as np
+import pytest
+
+from paper_2602_07400_amd import bitlogic as bl
+
+
+def _lib_or_skip():
+    try:
+        return bl.load_library()
+    except RuntimeError as e:                         # library not built
+        pytest.skip(str(e))
+
+
+def _bit(T, a):
+    return (int(T) >> int(a)) & 1
+
+
+def _check_node(conn, T, k_eff, conn_eff, T_eff):
+    wires = sorted(set(int(c) for c in conn))
+    rem = [int(c) for c in conn_eff[:k_eff]]
+    assert len(set(rem)) == k_eff, "remaining slots must read distinct wires"
+    assert set(rem) <= set(wires)
+    assert all(int(c) == 0 for c in conn_eff[k_eff:])
+    k_eff = int(k_eff)
+    assert k_eff == 6 or int(T_eff) >> (1 << k_eff) == 0
+    for v in range(1 << len(wires)):
+        val = {w: (v >> i) & 1 for i, w in enumerate(wires)}
+        a = sum(val[int(c)] << i for i, c in enumerate(conn))
+        a2 = sum(val[c] << i for i, c in enumerate(rem))
+        assert _bit(T, a) == _bit(T_eff, a2), (conn, hex(int(T)), v)
+    for i in range(k_eff):                            # minimal: every slot matters
+        assert any(_bit(T_eff, a) != _bit(T_eff, a ^ (1 << i)) for a in range(1 << k_eff))
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 6])
+@pytest.mark.parametrize("pool", [1, 2, 3, 8, 1000])
+def test_brute_force(k, pool):
+    _lib_or_skip()
+    rng = np.random.default_rng(100 * k + pool)
+    w, w_in = 300, 1000
+    base = np.stack([rng.choice(w_in, size=pool, replace=False) for _ in range(w)])
+    conn = np.take_along_axis(base, rng.integers(0, pool, size=(w, k)), axis=1).astype(np.int32)
+    tables = rng.integers(0, 2 ** 63, size=w).astype(np.uint64)
+    tables |= rng.integers(0, 2, size=w).astype(np.uint64) << np.uint64(63)
+    # also structured tables: functions of a subset of slots
+    for j in range(0, w, 3):
+        keep = rng.integers(0, 2, size=k)
+        t = 0
+        f = rng.integers(0, 2, size=1 << k)
+        for a in range(1 << k):
+            a_m = a & int(sum(int(b) << i for i, b in enumerate(keep)))
+            t |= int(f[a_m]) << a
+        tables[j] = np.uint64(t)
+    k_eff, conn_eff, t_eff = bl.bitlogic_specialize_layer(conn, tables, w_in)
+    assert k_eff.min() >= 0 and k_eff.max() <= k
+    for j in range(w):
+        _check_node(conn[j], tables[j], k_eff[j], conn_eff[j], t_eff[j])
+
+
+def test_hand_derived():
+    _lib_or_skip()
+    conn = np.array([
+        [5, 5, 7, 9],        # AND4 with slots 0, 1 tied -> AND(x5, x7, x9)
+        [5, 5, 7, 9],        # parity: x5 ^ x5 ^ x7 ^ x9 = x7 ^ x9
+        [1, 2, 3, 4],        # pass-through of slot 3
+        [1, 2, 3, 4],        # constant 1
+        [3, 2, 3, 2],        # x3 AND NOT x2 on two tied pairs
+        [8, 8, 8, 8],        # OR4 on one wire -> x8
+    ], dtype=np.int32)
+    # x3 & ~x2 with a = x3 + 2 x2 + 4 x3 + 8 x2: reachable a in {0, 5, 10, 15}
+    t_andnot = 1 << 5
+    tables = np.array([0x8000, 0x6996, 0xFF00, 0xFFFF, t_andnot, 0xFFFE], dtype=np.uint64)
+    k_eff, conn_eff, t_eff = bl.bitlogic_specialize_layer(conn, tables, 10)
+    assert k_eff.tolist() == [3, 2, 1, 0, 2, 1]
+    assert conn_eff[0, :3].tolist() == [5, 7, 9] and int(t_eff[0]) == 0x80
+    assert conn_eff[1, :2].tolist() == [7, 9] and int(t_eff[1]) == 0b0110
+    assert conn_eff[2, :1].tolist() == [4] and int(t_eff[2]) == 0b10
+    assert int(t_eff[3]) == 1
+    assert conn_eff[4, :2].tolist() == [3, 2] and int(t_eff[4]) == 0b0010
+    assert conn_eff[5, :1].tolist() == [8] and int(t_eff[5]) == 0b10
+    # every 16-entry table on a node with a tied pair needs at most 3 inputs
+    rng = np.random.default_rng(7)
+    conn = np.tile(np.array([[1, 4, 1, 6]], np.int32), (500, 1))
+    tables = rng.integers(0, 1 << 16, size=500).astype(np.uint64)
+    k_eff, _, _ = bl.bitlogic_specialize_layer(conn, tables, 10)
+    assert k_eff.max() <= 3
+
+
+def test_errors():
+    _lib_or_skip()
+    conn = np.array([[0, 10]], dtype=np.int32)
+    tables = np.array([6], dtype=np.uint64)
+    with pytest.raises(bl.BitlogicError):
+        bl.bitlogic_specialize_layer(conn, tables, 10)
+    with pytest.raises(bl.BitlogicError):
+        bl.bitlogic_specialize_layer(np.array([[-1, 0]], np.int32), tables, 10)
+    k_eff, _, _ = bl.bitlogic_specialize_layer(np.zeros((0, 3), np.int32),
+                                               np.zeros(0, np.uint64), 10)
+    assert k_eff.size == 0
+
+
+def _eval_layer(v, conn, tables, slots):
+    """Bits of one layer, per sample: v uint8 [n][w_in] -> [n][w]; node j
+    reads its first slots[j] connections (address bit i = slot i)."""
+    n = v.shape[0]
+    out = np.zeros((n, conn.shape[0]), np.uint8)
+    for j in range(conn.shape[0]):
+        a = np.zeros(n, np.int64)
+        for i in range(int(slots[j])):
+            a |= v[:, conn[j, i]].astype(np.int64) << i
+        out[:, j] = (np.array([int(tables[j])], dtype=object)[0] >> a.astype(object)) & 1
+    return out
+
+
+def _class_counts(v, c):
+    n, w = v.shape
+    return v.reshape(n, c, w // c).sum(axis=2)
+
+
+@pytest.mark.parametrize("ks,pool,c", [([6, 6], 3, 4), ([4, 2, 5], 2, 3), ([3, 6], 64, 2),
+                                       ([1, 6, 4], 1, 5)])
+def test_network_transform_preserves_scores(ks, pool, c):
+    _lib_or_skip()
+    rng = np.random.default_rng(sum(ks) * 10 + pool)
+    w_in0, n = 40, 300
+    widths = [96, 160, 320][:len(ks) - 1] + [c * 64]
+    layers, w_in = [], w_in0
+    for w, k in zip(widths, ks):
+        p = min(pool, w_in)
+        base = np.stack([rng.choice(w_in, size=p, replace=False) for _ in range(w)])
+        conn = np.take_along_axis(base, rng.integers(0, p, size=(w, k)), axis=1).astype(np.int32)
+        tab = rng.integers(0, 2 ** 63, size=w).astype(np.uint64)
+        if k < 6:
+            tab &= np.uint64((1 << (1 << k)) - 1)
+        tab[::7] = np.uint64(0)                          # constants
+        layers.append((conn, tab))
+        w_in = w
+    spec = bl.bitlogic_specialize_network(layers, w_in0, c)
+    x = rng.integers(0, 2, size=(n, w_in0)).astype(np.uint8)
+    v_ref, v_run, v_full = x, x, x
+    for l, ((conn, tab), (sc, st, fanin, order)) in enumerate(zip(layers, spec)):
+        w, k = conn.shape
+        assert sorted(order.tolist()) == list(range(w))
+        kn = sc.shape[1]                                  # largest effective fan-in
+        assert 1 <= kn <= k and fanin.shape == ((w + 31) // 32,) and fanin.max() <= kn
+        assert kn == max(1, int(fanin.max()))
+        if l == len(layers) - 1:                          # class groups keep their nodes
+            g = w // c
+            assert np.array_equal(order // g, np.arange(w) // g)
+        else:                                             # largest fan-in first
+            assert np.all(np.diff(fanin.astype(int)) <= 0)
+        v_ref = _eval_layer(v_ref, conn, tab, np.full(w, k))
+        v_run = _eval_layer(v_run, sc, st, np.repeat(fanin, 32)[:w])
+        v_full = _eval_layer(v_full, sc, st, np.full(w, kn))
+        # hidden activations are the original ones permuted
+        assert np.array_equal(v_run, v_ref[:, order])
+        assert np.array_equal(v_full, v_run)
+    assert np.array_equal(_class_counts(v_run, c), _class_counts(v_ref, c))
+
+
+def test_network_transform_errors():
+    _lib_or_skip()
+    conn = np.zeros((64, 2), np.int32)
+    tab = np.zeros(64, np.uint64)
+    with pytest.raises(bl.BitlogicError):                 # 64 not a multiple of 5 classes
+        bl.bitlogic_specialize_network([(conn, tab)], 10, 5)
+    bad = conn.copy()
+    bad[3, 1] = 10
+    with pytest.raises(bl.BitlogicError):
+        bl.bitlogic_specialize_network([(bad, tab)], 10, 4)
+    with pytest.raises(bl.BitlogicError):                 # layer 2 reads beyond layer 1's 64
+        bl.bitlogic_specialize_network([(conn, tab), (conn + 64, tab)], 10, 4)

@@ -76,3 +76,15 @@ def test_connectivity_sampler():
         draw_connectivity(rng, 1, 7, 6)
     t = draw_tables(rng, 1000, 2)
     assert t.max() < 16 and len(np.unique(t)) == 16
+
+
+def test_collapsed_routing_reads_at_most_three_wires():
+    from paper_2602_07400_amd.workloads import make_workload
+    wl = make_workload("c4_collapsed", n=64)
+    w_in = wl.config.wires
+    for conn, _ in wl.layers:
+        assert conn.shape[1] == 6 and conn.min() >= 0 and conn.max() < w_in
+        distinct = np.array([len(set(r)) for r in conn[:5000].tolist()])
+        assert distinct.max() <= 3 and distinct.min() >= 1
+        assert (distinct == 3).mean() > 0.5
+        w_in = conn.shape[0]
