@@ -290,25 +290,30 @@ int bitlogic_specialize_layer(const int32_t *conn, const uint64_t *tables, int32
  * evaluating the first kp slots, for any kp from the node's effective fan-in
  * up to k_out[l], gives the node's output.  The result computes the same
  * scores as the original network; its hidden activations are the original
- * ones permuted.
+ * ones permuted.  A layer whose multiplexer count (runs of
+ * BITLOGIC_SPECIALIZE_PASS nodes at their largest fan-in) would fall by less
+ * than the fraction min_gain is left as it is (applied_out[l] = 0: original
+ * nodes, order and tables, connections relabelled only), since the
+ * specialized kernels cost a little more than the plain ones at equal work;
+ * min_gain = 0 specializes every layer.
  *   w_in: encoder wires (n_features * n_bits); per layer l (host arrays of
  *   n_layers pointers): conn[l] [w_out[l]][k[l]], tables[l] [w_out[l]] in;
- *   k_out [n_layers]; conn_out[l] [w_out[l]][k_out[l]] (allocate
- *   w_out[l] * k[l] entries), tables_out[l] [w_out[l]],
- *   fanin_out[l] [ceil(w_out[l] / BITLOGIC_SPECIALIZE_PASS)] out;
- *   order_out: NULL, or per layer [w_out[l]] (the original node at each
+ *   k_out [n_layers], applied_out [n_layers]; conn_out[l]
+ *   [w_out[l]][k_out[l]] (allocate w_out[l] * k[l] entries), tables_out[l]
+ *   [w_out[l]], fanin_out[l] [ceil(w_out[l] / BITLOGIC_SPECIALIZE_PASS)]
+ *   out; order_out: NULL, or per layer [w_out[l]] (the original node at each
  *   position).  The specialized network for bitlogic_network_forward has
  *   layers {conn_out[l], tables_out[l], w_out[l], k_out[l]} and pass_fanin
- *   fanin_out (on the device).
- * Returns BITLOGIC_ERR_SHAPE if a connection is out of range or the last
- * width is not a multiple of n_classes. */
+ *   fanin_out[l] on the device where applied_out[l] is 1, NULL elsewhere.
+ * Returns BITLOGIC_ERR_SHAPE if a connection is out of range, the last width
+ * is not a multiple of n_classes or min_gain is outside [0, 1]. */
 #define BITLOGIC_SPECIALIZE_PASS 32
 int bitlogic_specialize_network(int32_t w_in, const int32_t *const *conn,
                                 const uint64_t *const *tables, const int32_t *w_out,
                                 const int32_t *k, int32_t n_layers, int32_t n_classes,
-                                int32_t *k_out, int32_t *const *conn_out,
-                                uint64_t *const *tables_out, uint8_t *const *fanin_out,
-                                int32_t *const *order_out);
+                                double min_gain, int32_t *k_out, int32_t *applied_out,
+                                int32_t *const *conn_out, uint64_t *const *tables_out,
+                                uint8_t *const *fanin_out, int32_t *const *order_out);
 
 enum { BITLOGIC_ENCODER_THERMOMETER = 0, BITLOGIC_ENCODER_BINARY = 1 };
 enum { BITLOGIC_HEAD_GROUPSUM = 0, BITLOGIC_HEAD_GROUPED_DSP = 1 };
@@ -329,7 +334,8 @@ typedef struct bitlogic_network {
     const int8_t *head_weights;     /* [c][c] int8, GROUPED_DSP only (c <= 128)   */
     const uint8_t *const *pass_fanin;
                                     /* NULL, or a host array of n_layers device
-                                       pointers: a non-NULL entry marks layer l
+                                       pointers (entries may be NULL): a
+                                       non-NULL entry marks layer l
                                        as specialized (bitlogic_specialize_network)
                                        and holds its fan-in per run of
                                        BITLOGIC_SPECIALIZE_PASS nodes: each

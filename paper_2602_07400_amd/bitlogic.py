@@ -104,8 +104,8 @@ def load_library():
         "bitlogic_forward_timed": ([P, i64, i32, P, i32, P, i32, i32, P, P, P, sz, P, P, i32],
                                    ctypes.c_int),
         "bitlogic_specialize_layer": ([P, P, i32, i32, i32, P, P, P], ctypes.c_int),
-        "bitlogic_specialize_network": ([i32, P, P, P, P, i32, i32, P, P, P, P, P],
-                                        ctypes.c_int),
+        "bitlogic_specialize_network": ([i32, P, P, P, P, i32, i32, ctypes.c_double, P, P, P,
+                                         P, P, P], ctypes.c_int),
         "bitlogic_status_string": ([ctypes.c_int], ctypes.c_char_p),
         "bitlogic_last_error": ([], ctypes.c_char_p),
         "bitlogic_version": ([], ctypes.c_int),
@@ -409,12 +409,13 @@ def bitlogic_specialize_layer(conn, tables, w_in: int):
     return k_eff, conn_eff, tables_eff
 
 
-def bitlogic_specialize_network(layers, w_in: int, n_classes: int):
+def bitlogic_specialize_network(layers, w_in: int, n_classes: int, min_gain: float = 0.0):
     """Table specialization of a whole network on the host
     (bitlogic_specialize_network): layers [(conn int32 [w][k], tables uint64
-    [w])] -> [(conn, tables, fanin uint8 [ceil(w / 32)], order int32 [w])] per
-    layer, the nodes reordered by effective fan-in; conn has the layer's
-    largest effective fan-in as its width."""
+    [w])] -> [(conn, tables, fanin uint8 [ceil(w / 32)] or None, order int32
+    [w])] per layer.  A specialized layer has its nodes reordered by effective
+    fan-in and the largest effective fan-in as its width; a layer that would
+    save less than min_gain of its multiplexers is kept (fanin None)."""
     conns = [np.ascontiguousarray(c, dtype=np.int32) for c, _ in layers]
     tabs = [np.ascontiguousarray(t, dtype=np.uint64) for _, t in layers]
     L = len(layers)
@@ -424,16 +425,19 @@ def bitlogic_specialize_network(layers, w_in: int, n_classes: int):
     arr = lambda xs, ty: (ty * L)(*[x.ctypes.data for x in xs])
     P = ctypes.c_void_p
     k_out = (ctypes.c_int32 * L)()
+    applied = (ctypes.c_int32 * L)()
     _check(load_library().bitlogic_specialize_network(
         int(w_in), arr(conns, P), arr(tabs, P),
         (ctypes.c_int32 * L)(*[c.shape[0] for c in conns]),
-        (ctypes.c_int32 * L)(*[c.shape[1] for c in conns]), L, int(n_classes), k_out,
+        (ctypes.c_int32 * L)(*[c.shape[1] for c in conns]), L, int(n_classes),
+        float(min_gain), k_out, applied,
         arr([o[0] for o in outs], P), arr([o[1] for o in outs], P),
         arr([o[2] for o in outs], P), arr([o[3] for o in outs], P)))
     res = []
-    for (c, t, f, o), kn in zip(outs, k_out):
+    for (c, t, f, o), kn, a in zip(outs, k_out, applied):
         w = c.shape[0]
-        res.append((np.ascontiguousarray(c.reshape(-1)[:w * kn].reshape(w, kn)), t, f, o))
+        res.append((np.ascontiguousarray(c.reshape(-1)[:w * kn].reshape(w, kn)), t,
+                    f if a else None, o))
     return res
 
 
@@ -470,7 +474,9 @@ class BitlogicModel:
         n_features and n_bits (thresholds None).  head_weights int8 [c][c]
         selects the quantized head.  specialize=True evaluates the network
         from its specialized tables (bitlogic_specialize_network: tied and
-        ignored inputs removed, nodes ordered by effective fan-in)."""
+        ignored inputs removed, nodes ordered by effective fan-in) wherever a
+        layer saves at least 10% of its multiplexers; a float sets that
+        fraction (0.0: every layer)."""
         if encoder == "thermometer":
             th = np.ascontiguousarray(thresholds, dtype=np.uint8)
             if th.ndim != 2:
@@ -498,16 +504,21 @@ class BitlogicModel:
         if w_in % n_classes != 0:
             raise ValueError("last width must be a multiple of n_classes")
         fanin = hist = order = None
-        if specialize:
-            spec = bitlogic_specialize_network(host_layers, d * b, n_classes)
+        if specialize is not False and specialize is not None:
+            gain = 0.1 if specialize is True else float(specialize)
+            spec = bitlogic_specialize_network(host_layers, d * b, n_classes, gain)
             hist, w_prev = [], d * b
-            for conn, tables in host_layers:
+            for (conn, tables), sp in zip(host_layers, spec):
                 k_eff, _, _ = bitlogic_specialize_layer(conn, tables, w_prev)
-                hist.append(np.bincount(k_eff, minlength=MAX_FANIN + 1))
+                hist.append(None if sp[2] is None else
+                            np.bincount(k_eff, minlength=MAX_FANIN + 1))
                 w_prev = conn.shape[0]
             host_layers = [(c, t) for c, t, _, _ in spec]
-            fanin = [torch.from_numpy(f).to(device) for _, _, f, _ in spec]
+            fanin = [None if f is None else torch.from_numpy(f).to(device)
+                     for _, _, f, _ in spec]
             order = [o for _, _, _, o in spec]
+            if all(f is None for f in fanin):
+                fanin = None
         for conn, tables in host_layers:
             dev_layers.append((torch.from_numpy(conn).to(device),
                                torch.from_numpy(tables.view(np.int64)).to(device)))
@@ -523,7 +534,8 @@ class BitlogicModel:
         if not self.pass_fanin:
             return None, None
         ptrs = (ctypes.c_void_p * len(self.layers))(
-            *[_dev(f, "pass_fanin", (torch.uint8,)) for f in self.pass_fanin])
+            *[None if f is None else _dev(f, "pass_fanin", (torch.uint8,))
+              for f in self.pass_fanin])
         return ctypes.cast(ptrs, ctypes.c_void_p), ptrs
 
     def _net(self):

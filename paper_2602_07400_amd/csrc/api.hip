@@ -609,11 +609,12 @@ int bitlogic_specialize_layer(const int32_t *conn, const uint64_t *tables, int32
 int bitlogic_specialize_network(int32_t w_in, const int32_t *const *conn,
                                 const uint64_t *const *tables, const int32_t *w_out,
                                 const int32_t *k, int32_t n_layers, int32_t n_classes,
-                                int32_t *k_out, int32_t *const *conn_out,
-                                uint64_t *const *tables_out, uint8_t *const *fanin_out,
-                                int32_t *const *order_out)
+                                double min_gain, int32_t *k_out, int32_t *applied_out,
+                                int32_t *const *conn_out, uint64_t *const *tables_out,
+                                uint8_t *const *fanin_out, int32_t *const *order_out)
 {
-    if (!conn || !tables || !w_out || !k || !k_out || !conn_out || !tables_out || !fanin_out)
+    if (!conn || !tables || !w_out || !k || !k_out || !applied_out || !conn_out || !tables_out ||
+        !fanin_out)
         return fail(BITLOGIC_ERR_NULL, "specialize_network: NULL pointer");
     if (n_layers < 1 || w_in <= 0 || n_classes < 1)
         return fail(BITLOGIC_ERR_SHAPE, "specialize_network: need n_layers, w_in, n_classes > 0");
@@ -637,8 +638,10 @@ int bitlogic_specialize_network(int32_t w_in, const int32_t *const *conn,
     if (wi % n_classes != 0)
         return fail(BITLOGIC_ERR_SHAPE, "specialize_network: last width %d not a multiple of %d",
                     wi, n_classes);
-    bl::specialize_network(w_in, n_layers, w_out, k, conn, tables, n_classes, k_out, conn_out,
-                           tables_out, fanin_out, order_out);
+    if (!(min_gain >= 0.0 && min_gain <= 1.0))
+        return fail(BITLOGIC_ERR_SHAPE, "specialize_network: min_gain outside [0, 1]");
+    bl::specialize_network(w_in, n_layers, w_out, k, conn, tables, n_classes, min_gain, k_out,
+                           applied_out, conn_out, tables_out, fanin_out, order_out);
     return ok();
 }
 

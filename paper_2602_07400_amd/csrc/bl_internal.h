@@ -87,13 +87,16 @@ int specialize_node(const int32_t *conn, uint64_t T, int k, int32_t *conn_out, u
 // last layer, of c classes), the next layer's connections relabelled, and per
 // kSpecPass nodes the largest fan-in, to which the pass's nodes are padded.
 // w[l], k[l]: layer widths and fan-ins; conn/tables: the network (host);
-// outputs per layer: k_out (the largest effective fan-in, at least 1),
+// min_gain: the least fraction of multiplexers a layer must save to be
+// specialized; outputs per layer: k_out (the largest effective fan-in, at
+// least 1; k for a layer left as is), applied_out (1 if specialized),
 // conn_out [w][k_out], tables_out [w] (over k_out slots), fanin_out
 // [ceil(w / kSpecPass)], order_out [w] (original node at each position; may
 // be NULL).  Connections must be in range (the caller checks).
 void specialize_network(int32_t w_in, int32_t L, const int32_t *w, const int32_t *k,
                         const int32_t *const *conn, const uint64_t *const *tables, int32_t c,
-                        int32_t *k_out, int32_t *const *conn_out, uint64_t *const *tables_out,
+                        double min_gain, int32_t *k_out, int32_t *applied_out,
+                        int32_t *const *conn_out, uint64_t *const *tables_out,
                         uint8_t *const *fanin_out, int32_t *const *order_out);
 
 // Last LUT layer fused with the GroupSum head (slab layout): writes the head's

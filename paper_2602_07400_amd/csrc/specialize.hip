@@ -30,6 +30,9 @@
 // for a constant node) and its table is extended over all kn slots so that
 // it ignores them, so evaluating any kp' with k' <= kp' <= kn slots gives the
 // node's output (a kernel pass spanning several runs takes their maximum).
+// A layer whose multiplexer count would fall by less than min_gain keeps its
+// nodes, order and tables: the specialized kernels cost a little more than
+// the plain ones at equal work.
 #include <algorithm>
 #include <numeric>
 #include <vector>
@@ -119,7 +122,8 @@ int specialize_node(const int32_t *conn, uint64_t T, int k, int32_t *conn_out, u
 
 void specialize_network(int32_t w_in, int32_t L, const int32_t *w, const int32_t *k,
                         const int32_t *const *conn, const uint64_t *const *tables, int32_t c,
-                        int32_t *k_out, int32_t *const *conn_out, uint64_t *const *tables_out,
+                        double min_gain, int32_t *k_out, int32_t *applied_out,
+                        int32_t *const *conn_out, uint64_t *const *tables_out,
                         uint8_t *const *fanin_out, int32_t *const *order_out)
 {
     (void)w_in;
@@ -137,17 +141,41 @@ void specialize_network(int32_t w_in, int32_t L, const int32_t *w, const int32_t
         for (int32_t s0 = 0; s0 < wl; s0 += seg)
             std::stable_sort(order.begin() + s0, order.begin() + std::min(wl, s0 + seg),
                              [&](int32_t a, int32_t b) { return ke[a] > ke[b]; });
+        const int32_t n_pass = (wl + kSpecPass - 1) / kSpecPass;
+        std::vector<int> run_k(n_pass, 0);
+        double mux_spec = 0;
+        for (int32_t q = 0; q < n_pass; ++q) {
+            const int32_t p0 = q * kSpecPass, p1 = std::min(wl, p0 + kSpecPass);
+            for (int32_t p = p0; p < p1; ++p)
+                run_k[q] = std::max(run_k[q], ke[order[p]]);
+            mux_spec += (double)(p1 - p0) * ((1 << run_k[q]) - 1);
+        }
+        const double mux_orig = (double)wl * ((1 << kl) - 1);
+        if (mux_spec > (1.0 - min_gain) * mux_orig) {
+            // too little to gain: the layer stays as it is (connections
+            // relabelled to the previous layer's order only)
+            applied_out[l] = 0;
+            k_out[l] = kl;
+            for (int64_t q = 0; q < (int64_t)wl * kl; ++q) {
+                const int32_t v = conn[l][q];
+                conn_out[l][q] = pos_prev.empty() ? v : pos_prev[v];
+            }
+            std::copy(tables[l], tables[l] + wl, tables_out[l]);
+            std::fill(fanin_out[l], fanin_out[l] + n_pass, (uint8_t)kl);
+            if (order_out && order_out[l])
+                std::iota(order_out[l], order_out[l] + wl, 0);
+            pos_prev.clear();
+            continue;
+        }
+        applied_out[l] = 1;
         // the specialized layer's fan-in: its largest effective fan-in
         int32_t kn = 1;
         for (int32_t j = 0; j < wl; ++j)
             kn = std::max(kn, ke[j]);
         k_out[l] = kn;
-        const int32_t n_pass = (wl + kSpecPass - 1) / kSpecPass;
         for (int32_t q = 0; q < n_pass; ++q) {
             const int32_t p0 = q * kSpecPass, p1 = std::min(wl, p0 + kSpecPass);
-            int kp = 0;
-            for (int32_t p = p0; p < p1; ++p)
-                kp = std::max(kp, ke[order[p]]);
+            const int kp = run_k[q];
             fanin_out[l][q] = (uint8_t)kp;
             for (int32_t p = p0; p < p1; ++p) {
                 const int32_t j = order[p];

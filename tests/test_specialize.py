@@ -130,9 +130,10 @@ def _class_counts(v, c):
     return v.reshape(n, c, w // c).sum(axis=2)
 
 
-@pytest.mark.parametrize("ks,pool,c", [([6, 6], 3, 4), ([4, 2, 5], 2, 3), ([3, 6], 64, 2),
-                                       ([1, 6, 4], 1, 5)])
-def test_network_transform_preserves_scores(ks, pool, c):
+@pytest.mark.parametrize("ks,pool,c,min_gain", [([6, 6], 3, 4, 0.0), ([4, 2, 5], 2, 3, 0.0),
+                                                ([3, 6], 64, 2, 0.0), ([1, 6, 4], 1, 5, 0.0),
+                                                ([6, 6, 6], 3, 4, 0.1), ([5, 6], 64, 2, 0.1)])
+def test_network_transform_preserves_scores(ks, pool, c, min_gain):
     _lib_or_skip()
     rng = np.random.default_rng(sum(ks) * 10 + pool)
     w_in0, n = 40, 300
@@ -148,22 +149,29 @@ def test_network_transform_preserves_scores(ks, pool, c):
         tab[::7] = np.uint64(0)                          # constants
         layers.append((conn, tab))
         w_in = w
-    spec = bl.bitlogic_specialize_network(layers, w_in0, c)
+    spec = bl.bitlogic_specialize_network(layers, w_in0, c, min_gain)
     x = rng.integers(0, 2, size=(n, w_in0)).astype(np.uint8)
     v_ref, v_run, v_full = x, x, x
     for l, ((conn, tab), (sc, st, fanin, order)) in enumerate(zip(layers, spec)):
         w, k = conn.shape
         assert sorted(order.tolist()) == list(range(w))
         kn = sc.shape[1]                                  # largest effective fan-in
-        assert 1 <= kn <= k and fanin.shape == ((w + 31) // 32,) and fanin.max() <= kn
-        assert kn == max(1, int(fanin.max()))
-        if l == len(layers) - 1:                          # class groups keep their nodes
+        if fanin is None:                                 # kept: original nodes and order
+            assert min_gain > 0 and kn == k and np.array_equal(order, np.arange(w))
+            assert np.array_equal(st, tab)
+        else:
+            assert 1 <= kn <= k and fanin.shape == ((w + 31) // 32,) and fanin.max() <= kn
+            assert kn == max(1, int(fanin.max()))
+        if fanin is None:
+            pass
+        elif l == len(layers) - 1:                        # class groups keep their nodes
             g = w // c
             assert np.array_equal(order // g, np.arange(w) // g)
         else:                                             # largest fan-in first
             assert np.all(np.diff(fanin.astype(int)) <= 0)
         v_ref = _eval_layer(v_ref, conn, tab, np.full(w, k))
-        v_run = _eval_layer(v_run, sc, st, np.repeat(fanin, 32)[:w])
+        v_run = _eval_layer(v_run, sc, st, np.repeat(fanin, 32)[:w] if fanin is not None
+                            else np.full(w, kn))
         v_full = _eval_layer(v_full, sc, st, np.full(w, kn))
         # hidden activations are the original ones permuted
         assert np.array_equal(v_run, v_ref[:, order])
@@ -183,3 +191,22 @@ def test_network_transform_errors():
         bl.bitlogic_specialize_network([(bad, tab)], 10, 4)
     with pytest.raises(bl.BitlogicError):                 # layer 2 reads beyond layer 1's 64
         bl.bitlogic_specialize_network([(conn, tab), (conn + 64, tab)], 10, 4)
+
+
+def test_min_gain_keeps_layers_with_little_to_save():
+    _lib_or_skip()
+    rng = np.random.default_rng(3)
+    w_in, w = 200, 256
+    # distinct routing, random 6-input tables: nothing to gain
+    plain = np.stack([rng.choice(w_in, size=6, replace=False) for _ in range(w)]).astype(np.int32)
+    tab = rng.integers(0, 2 ** 63, size=w).astype(np.uint64)
+    # every slot on one of 2 wires: at most 2 inputs
+    tied = np.take_along_axis(np.stack([rng.choice(w, size=2, replace=False) for _ in range(w)]),
+                              rng.integers(0, 2, size=(w, 6)), axis=1).astype(np.int32)
+    spec = bl.bitlogic_specialize_network([(plain, tab), (tied, tab)], w_in, 4, 0.1)
+    assert spec[0][2] is None and np.array_equal(spec[0][0], plain)
+    assert spec[1][2] is not None and spec[1][0].shape[1] <= 2
+    spec = bl.bitlogic_specialize_network([(plain, tab), (tied, tab)], w_in, 4, 0.0)
+    assert spec[0][2] is not None
+    with pytest.raises(bl.BitlogicError):
+        bl.bitlogic_specialize_network([(plain, tab)], w_in, 4, 1.5)

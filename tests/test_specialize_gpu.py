@@ -87,7 +87,7 @@ def _oracle_dsp(x, th, layers, c, binary_bits, dsp):
 ])
 def test_specialized_forward(case):
     d, b, widths, ks, c, n, pool = case
-    spec = True
+    spec = 0.0                                    # every layer specialized
     rng = np.random.default_rng(n + pool)
     x = rng.integers(0, 256, size=(n, d), dtype=np.uint8)
     th = np.sort(rng.integers(0, 256, size=(d, b)), axis=1).astype(np.uint8)
@@ -96,6 +96,24 @@ def test_specialized_forward(case):
           flush=True)
     m = _check(x, th, layers, c, spec)
     assert [int(h.sum()) for h in m.fanin_histogram] == widths
+    assert all(f is not None for f in m.pass_fanin)
+
+
+def test_gain_threshold_mixes_kept_and_specialized_layers():
+    # layer 1 distinct routing with random tables (kept), layers 2 and 3
+    # collapsed (specialized): the kept layer's connections are unchanged, the
+    # next one reads through the specialized layer's new order
+    rng = np.random.default_rng(11)
+    d, b, c, n = 64, 4, 10, 64 * 16 * 3 + 5
+    x = rng.integers(0, 256, size=(n, d), dtype=np.uint8)
+    th = np.sort(rng.integers(0, 256, size=(d, b)), axis=1).astype(np.uint8)
+    conn0 = np.stack([rng.choice(d * b, size=6, replace=False) for _ in range(2000)])
+    first = [(conn0.astype(np.int32), rng.integers(0, 2 ** 63, size=2000).astype(np.uint64))]
+    rest = _network(rng, 2000, [1500, 1280], [6, 6], 2)
+    layers = first + rest
+    print("[spec-mixed]", flush=True)
+    m = _check(x, th, layers, c, True)
+    assert m.pass_fanin[0] is None and m.pass_fanin[1] is not None
 
 
 @pytest.mark.parametrize("n", [1000, 64 * 33])
@@ -106,17 +124,21 @@ def test_specialized_binary_encoder_and_dsp_head(n):
     layers = _network(rng, d * b, [1200, 1200], [6, 4], 3)
     dsp = rng.integers(-127, 128, size=(c, c)).astype(np.int8)
     print(f"[spec-binary-dsp] n={n}", flush=True)
-    _check(x, None, layers, c, True, binary_bits=b, dsp=dsp)
+    _check(x, None, layers, c, 0.0, binary_bits=b, dsp=dsp)
     th = np.sort(rng.integers(0, 256, size=(d, b)), axis=1).astype(np.uint8)
-    _check(x, th, layers, c, True, dsp=dsp)
+    _check(x, th, layers, c, 0.0, dsp=dsp)
 
 
 def test_specialized_unique_routing_matches_unspecialized():
     # distinct random routing: specialization leaves almost every node at
-    # fan-in k; the result must not change
+    # fan-in k; forced on (0.0) the result must not change, and by default
+    # the layers are kept
     wl = make_workload("c1_mnist_tiny")
     print("[spec-c1]", flush=True)
-    _check(wl.x, wl.thresholds, wl.layers, wl.n_classes, True)
+    _check(wl.x, wl.thresholds, wl.layers, wl.n_classes, 0.0)
+    m = bl.BitlogicModel.from_numpy(wl.thresholds, wl.layers, wl.n_classes, device=DEV,
+                                    specialize=True)
+    assert m.pass_fanin is None
 
 
 def test_collapsed_workload_full_batch_sampled():
@@ -129,3 +151,4 @@ def test_collapsed_workload_full_batch_sampled():
     m = _check(wl.x, wl.thresholds, wl.layers, wl.n_classes, True, sample=idx)
     for h in m.fanin_histogram:
         assert h[4:].sum() == 0                      # at most 3 distinct wires per node
+    assert all(layer[0].shape[1] == 3 for layer in m.layers)
