@@ -369,14 +369,38 @@ hipError_t launch_slab_k(const uint64_t *in, int32_t w_in, int64_t n_slabs,
 // that the head's finish kernel turns into scores and argmax.  The last
 // layer's output tensor is never written or read back.
 //
-// Mapping: slab width 16 words, 8 lanes per node (2 words = 4 half-words
-// each), 32 nodes per pass of the 256-thread block.
-constexpr int kHeadLPN = 8;
-constexpr int kHeadR = 2;
-constexpr int kHeadPassNodes = kThreads / kHeadLPN;   // 32
-constexpr int kHeadCP = 5;                            // counter planes: up to 31 passes
-constexpr int kHeadMaxPasses = 20;                    // nodes per block <= 640
+// Mapping: slab width 16 words.  When the group size is a multiple of 64,
+// 4 lanes share a node (4 words = 8 half-words each, 64 nodes per pass of the
+// 256-thread block, at most 15 passes per block, 4 counter planes): each
+// node's 64 table masks serve 8 half-words, and a C4 class group of 640
+// nodes is one block, so the finish reads one counter per class.  The kernel
+// is held to 128 VGPRs (4 waves per SIMD; at K = 6 the compiler spills 4
+// dwords).  Otherwise 8 lanes share a node (2 words each, 32 nodes per pass,
+// up to 20 passes, 5 counter planes).
+template <int LPN>
+struct HeadCfg;
+#ifndef BL_HEAD4_CP
+#define BL_HEAD4_CP 4
+#endif
+#ifndef BL_HEAD_MINWAVES
+#define BL_HEAD_MINWAVES 4
+#endif
+template <>
+struct HeadCfg<4> {
+    static constexpr int R = 4, PN = kThreads / 4, CP = BL_HEAD4_CP,
+                         MaxPasses = (1 << BL_HEAD4_CP) - 1;
+};
+template <>
+struct HeadCfg<8> {
+    static constexpr int R = 2, PN = kThreads / 8, CP = 5, MaxPasses = 20;
+};
 constexpr int kHeadHalves = 2 * kSlabWords;           // 32 half-words per slab
+
+// lanes per node of the fused head for group size g
+int head_lanes(int32_t g)
+{
+    return g % HeadCfg<4>::PN == 0 ? 4 : 8;
+}
 
 // acc (NP planes) += v (NQ planes), bit-sliced ripple carry
 template <int NP, int NQ>
@@ -392,15 +416,19 @@ __device__ __forceinline__ void bs_add(uint32_t (&acc)[NP], const uint32_t (&v)[
     }
 }
 
-template <int K, int P, bool SPEC>
-__global__ __launch_bounds__(kThreads) void k_lut_slab_head(
+template <int K, int P, bool SPEC, int LPN>
+__global__ __launch_bounds__(kThreads, BL_HEAD_MINWAVES) void k_lut_slab_head(
     const uint64_t *__restrict__ in, int32_t w_in, const int32_t *__restrict__ conn,
     const uint64_t *__restrict__ tables, int32_t g, int32_t nb, int32_t n_nblk,
     int32_t n_slabs, int64_t W, int32_t c, int32_t splits, uint64_t *__restrict__ planes,
     const uint8_t *__restrict__ fanin)
 {
-    static_assert(kSlabWords == 16 && kSlabWords == kHeadLPN * kHeadR, "slab of 16 words");
+    using Cfg = HeadCfg<LPN>;
+    constexpr int kHeadR = Cfg::R, kHeadPassNodes = Cfg::PN, kHeadCP = Cfg::CP;
+    constexpr int kHeadMaxPasses = Cfg::MaxPasses;
+    static_assert(kSlabWords == 16 && kSlabWords == LPN * kHeadR, "slab of 16 words");
     static_assert(P >= kHeadCP, "final planes hold the per-lane counters");
+    static_assert(kHeadPassNodes % 8 == 0, "8 threads per half-word sum the node lanes");
     // connections and tables while the nodes run, then the counter reduction
     constexpr int kStageBytes = kHeadMaxPasses * kHeadPassNodes * (K * 4 + 8);
     constexpr int kRedBytes = kHeadHalves * kHeadPassNodes * kHeadCP * 4;
@@ -427,8 +455,8 @@ __global__ __launch_bounds__(kThreads) void k_lut_slab_head(
         s_tab[q] = tables[node0 + q];
     __syncthreads();
 
-    const int sub = threadIdx.x % kHeadLPN;
-    const int lnode = threadIdx.x / kHeadLPN;
+    const int sub = threadIdx.x % LPN;
+    const int lnode = threadIdx.x / LPN;
     const uint64_t *src = in + (int64_t)slab * w_in * kSlabWords + sub * kHeadR;
 
     uint32_t ctr[2 * kHeadR][kHeadCP];
@@ -472,8 +500,9 @@ __global__ __launch_bounds__(kThreads) void k_lut_slab_head(
             s_red[sub * 2 * kHeadR + h][lnode][p] = ctr[h][p];
     __syncthreads();
 
-    // thread t sums 4 node lanes of half-word t/8; the 8 threads of a
+    // thread t sums PN/8 node lanes of half-word t/8; the 8 threads of a
     // half-word then combine with xor swizzles over lanes 1, 2, 4
+    constexpr int kPerThread = kHeadPassNodes / 8;
     const int hw = threadIdx.x / 8;
     const int part = threadIdx.x % 8;
     uint32_t acc[P];
@@ -481,11 +510,11 @@ __global__ __launch_bounds__(kThreads) void k_lut_slab_head(
     for (int p = 0; p < P; ++p)
         acc[p] = 0;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < kPerThread; ++q) {
         uint32_t v[kHeadCP];
 #pragma unroll
         for (int p = 0; p < kHeadCP; ++p)
-            v[p] = s_red[hw][part * 4 + q][p];
+            v[p] = s_red[hw][part * kPerThread + q][p];
         bs_add<P, kHeadCP>(acc, v);
     }
     {
@@ -517,26 +546,42 @@ __global__ __launch_bounds__(kThreads) void k_lut_slab_head(
     }
 }
 
-template <int K, int P>
-hipError_t launch_slab_head_kp(const uint64_t *in, int32_t w_in, int64_t n_slabs,
-                               const int32_t *conn, const uint64_t *tables, int32_t w_out,
-                               int32_t g, int32_t nb, int64_t W, int32_t c, uint64_t *planes,
-                               const uint8_t *fanin, hipStream_t stream)
+template <int K, int P, int LPN>
+hipError_t launch_slab_head_kpl(const uint64_t *in, int32_t w_in, int64_t n_slabs,
+                                const int32_t *conn, const uint64_t *tables, int32_t w_out,
+                                int32_t g, int32_t nb, int64_t W, int32_t c, uint64_t *planes,
+                                const uint8_t *fanin, hipStream_t stream)
 {
+    if (nb % HeadCfg<LPN>::PN != 0 || nb / HeadCfg<LPN>::PN > HeadCfg<LPN>::MaxPasses ||
+        g % nb != 0)
+        return hipErrorInvalidValue;
     const int32_t n_nblk = w_out / nb;
     const int64_t slabs_pad = (n_slabs + kXcds - 1) / kXcds * kXcds;
     const int64_t blocks = slabs_pad * n_nblk;
     if (blocks > 0x7fffffff)
         return hipErrorInvalidConfiguration;
     if (fanin)
-        hipLaunchKernelGGL((k_lut_slab_head<K, P, true>), dim3((unsigned)blocks), dim3(kThreads),
-                           0, stream, in, w_in, conn, tables, g, nb, n_nblk, (int32_t)n_slabs, W,
-                           c, g / nb, planes, fanin);
+        hipLaunchKernelGGL((k_lut_slab_head<K, P, true, LPN>), dim3((unsigned)blocks),
+                           dim3(kThreads), 0, stream, in, w_in, conn, tables, g, nb, n_nblk,
+                           (int32_t)n_slabs, W, c, g / nb, planes, fanin);
     else
-        hipLaunchKernelGGL((k_lut_slab_head<K, P, false>), dim3((unsigned)blocks),
+        hipLaunchKernelGGL((k_lut_slab_head<K, P, false, LPN>), dim3((unsigned)blocks),
                            dim3(kThreads), 0, stream, in, w_in, conn, tables, g, nb, n_nblk,
                            (int32_t)n_slabs, W, c, g / nb, planes, fanin);
     return hipGetLastError();
+}
+
+template <int K, int P>
+hipError_t launch_slab_head_kp(const uint64_t *in, int32_t w_in, int64_t n_slabs,
+                               const int32_t *conn, const uint64_t *tables, int32_t w_out,
+                               int32_t g, int32_t nb, int64_t W, int32_t c, uint64_t *planes,
+                               const uint8_t *fanin, hipStream_t stream)
+{
+    if (head_lanes(g) == 4)
+        return launch_slab_head_kpl<K, P, 4>(in, w_in, n_slabs, conn, tables, w_out, g, nb, W, c,
+                                             planes, fanin, stream);
+    return launch_slab_head_kpl<K, P, 8>(in, w_in, n_slabs, conn, tables, w_out, g, nb, W, c,
+                                         planes, fanin, stream);
 }
 
 template <int K>
@@ -617,17 +662,21 @@ hipError_t launch_lut_layer_slab(const uint64_t *in, int32_t w_in, int64_t n_sla
 
 int32_t fused_head_nodes(int32_t g, int32_t c, int64_t n_slabs)
 {
-    if (kSlabWords != 16 || g <= 0 || g % kHeadPassNodes != 0)
+    if (kSlabWords != 16 || g <= 0)
         return 0;
-    const int32_t units = g / kHeadPassNodes;
+    const bool four = head_lanes(g) == 4;
+    const int32_t pn = four ? HeadCfg<4>::PN : HeadCfg<8>::PN;
+    if (g % pn != 0)
+        return 0;
+    const int32_t units = g / pn;
     // small batches: fewer passes per block until the launch has
     // kSlabSmallBlocks blocks (n_slabs * c * units / p of them)
-    int max_p = kHeadMaxPasses;
+    int max_p = four ? HeadCfg<4>::MaxPasses : HeadCfg<8>::MaxPasses;
     while (max_p > 1 && n_slabs * c * (int64_t)(units / max_p) < kSlabSmallBlocks)
         --max_p;
     for (int p = max_p; p >= 1; --p)
         if (units % p == 0)
-            return p * kHeadPassNodes;
+            return p * pn;
     return 0;
 }
 
