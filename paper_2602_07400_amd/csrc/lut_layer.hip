@@ -402,6 +402,25 @@ int head_lanes(int32_t g)
     return g % HeadCfg<4>::PN == 0 ? 4 : 8;
 }
 
+// Bit-sliced counter ctr (CP planes) += one bit per lane of o, ripple carry:
+// 2 ops per plane, 1 for the top plane.  Each plane is updated in place (a
+// tied asm operand), so the counters keep their registers from one pass to
+// the next instead of being rotated by moves at the loop edge.
+template <int CP>
+__device__ __forceinline__ void bs_count(uint32_t (&ctr)[CP], uint32_t o)
+{
+    uint32_t carry = o;
+#pragma unroll
+    for (int p = 0; p < CP - 1; ++p) {
+        uint32_t next;
+        asm("v_and_b32 %1, %0, %2\n\tv_xor_b32 %0, %0, %2"
+            : "+v"(ctr[p]), "=&v"(next)
+            : "v"(carry));
+        carry = next;
+    }
+    asm("v_xor_b32 %0, %0, %1" : "+v"(ctr[CP - 1]) : "v"(carry));
+}
+
 // acc (NP planes) += v (NQ planes), bit-sliced ripple carry
 template <int NP, int NQ>
 __device__ __forceinline__ void bs_add(uint32_t (&acc)[NP], const uint32_t (&v)[NQ])
@@ -479,15 +498,8 @@ __global__ __launch_bounds__(kThreads, BL_HEAD_MINWAVES) void k_lut_slab_head(
             eval_node<K, kHeadR>(s_tab[jl], xv, o);
         }
 #pragma unroll
-        for (int h = 0; h < 2 * kHeadR; ++h) {
-            uint32_t carry = o[h];
-#pragma unroll
-            for (int p = 0; p < kHeadCP; ++p) {
-                const uint32_t t = ctr[h][p] & carry;
-                ctr[h][p] ^= carry;
-                carry = t;
-            }
-        }
+        for (int h = 0; h < 2 * kHeadR; ++h)
+            bs_count<kHeadCP>(ctr[h], o[h]);
     }
 
     // lane counters -> LDS (over the staging area), one row of 32 node lanes
