@@ -137,9 +137,8 @@ STAGE_KERNELS = {"encode": "k_encode_t / k_encode_ballot (encoder + bit-pack)",
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (the path shards by samples with no exchange; "
-              f"a multi-GPU run is not part of this build); got --gpus {args.gpus}",
-              file=sys.stderr)
+        print(f"bench.py runs on one GPU only: the path shards by samples with no exchange, and "
+              f"this library has no multi-GPU driver; got --gpus {args.gpus}", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
