@@ -101,9 +101,9 @@ void specialize_network(int32_t w_in, int32_t L, const int32_t *w, const int32_t
 
 // Last LUT layer fused with the GroupSum head (slab layout): writes the head's
 // bit planes instead of the layer's bits.  fused_head_nodes(g, c, n_slabs) is the
-// node count of one block (a multiple of 32 dividing the group size g; fewer
-// passes per block for small batches), or 0 when g does not allow the fused
-// kernel.
+// node count nb of one block (a multiple of 64; a class group of g nodes takes
+// ceil(g / nb) blocks, the last one possibly short; fewer passes per block for
+// small batches), or 0 when the shape does not allow the fused kernel.
 int32_t fused_head_nodes(int32_t g, int32_t c, int64_t n_slabs);
 hipError_t launch_lut_slab_head(const uint64_t *in, int32_t w_in, int64_t n_slabs,
                                 const int32_t *conn, const uint64_t *tables, int32_t w_out,
@@ -117,7 +117,7 @@ struct HeadPlan {
     size_t ws_bytes;       // scratch bytes
 };
 HeadPlan plan_head(int32_t w, int64_t n, int32_t c);
-// Plan of the fused last layer + head: splits = g / nb, planes = bit length of nb.
+// Plan of the fused last layer + head: splits = ceil(g / nb), planes = bit length of nb.
 HeadPlan plan_fused_head(int32_t w, int64_t n, int32_t c, int32_t nb);
 // Finish step only (planes -> scores, argmax).  With dsp_weights (int8
 // [c][c], c <= 128) the quantized head's logits replace the scores.

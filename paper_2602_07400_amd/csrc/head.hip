@@ -578,7 +578,7 @@ HeadPlan plan_fused_head(int32_t w, int64_t n, int32_t c, int32_t nb)
     HeadPlan p{};
     const int64_t W = (n + 63) / 64;
     const int32_t g = w / c;
-    p.splits = g / nb;
+    p.splits = (g + nb - 1) / nb;                // the last block of a group may be short
     p.rows_per_split = nb;
     p.planes = bit_length(nb);
     p.ws_bytes = (size_t)c * p.splits * p.planes * W * sizeof(uint64_t);

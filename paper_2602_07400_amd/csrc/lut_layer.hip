@@ -247,7 +247,8 @@ __device__ __forceinline__ void spec_eval(int kp, const uint64_t *src, const int
         spec_eval<KQ + 1, K, R>(kp, src, c, S, T, o);
 }
 
-// evaluated fan-in of the PN nodes from node n0 (a multiple of kSpecPass)
+// evaluated fan-in of the PN nodes from node n0: the largest entry of the
+// runs of kSpecPass nodes they touch (n0 need not start a run)
 template <int PN, int K>
 __device__ __forceinline__ int pass_fanin(const uint8_t *fanin, int32_t n_fanin, int n0)
 {
@@ -255,8 +256,8 @@ __device__ __forceinline__ int pass_fanin(const uint8_t *fanin, int32_t n_fanin,
     const int e0 = n0 / kSpecPass;
     int kp = 0;
 #pragma unroll
-    for (int e = 0; e < PN / kSpecPass; ++e)
-        if (e0 + e < n_fanin)
+    for (int e = 0; e <= PN / kSpecPass; ++e)
+        if (e0 + e < n_fanin && (e < PN / kSpecPass || n0 % kSpecPass != 0))
             kp = max(kp, (int)fanin[e0 + e]);
     return __builtin_amdgcn_readfirstlane(min(kp, K));
 }
@@ -369,38 +370,28 @@ hipError_t launch_slab_k(const uint64_t *in, int32_t w_in, int64_t n_slabs,
 // that the head's finish kernel turns into scores and argmax.  The last
 // layer's output tensor is never written or read back.
 //
-// Mapping: slab width 16 words.  When the group size is a multiple of 64,
-// 4 lanes share a node (4 words = 8 half-words each, 64 nodes per pass of the
-// 256-thread block, at most 15 passes per block, 4 counter planes): each
-// node's 64 table masks serve 8 half-words, and a C4 class group of 640
+// Mapping: slab width 16 words; 4 lanes share a node (4 words = 8 half-words
+// each, 64 nodes per pass of the 256-thread block, at most 15 passes per
+// block, 4 counter planes), so each node's 64 table masks serve 8 half-words.
+// A class group of g nodes is split into ceil(g / nb) blocks of nb nodes (a
+// multiple of 64); the last block of a group, and its last pass, may be
+// short: its padding nodes get connections 0 and a constant-0 table, so they
+// evaluate to 0 and add nothing to the counters.  A C4 class group of 640
 // nodes is one block, so the finish reads one counter per class.  The kernel
 // is held to 128 VGPRs (4 waves per SIMD; at K = 6 the compiler spills 4
-// dwords).  Otherwise 8 lanes share a node (2 words each, 32 nodes per pass,
-// up to 20 passes, 5 counter planes).
-template <int LPN>
-struct HeadCfg;
-#ifndef BL_HEAD4_CP
-#define BL_HEAD4_CP 4
+// dwords).
+#ifndef BL_HEAD_CP
+#define BL_HEAD_CP 4
 #endif
 #ifndef BL_HEAD_MINWAVES
 #define BL_HEAD_MINWAVES 4
 #endif
-template <>
-struct HeadCfg<4> {
-    static constexpr int R = 4, PN = kThreads / 4, CP = BL_HEAD4_CP,
-                         MaxPasses = (1 << BL_HEAD4_CP) - 1;
-};
-template <>
-struct HeadCfg<8> {
-    static constexpr int R = 2, PN = kThreads / 8, CP = 5, MaxPasses = 20;
-};
-constexpr int kHeadHalves = 2 * kSlabWords;           // 32 half-words per slab
-
-// lanes per node of the fused head for group size g
-int head_lanes(int32_t g)
-{
-    return g % HeadCfg<4>::PN == 0 ? 4 : 8;
-}
+constexpr int kHeadLPN = 4;
+constexpr int kHeadR = kSlabWords / kHeadLPN;
+constexpr int kHeadPassNodes = kThreads / kHeadLPN;          // 64
+constexpr int kHeadCP = BL_HEAD_CP;                          // counter planes
+constexpr int kHeadMaxPasses = (1 << BL_HEAD_CP) - 1;         // passes per block
+constexpr int kHeadHalves = 2 * kSlabWords;                  // 32 half-words per slab
 
 // Bit-sliced counter ctr (CP planes) += one bit per lane of o, ripple carry:
 // 2 ops per plane, 1 for the top plane.  Each plane is updated in place (a
@@ -435,17 +426,14 @@ __device__ __forceinline__ void bs_add(uint32_t (&acc)[NP], const uint32_t (&v)[
     }
 }
 
-template <int K, int P, bool SPEC, int LPN>
+template <int K, int P, bool SPEC>
 __global__ __launch_bounds__(kThreads, BL_HEAD_MINWAVES) void k_lut_slab_head(
     const uint64_t *__restrict__ in, int32_t w_in, const int32_t *__restrict__ conn,
     const uint64_t *__restrict__ tables, int32_t g, int32_t nb, int32_t n_nblk,
     int32_t n_slabs, int64_t W, int32_t c, int32_t splits, uint64_t *__restrict__ planes,
     const uint8_t *__restrict__ fanin)
 {
-    using Cfg = HeadCfg<LPN>;
-    constexpr int kHeadR = Cfg::R, kHeadPassNodes = Cfg::PN, kHeadCP = Cfg::CP;
-    constexpr int kHeadMaxPasses = Cfg::MaxPasses;
-    static_assert(kSlabWords == 16 && kSlabWords == LPN * kHeadR, "slab of 16 words");
+    static_assert(kSlabWords == 16 && kSlabWords == kHeadLPN * kHeadR, "slab of 16 words");
     static_assert(P >= kHeadCP, "final planes hold the per-lane counters");
     static_assert(kHeadPassNodes % 8 == 0, "8 threads per half-word sum the node lanes");
     // connections and tables while the nodes run, then the counter reduction
@@ -463,19 +451,22 @@ __global__ __launch_bounds__(kThreads, BL_HEAD_MINWAVES) void k_lut_slab_head(
     const int nblk = loc % n_nblk;
     if (slab >= n_slabs)
         return;
-    const int node0 = nblk * nb;                 // nb divides g: one class per block
-    const int cls = node0 / g;
-    const int split = (node0 % g) / nb;
-    const int passes = nb / kHeadPassNodes;
+    const int cls = nblk / splits;               // one class per block
+    const int split = nblk % splits;
+    const int nodes = min(nb, g - split * nb);   // the group's last block may be short
+    const int node0 = cls * g + split * nb;
+    const int passes = (nodes + kHeadPassNodes - 1) / kHeadPassNodes;
 
-    for (int q = threadIdx.x; q < nb * K; q += kThreads)
-        s_conn[q] = conn[(int64_t)node0 * K + q];
-    for (int q = threadIdx.x; q < nb; q += kThreads)
-        s_tab[q] = tables[node0 + q];
+    // padding nodes of a short last pass: wire 0 and the constant-0 table
+    const int staged = passes * kHeadPassNodes;
+    for (int q = threadIdx.x; q < staged * K; q += kThreads)
+        s_conn[q] = q < nodes * K ? conn[(int64_t)node0 * K + q] : 0;
+    for (int q = threadIdx.x; q < staged; q += kThreads)
+        s_tab[q] = q < nodes ? tables[node0 + q] : 0;
     __syncthreads();
 
-    const int sub = threadIdx.x % LPN;
-    const int lnode = threadIdx.x / LPN;
+    const int sub = threadIdx.x % kHeadLPN;
+    const int lnode = threadIdx.x / kHeadLPN;
     const uint64_t *src = in + (int64_t)slab * w_in * kSlabWords + sub * kHeadR;
 
     uint32_t ctr[2 * kHeadR][kHeadCP];
@@ -489,7 +480,7 @@ __global__ __launch_bounds__(kThreads, BL_HEAD_MINWAVES) void k_lut_slab_head(
         const int jl = pass * kHeadPassNodes + lnode;
         uint32_t o[2 * kHeadR];
         if constexpr (SPEC) {
-            const int kp = pass_fanin<kHeadPassNodes, K>(fanin, (g * c) / kSpecPass,
+            const int kp = pass_fanin<kHeadPassNodes, K>(fanin, (g * c + kSpecPass - 1) / kSpecPass,
                                                          node0 + pass * kHeadPassNodes);
             spec_eval<0, K, kHeadR>(kp, src, &s_conn[jl * K], kSlabWords, s_tab[jl], o);
         } else {
@@ -558,42 +549,29 @@ __global__ __launch_bounds__(kThreads, BL_HEAD_MINWAVES) void k_lut_slab_head(
     }
 }
 
-template <int K, int P, int LPN>
-hipError_t launch_slab_head_kpl(const uint64_t *in, int32_t w_in, int64_t n_slabs,
-                                const int32_t *conn, const uint64_t *tables, int32_t w_out,
-                                int32_t g, int32_t nb, int64_t W, int32_t c, uint64_t *planes,
-                                const uint8_t *fanin, hipStream_t stream)
-{
-    if (nb % HeadCfg<LPN>::PN != 0 || nb / HeadCfg<LPN>::PN > HeadCfg<LPN>::MaxPasses ||
-        g % nb != 0)
-        return hipErrorInvalidValue;
-    const int32_t n_nblk = w_out / nb;
-    const int64_t slabs_pad = (n_slabs + kXcds - 1) / kXcds * kXcds;
-    const int64_t blocks = slabs_pad * n_nblk;
-    if (blocks > 0x7fffffff)
-        return hipErrorInvalidConfiguration;
-    if (fanin)
-        hipLaunchKernelGGL((k_lut_slab_head<K, P, true, LPN>), dim3((unsigned)blocks),
-                           dim3(kThreads), 0, stream, in, w_in, conn, tables, g, nb, n_nblk,
-                           (int32_t)n_slabs, W, c, g / nb, planes, fanin);
-    else
-        hipLaunchKernelGGL((k_lut_slab_head<K, P, false, LPN>), dim3((unsigned)blocks),
-                           dim3(kThreads), 0, stream, in, w_in, conn, tables, g, nb, n_nblk,
-                           (int32_t)n_slabs, W, c, g / nb, planes, fanin);
-    return hipGetLastError();
-}
-
 template <int K, int P>
 hipError_t launch_slab_head_kp(const uint64_t *in, int32_t w_in, int64_t n_slabs,
                                const int32_t *conn, const uint64_t *tables, int32_t w_out,
                                int32_t g, int32_t nb, int64_t W, int32_t c, uint64_t *planes,
                                const uint8_t *fanin, hipStream_t stream)
 {
-    if (head_lanes(g) == 4)
-        return launch_slab_head_kpl<K, P, 4>(in, w_in, n_slabs, conn, tables, w_out, g, nb, W, c,
-                                             planes, fanin, stream);
-    return launch_slab_head_kpl<K, P, 8>(in, w_in, n_slabs, conn, tables, w_out, g, nb, W, c,
-                                         planes, fanin, stream);
+    if (nb <= 0 || nb % kHeadPassNodes != 0 || nb / kHeadPassNodes > kHeadMaxPasses || g <= 0)
+        return hipErrorInvalidValue;
+    const int32_t splits = (g + nb - 1) / nb;
+    const int64_t n_nblk = (int64_t)c * splits;
+    const int64_t slabs_pad = (n_slabs + kXcds - 1) / kXcds * kXcds;
+    const int64_t blocks = slabs_pad * n_nblk;
+    if (blocks > 0x7fffffff)
+        return hipErrorInvalidConfiguration;
+    if (fanin)
+        hipLaunchKernelGGL((k_lut_slab_head<K, P, true>), dim3((unsigned)blocks), dim3(kThreads),
+                           0, stream, in, w_in, conn, tables, g, nb, (int32_t)n_nblk,
+                           (int32_t)n_slabs, W, c, splits, planes, fanin);
+    else
+        hipLaunchKernelGGL((k_lut_slab_head<K, P, false>), dim3((unsigned)blocks),
+                           dim3(kThreads), 0, stream, in, w_in, conn, tables, g, nb,
+                           (int32_t)n_nblk, (int32_t)n_slabs, W, c, splits, planes, fanin);
+    return hipGetLastError();
 }
 
 template <int K>
@@ -674,22 +652,23 @@ hipError_t launch_lut_layer_slab(const uint64_t *in, int32_t w_in, int64_t n_sla
 
 int32_t fused_head_nodes(int32_t g, int32_t c, int64_t n_slabs)
 {
-    if (kSlabWords != 16 || g <= 0)
+    if (kSlabWords != 16 || g <= 0 || c <= 0)
         return 0;
-    const bool four = head_lanes(g) == 4;
-    const int32_t pn = four ? HeadCfg<4>::PN : HeadCfg<8>::PN;
-    if (g % pn != 0)
-        return 0;
-    const int32_t units = g / pn;
+    const int32_t units = (g + kHeadPassNodes - 1) / kHeadPassNodes;
     // small batches: fewer passes per block until the launch has
-    // kSlabSmallBlocks blocks (n_slabs * c * units / p of them)
-    int max_p = four ? HeadCfg<4>::MaxPasses : HeadCfg<8>::MaxPasses;
-    while (max_p > 1 && n_slabs * c * (int64_t)(units / max_p) < kSlabSmallBlocks)
+    // kSlabSmallBlocks blocks (n_slabs * c * ceil(units / p) of them)
+    int max_p = kHeadMaxPasses;
+    while (max_p > 1 &&
+           n_slabs * c * (int64_t)((units + max_p - 1) / max_p) < kSlabSmallBlocks)
         --max_p;
-    for (int p = max_p; p >= 1; --p)
+    // whole blocks of equal size when a divisor of the passes allows it (it
+    // measured faster than fewer, longer blocks: C5's 100 passes as 10 x 10
+    // against 6 x 15 + 10), else the fewest blocks with balanced passes
+    for (int p = max_p; 2 * p >= max_p; --p)
         if (units % p == 0)
-            return p * pn;
-    return 0;
+            return p * kHeadPassNodes;
+    const int32_t splits = (units + max_p - 1) / max_p;
+    return (units + splits - 1) / splits * kHeadPassNodes;
 }
 
 hipError_t launch_lut_slab_head(const uint64_t *in, int32_t w_in, int64_t n_slabs,

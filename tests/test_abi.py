@@ -108,14 +108,23 @@ def _layers(specs):
     return ctypes.cast(arr, ctypes.c_void_p), arr
 
 
-def test_forward_workspace_formula(lib):
+def test_forward_workspace_formula(lib, monkeypatch):
     p, keep = _layers([(1000, 6), (1000, 6)])
     n, d, b, c = 4096, 784, 1, 10
-    need = lib.bitlogic_forward_workspace_bytes(n, d, b, p, 2, c)
     W = 64
     rnd = lambda v: (v + 255) // 256 * 256
+    # fused last layer + head: layer 2 is not stored; counter planes of two
+    # one-pass blocks per class (a batch this small takes the most blocks:
+    # 100 nodes -> 64 + 36, 7 planes each)
+    monkeypatch.delenv("BITLOGIC_UNFUSED_HEAD", raising=False)
+    need = lib.bitlogic_forward_workspace_bytes(n, d, b, p, 2, c)
+    assert need == rnd(d * b * W * 8) + rnd(1000 * W * 8) + rnd(c * 2 * 7 * W * 8)
+    # separate head: both layers stored, plus the head's own workspace
+    monkeypatch.setenv("BITLOGIC_UNFUSED_HEAD", "1")
+    need = lib.bitlogic_forward_workspace_bytes(n, d, b, p, 2, c)
     head = lib.bitlogic_groupsum_head_workspace_bytes(1000, n, c)
     assert need == rnd(d * b * W * 8) + 2 * rnd(1000 * W * 8) + rnd(head)
+    monkeypatch.delenv("BITLOGIC_UNFUSED_HEAD")
     # bad shapes give 0
     assert lib.bitlogic_forward_workspace_bytes(n, d, b, p, 2, 7) == 0
     assert lib.bitlogic_forward_workspace_bytes(n, d, b, p, 0, c) == 0
@@ -172,21 +181,35 @@ def test_forward_plan(lib, monkeypatch):
     monkeypatch.delenv("BITLOGIC_UNFUSED_HEAD", raising=False)
     info = bl._ForwardInfo()
     ref = ctypes.byref(info)
-    # group size 100 is not a multiple of 32: separate head kernels
+    # group size 100: fused; at 4096 samples one-pass blocks (64 + 36 nodes);
+    # at 2^20 samples one block of two passes (the second one short)
     p, keep = _layers([(1000, 6), (1000, 6)])
     assert lib.bitlogic_forward_plan(4096, 784, 1, p, 2, 10, ref) == OK
     assert info.workspace_bytes == lib.bitlogic_forward_workspace_bytes(4096, 784, 1, p, 2, 10)
-    assert info.fused_head == 0 and info.slab_words >= 1
-    assert info.head_splits >= 1 and info.head_planes >= 1
-    # group size 640: last layer and head fused; planes hold counts up to the block size
+    assert info.fused_head == 1 and info.slab_words >= 1
+    assert info.head_splits == 2 and info.head_planes == 7          # counts up to 64
+    assert lib.bitlogic_forward_plan(1 << 20, 784, 1, p, 2, 10, ref) == OK
+    assert info.head_splits == 1 and info.head_planes == 8          # counts up to 128
+    # group size 640: one block of 10 passes per class; planes hold counts up
+    # to the block size
     p4, keep4 = _layers([(64000, 6), (64000, 6)])
     assert lib.bitlogic_forward_plan(1 << 18, 3072, 7, p4, 2, 100, ref) == OK
     assert info.fused_head == 1
     assert info.workspace_bytes == lib.bitlogic_forward_workspace_bytes(1 << 18, 3072, 7, p4, 2,
                                                                         100)
-    nb = 640 // info.head_splits
-    assert nb * info.head_splits == 640 and nb % 32 == 0
-    assert (1 << info.head_planes) > nb
+    assert info.head_splits == 1 and info.head_planes == 10
+    # group size 6400 (C5): 100 passes as 10 equal blocks of 10
+    p5, keep5 = _layers([(64000, 4), (64000, 4)])
+    assert lib.bitlogic_forward_plan(1 << 18, 3072, 3, p5, 2, 10, ref) == OK
+    assert info.head_splits == 10 and info.head_planes == 10
+    # group size 800 (C2): 12.5 passes, one block with a short last pass
+    p2, keep2 = _layers([(8000, 6), (8000, 6)])
+    assert lib.bitlogic_forward_plan(1 << 20, 784, 7, p2, 2, 10, ref) == OK
+    assert info.head_splits == 1 and info.head_planes == 10
+    # group size 1 (one node per class) still fuses: one padded pass
+    p1, keep1 = _layers([(1000, 6), (64, 6)])
+    assert lib.bitlogic_forward_plan(4096, 784, 1, p1, 2, 64, ref) == OK
+    assert info.fused_head == 1 and info.head_splits == 1
     monkeypatch.setenv("BITLOGIC_UNFUSED_HEAD", "1")
     assert lib.bitlogic_forward_plan(1 << 18, 3072, 7, p4, 2, 100, ref) == OK
     assert info.fused_head == 0
