@@ -153,6 +153,9 @@ __global__ __launch_bounds__(kThreads) void k_head_finish(
         for (int ii = wave; ii < cn; ii += kWaves) {
             const int i = c0 + ii;
             int32_t cnt = 0;
+            // four splits' loads in flight together (a class's splits are
+            // otherwise a chain of dependent scalar loads)
+#pragma unroll 4
             for (int q = 0; q < S; ++q) {
                 const uint64_t *pl = pc + ((int64_t)i * S + q) * P;
                 int32_t part = 0;
