@@ -166,7 +166,7 @@ def bitlogic_encode(x: torch.Tensor, thresholds: torch.Tensor,
     n, d = x.shape
     b = thresholds.shape[1]
     if bits_out is None:
-        bits_out = torch.empty((d * b, words(n)), dtype=torch.int64, device=x.device)
+        bits_out = _empty((d * b, words(n)), torch.int64, x.device, stream)
     _check(load_library().bitlogic_encode(
         _dev(x, "x", _U8), n, d, _dev(thresholds, "thresholds", _U8), b,
         _dev(bits_out, "bits_out", _U64), _stream(stream, x.device)))
@@ -179,7 +179,7 @@ def bitlogic_lut_layer(bits_in: torch.Tensor, conn: torch.Tensor, tables: torch.
     w_in, n_words = bits_in.shape
     w, k = conn.shape
     if bits_out is None:
-        bits_out = torch.empty((w, n_words), dtype=torch.int64, device=bits_in.device)
+        bits_out = _empty((w, n_words), torch.int64, bits_in.device, stream)
     _check(load_library().bitlogic_lut_layer(
         _dev(bits_in, "bits_in", _U64), w_in, n_words, _dev(conn, "conn", _I32),
         _dev(tables, "tables", _U64), w, k, _dev(bits_out, "bits_out", _U64),
@@ -191,12 +191,30 @@ def bitlogic_groupsum_head_workspace_bytes(w: int, n_samples: int, n_classes: in
     return int(load_library().bitlogic_groupsum_head_workspace_bytes(w, n_samples, n_classes))
 
 
-def _workspace(nbytes: int, device, given: Optional[torch.Tensor]) -> Tuple[int, int]:
+def _on_stream(t: Optional[torch.Tensor], handle: int, device) -> Optional[torch.Tensor]:
+    """Tell torch's caching allocator that a tensor this module allocated is used
+    on the HIP stream `handle`, when that is not the current stream: its memory
+    is then not handed out again before the stream's work on it is done."""
+    if t is not None and handle != torch.cuda.current_stream(device).cuda_stream:
+        t.record_stream(torch.cuda.ExternalStream(handle, device=device))
+    return t
+
+
+def _empty(shape, dtype, device, stream) -> torch.Tensor:
+    """An output this module allocates for a call on `stream` (see _on_stream)."""
+    return _on_stream(torch.empty(shape, dtype=dtype, device=device), _stream(stream, device),
+                      device)
+
+
+def _workspace(nbytes: int, device, given: Optional[torch.Tensor],
+               handle: Optional[int] = None) -> Tuple[int, int]:
     if given is not None:
         return _dev(given, "workspace", (torch.uint8,)), given.numel()
     if nbytes == 0:
         return 0, 0
     buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    if handle is not None:
+        _on_stream(buf, handle, device)
     _workspace.keep = buf        # kept alive until the next call allocates one
     return buf.data_ptr(), nbytes
 
@@ -210,11 +228,11 @@ def bitlogic_groupsum_head(bits: torch.Tensor, n_samples: int, n_classes: int,
     w = bits.shape[0]
     dev = bits.device
     if scores is None and want_scores:
-        scores = torch.empty((n_samples, n_classes), dtype=torch.int32, device=dev)
+        scores = _empty((n_samples, n_classes), torch.int32, dev, stream)
     if argmax is None:
-        argmax = torch.empty((n_samples,), dtype=torch.int32, device=dev)
+        argmax = _empty((n_samples,), torch.int32, dev, stream)
     ws_ptr, ws_bytes = _workspace(bitlogic_groupsum_head_workspace_bytes(w, n_samples, n_classes),
-                                  dev, workspace)
+                                  dev, workspace, _stream(stream, dev))
     _check(load_library().bitlogic_groupsum_head(
         _dev(bits, "bits", _U64), w, n_samples, n_classes,
         _dev(scores, "scores", _I32) if scores is not None else None,
@@ -263,7 +281,7 @@ def bitlogic_encode_binary(x: torch.Tensor, n_bits: int,
     wire f*n_bits+t = bit t of round(x * (2^n_bits - 1) / 255)."""
     n, d = x.shape
     if bits_out is None:
-        bits_out = torch.empty((d * n_bits, words(n)), dtype=torch.int64, device=x.device)
+        bits_out = _empty((d * n_bits, words(n)), torch.int64, x.device, stream)
     _check(load_library().bitlogic_encode_binary(_dev(x, "x", _U8), n, d, int(n_bits),
                                                  _dev(bits_out, "bits_out", _U64),
                                                  _stream(stream, x.device)))
@@ -279,10 +297,10 @@ def bitlogic_fit_quantile_thresholds(x: torch.Tensor, n_thresholds: int, n_group
     n, d = x.shape
     dev = x.device
     if out is None:
-        out = torch.empty((d, n_thresholds), dtype=torch.uint8, device=dev)
+        out = _empty((d, n_thresholds), torch.uint8, dev, stream)
     lib = load_library()
     need = int(lib.bitlogic_fit_quantile_thresholds_workspace_bytes(int(n_groups)))
-    ws_ptr, ws_bytes = _workspace(max(need, 8), dev, workspace)
+    ws_ptr, ws_bytes = _workspace(max(need, 8), dev, workspace, _stream(stream, dev))
     _check(lib.bitlogic_fit_quantile_thresholds(_dev(x, "x", _U8), n, d, int(n_thresholds),
                                                 int(n_groups), _dev(out, "out", _U8), ws_ptr,
                                                 ws_bytes, _stream(stream, dev)))
@@ -300,9 +318,9 @@ def bitlogic_grouped_dsp_head(counts: torch.Tensor, weights: torch.Tensor,
     if tuple(weights.shape) != (c, c):
         raise ValueError(f"weights must be [{c}][{c}]")
     if logits is None and want_logits:
-        logits = torch.empty((n, c), dtype=torch.int32, device=dev)
+        logits = _empty((n, c), torch.int32, dev, stream)
     if argmax is None:
-        argmax = torch.empty((n,), dtype=torch.int32, device=dev)
+        argmax = _empty((n,), torch.int32, dev, stream)
     _check(load_library().bitlogic_grouped_dsp_head(
         _dev(counts, "counts", _I32), n, c, _dev(weights, "weights", _I8),
         _dev(logits, "logits", _I32) if logits is not None else None,
@@ -327,10 +345,10 @@ def bitlogic_forward_grouped_dsp(x: torch.Tensor, thresholds: torch.Tensor,
     need = int(lib.bitlogic_forward_workspace_bytes(
         n, d, b, ctypes.cast(arr, ctypes.c_void_p), len(arr), n_classes))
     if logits is None and want_logits:
-        logits = torch.empty((n, n_classes), dtype=torch.int32, device=dev)
+        logits = _empty((n, n_classes), torch.int32, dev, stream)
     if argmax is None:
-        argmax = torch.empty((n,), dtype=torch.int32, device=dev)
-    ws_ptr, ws_bytes = _workspace(need, dev, workspace)
+        argmax = _empty((n,), torch.int32, dev, stream)
+    ws_ptr, ws_bytes = _workspace(need, dev, workspace, _stream(stream, dev))
     _check(lib.bitlogic_forward_grouped_dsp(
         _dev(x, "x", _U8), n, d, _dev(thresholds, "thresholds", _U8), b,
         ctypes.cast(arr, ctypes.c_void_p), len(arr), n_classes, _dev(weights, "weights", _I8),
@@ -349,10 +367,10 @@ def _forward(x, thresholds, layers, n_classes, scores, argmax, workspace, stream
     need = int(lib.bitlogic_forward_workspace_bytes(
         n, d, b, ctypes.cast(arr, ctypes.c_void_p), len(arr), n_classes))
     if scores is None and want_scores:
-        scores = torch.empty((n, n_classes), dtype=torch.int32, device=dev)
+        scores = _empty((n, n_classes), torch.int32, dev, stream)
     if argmax is None:
-        argmax = torch.empty((n,), dtype=torch.int32, device=dev)
-    ws_ptr, ws_bytes = _workspace(need, dev, workspace)
+        argmax = _empty((n,), torch.int32, dev, stream)
+    ws_ptr, ws_bytes = _workspace(need, dev, workspace, _stream(stream, dev))
     args = [_dev(x, "x", _U8), n, d, _dev(thresholds, "thresholds", _U8), b,
             ctypes.cast(arr, ctypes.c_void_p), len(arr), n_classes,
             _dev(scores, "scores", _I32) if scores is not None else None,
@@ -590,10 +608,10 @@ def bitlogic_network_forward(model: BitlogicModel, x: torch.Tensor,
     lib = load_library()
     need = int(lib.bitlogic_network_workspace_bytes(ctypes.byref(net), n))
     if out is None and want_scores:
-        out = torch.empty((n, model.n_classes), dtype=torch.int32, device=dev)
+        out = _empty((n, model.n_classes), torch.int32, dev, stream)
     if argmax is None:
-        argmax = torch.empty((n,), dtype=torch.int32, device=dev)
-    ws_ptr, ws_bytes = _workspace(need, dev, workspace)
+        argmax = _empty((n,), torch.int32, dev, stream)
+    ws_ptr, ws_bytes = _workspace(need, dev, workspace, _stream(stream, dev))
     if events is None:
         ev_ptr, n_ev = None, 0
     else:
