@@ -9,7 +9,9 @@
 // k_encode_t (b <= 8, the hot path).  A block first fills an LDS code table
 // code[f][v] = sum_t (v > theta[f][t]) << t for its tile of features and every
 // pixel value v, then reuses it for several tiles of 16 columns (1024
-// samples); each wave packs 4 of the 16 columns, one at a time.  The table is
+// samples); each wave packs 4 of the 16 columns, one at a time (at small
+// batches 2 or 4 blocks share a tile's columns, down to one per wave, so that
+// more blocks share the latency).  The table is
 // built four codes per thread at a time: a dword holds the codes of four
 // consecutive values, and threshold t sets its bit from the first value above
 // it on.  A lane loads
@@ -71,7 +73,6 @@ struct EncGeom {
 
 constexpr int kEncCols = 16;     // columns per output tile: 128-byte row segments
 constexpr int kOtRow = kEncCols + 1;   // LDS words per tile row (odd: no bank conflicts)
-constexpr int kColsPerWave = kEncCols / (kThreads / kWave);
 
 // This lane's kDw pixel dwords (features f0 .. f0 + 4*kDw - 1 of sample s);
 // zero past the batch or past the last feature.  `full` (wave-uniform): the
@@ -108,7 +109,7 @@ __device__ __forceinline__ void load_pixels(const uint8_t *__restrict__ x, int64
     }
 }
 
-template <int B, int LAYOUT>
+template <int B, int LAYOUT, int CS>
 __global__ __launch_bounds__(kThreads) void k_encode_t(
     const uint8_t *__restrict__ x, int64_t n, int32_t d, const uint8_t *__restrict__ th,
     uint64_t *__restrict__ out, int64_t W, int64_t W_cols, int32_t n_ftiles,
@@ -165,26 +166,32 @@ __global__ __launch_bounds__(kThreads) void k_encode_t(
     uint32_t amt[5], msk[5];
     transpose_consts(lane, amt, msk);
 
-    const int64_t t0 = tg * tiles_per_block;
+    // block tg covers part (tg % CS) of the columns of tile group tg / CS:
+    // cpb columns per tile, cpw consecutive columns per wave
+    constexpr int cpb = kEncCols / CS;
+    constexpr int cpw = cpb / (kThreads / kWave);
+    static_assert(cpw >= 1, "at least one column per wave");
+    const int part = (int)(tg % CS);
+    const int c_first = part * cpb + wave * cpw;      // this wave's first column of a tile
+    const int64_t t0 = (tg / CS) * tiles_per_block;
     const int64_t t1 = min(t0 + tiles_per_block, n_tiles);
-    // this wave's columns: kColsPerWave consecutive columns of every tile
     // columns whose 64 samples are all in the batch, in a full aligned tile
     const bool tile_full = aligned4 && nf == G::kFT;
     auto col_full = [&](int64_t gcol) { return tile_full && (gcol + 1) * kWave <= n; };
     uint32_t px[G::kDw];
     {
-        const int64_t gcol = t0 * kEncCols + wave * kColsPerWave;
+        const int64_t gcol = t0 * kEncCols + c_first;
         load_pixels<G::kDw>(x, gcol * kWave + lane, n, d, f0, nf, aligned4, col_full(gcol), px);
     }
     for (int64_t tile = t0; tile < t1; ++tile) {
-        for (int cw = 0; cw < kColsPerWave; ++cw) {
-            const int col = wave * kColsPerWave + cw;      // column inside the tile
+        for (int cw = 0; cw < cpw; ++cw) {
+            const int col = c_first + cw;                  // column inside the tile
             // prefetch the next column's pixels while this one is packed
             uint32_t nx[G::kDw];
-            const bool more = cw + 1 < kColsPerWave || tile + 1 < t1;
+            const bool more = cw + 1 < cpw || tile + 1 < t1;
             if (more) {
-                const int64_t ncol = (cw + 1 < kColsPerWave) ? tile * kEncCols + col + 1
-                                                             : (tile + 1) * kEncCols + wave * kColsPerWave;
+                const int64_t ncol = (cw + 1 < cpw) ? tile * kEncCols + col + 1
+                                                    : (tile + 1) * kEncCols + c_first;
                 load_pixels<G::kDw>(x, ncol * kWave + lane, n, d, f0, nf, aligned4, col_full(ncol),
                                     nx);
             }
@@ -219,9 +226,9 @@ __global__ __launch_bounds__(kThreads) void k_encode_t(
         __syncthreads();
         // write the tile: each wire's 16 words are one contiguous row segment
         const int64_t wb0 = tile * kEncCols;
-        for (int e = threadIdx.x; e < kWires * (kEncCols / 2); e += kThreads) {
-            const int r = e / (kEncCols / 2);              // tile wire row
-            const int c2 = 2 * (e % (kEncCols / 2));       // even column
+        for (int e = threadIdx.x; e < kWires * (cpb / 2); e += kThreads) {
+            const int r = e / (cpb / 2);                   // tile wire row
+            const int c2 = part * cpb + 2 * (e % (cpb / 2));   // even column
             const int gi = r / G::kWPG, p = r % G::kWPG;
             const int fg = gi * G::kFPG + p / B;           // feature of this wire in the tile
             const int64_t wb = wb0 + c2;
@@ -348,15 +355,29 @@ hipError_t launch_t(const uint8_t *x, int64_t n, int32_t d, const uint8_t *th, u
     // apart, and the lines are fetched again)
     int64_t tpb = n_tiles * n_ftiles / 2048;
     tpb = tpb < 1 ? 1 : (tpb > BL_ENC_TPB ? BL_ENC_TPB : tpb);
-    const int64_t n_tg = (n_tiles + tpb - 1) / tpb;
+    // small batches: split each tile's 16 columns over 2 or 4 blocks (down to
+    // one column per wave), so that more blocks share the latency
+    int32_t csplit = 1;
+    while (csplit < 4 && n_tiles * n_ftiles * csplit < 1024)
+        csplit *= 2;
+    const int64_t n_tg = (n_tiles + tpb - 1) / tpb * csplit;
     const int64_t n_tg_pad = (n_tg + kXcds - 1) / kXcds * kXcds;
     const int64_t blocks = n_tg_pad * n_ftiles;
     if (blocks > 0x7fffffff)
         return hipErrorInvalidConfiguration;
     const int aligned4 = (d % 4 == 0) && ((uintptr_t)x % 4 == 0);
-    hipLaunchKernelGGL((k_encode_t<B, LAYOUT>), dim3((unsigned)blocks), dim3(kThreads), 0, stream,
-                       x, n, d, th, out, W, W_cols, n_ftiles, (int32_t)tpb, n_tiles, n_tg,
-                       aligned4, kind);
+    if (csplit == 4)
+        hipLaunchKernelGGL((k_encode_t<B, LAYOUT, 4>), dim3((unsigned)blocks), dim3(kThreads), 0,
+                           stream, x, n, d, th, out, W, W_cols, n_ftiles, (int32_t)tpb, n_tiles,
+                           n_tg, aligned4, kind);
+    else if (csplit == 2)
+        hipLaunchKernelGGL((k_encode_t<B, LAYOUT, 2>), dim3((unsigned)blocks), dim3(kThreads), 0,
+                           stream, x, n, d, th, out, W, W_cols, n_ftiles, (int32_t)tpb, n_tiles,
+                           n_tg, aligned4, kind);
+    else
+        hipLaunchKernelGGL((k_encode_t<B, LAYOUT, 1>), dim3((unsigned)blocks), dim3(kThreads), 0,
+                           stream, x, n, d, th, out, W, W_cols, n_ftiles, (int32_t)tpb, n_tiles,
+                           n_tg, aligned4, kind);
     return hipGetLastError();
 }
 
