@@ -14,7 +14,8 @@
 // group (LDS atomics), then adds it into the global 64-bit histogram.  Rows
 // are read as coalesced dwords: a thread keeps its columns (and their
 // groups) and walks the rows, eight rows' loads at a time.  k_fit_select:
-// one block per group turns the histogram into the ladder.
+// one block per group turns the histogram into the ladder (a block prefix sum,
+// one thread per bin).
 #include "bl_internal.h"
 
 namespace bl {
@@ -97,23 +98,30 @@ __global__ __launch_bounds__(kThreads) void k_fit_select(
     const uint64_t *__restrict__ ws, int64_t total, int32_t per, int32_t b,
     uint8_t *__restrict__ th)
 {
+    static_assert(kThreads == 256, "one thread per histogram bin");
     __shared__ uint64_t cum[256];
     __shared__ uint8_t ladder[64];
     const int grp = blockIdx.x;
-    if (threadIdx.x == 0) {
-        uint64_t c = 0;
-        for (int v = 0; v < 256; ++v) {
-            c += ws[grp * 256 + v];
-            cum[v] = c;
-        }
-    }
+    const int v = threadIdx.x;
+    // inclusive prefix sum of the 256 bins (Hillis-Steele, 8 steps)
+    cum[v] = ws[grp * 256 + v];
     __syncthreads();
-    if (threadIdx.x < b) {
-        const uint64_t need = (uint64_t)(threadIdx.x + 1) * (uint64_t)total;
-        int v = 0;
-        while (v < 255 && cum[v] * (uint64_t)(b + 1) < need)
-            ++v;
-        ladder[threadIdx.x] = (uint8_t)v;
+#pragma unroll
+    for (int off = 1; off < 256; off <<= 1) {
+        const uint64_t add = v >= off ? cum[v - off] : 0;
+        __syncthreads();
+        cum[v] += add;
+        __syncthreads();
+    }
+    // threshold i is the smallest v with (b + 1) cum(v) >= i total (255 if
+    // none): thread v sets it where the criterion first holds
+    const uint64_t b1 = (uint64_t)(b + 1);
+    for (int i = 1; i <= b; ++i) {
+        const uint64_t need = (uint64_t)i * (uint64_t)total;
+        const bool here = cum[v] * b1 >= need;
+        const bool before = v > 0 && cum[v - 1] * b1 >= need;
+        if ((here && !before) || (v == 255 && !here))
+            ladder[i - 1] = (uint8_t)v;
     }
     __syncthreads();
     uint8_t *dst = th + (int64_t)grp * per * b;
