@@ -370,7 +370,11 @@ const char *bitlogic_status_string(int status);
 /* Detail of the last failing call on this host thread ("" if none). */
 const char *bitlogic_last_error(void);
 
-/* Library version, major * 10000 + minor * 100 + patch. */
+/* Library version, major * 10000 + minor * 100 + patch.  A caller built
+ * against this header can check bitlogic_version() == BITLOGIC_VERSION
+ * before using the structs above (0.3.0 added bitlogic_network.pass_fanin and
+ * the specialization calls). */
+#define BITLOGIC_VERSION 300
 int bitlogic_version(void);
 
 #ifdef __cplusplus

@@ -693,6 +693,6 @@ const char *bitlogic_status_string(int status)
 
 const char *bitlogic_last_error(void) { return g_last_error; }
 
-int bitlogic_version(void) { return 200; }
+int bitlogic_version(void) { return BITLOGIC_VERSION; }
 
 }  // extern "C"

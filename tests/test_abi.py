@@ -47,7 +47,8 @@ def test_status_strings(lib):
     for s in range(7):
         assert bl.bitlogic_status_string(s) and bl.bitlogic_status_string(s) != "unknown status"
     assert bl.bitlogic_status_string(99) == "unknown status"
-    assert bl.bitlogic_version() >= 100
+    hdr = open(os.path.join(os.path.dirname(__file__), "..", "include", "bitlogic.h")).read()
+    assert bl.bitlogic_version() == int(re.search(r"#define BITLOGIC_VERSION (\d+)", hdr).group(1))
 
 
 def _err(lib):
