@@ -110,6 +110,18 @@ def algorithmic(cfg, n, fused_head, binary_bits=0, fanin_hist=None):
     return st
 
 
+def cpu_model() -> str:
+    """The host CPU's model name, from /proc/cpuinfo (empty if unreadable)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return ""
+
+
 def measured_traffic(stage):
     """HBM bytes per launch of `stage` from the committed rocprofv3 counter
     summary (FETCH_SIZE + WRITE_SIZE, scaled), or None when a kernel source
@@ -374,11 +386,20 @@ def main():
         cpu_s = time.perf_counter() - t0
         agree = bool(np.array_equal(scores.cpu().numpy()[idx].astype(np.int64), rs) and
                      np.array_equal(argmax.cpu().numpy()[idx], rp))
+        # one thread on a smaller sample (about a tenth of the time budget)
+        m1 = int(min(m, max(64, args.cpu_seconds / 10 / max(per * threads, 1e-9))))
+        t0 = time.perf_counter()
+        oracle.forward(xs[:m1], wl.thresholds, wl.layers, wl.n_classes, n_threads=1,
+                       binary_bits=binary_bits)
+        cpu1_s = time.perf_counter() - t0
         cpu = {"value": round(m / cpu_s / 1e6, 6), "unit": "MSamples/s", "cores": threads,
                "kind": "oracle",
                "sample": f"{m} random samples of the {n}-sample batch, whole forward, "
                          f"{cpu_s:.1f} s on {threads} OpenMP threads",
-               "gpu_agrees_on_sample": agree}
+               "gpu_agrees_on_sample": agree,
+               "single_thread_value": round(m1 / cpu1_s / 1e6, 6),
+               "single_thread_sample": f"the first {m1} of those samples, {cpu1_s:.1f} s",
+               "cpu_model": cpu_model()}
         print(f"[bench] oracle: {m} samples in {cpu_s:.1f}s on {threads} threads; "
               f"GPU agrees: {agree}", file=sys.stderr, flush=True)
 
