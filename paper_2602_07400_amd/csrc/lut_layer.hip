@@ -322,8 +322,18 @@ __global__ __launch_bounds__(kThreads, BL_LUT_MINWAVES) void k_lut_slab(
 // batch is so small that 512-node blocks would leave most CUs idle and each
 // block's passes would run one gather latency after another.
 constexpr int kSlabNB = 512;
-constexpr int kSlabNBSmall = kThreads / kSlabLanes;     // one pass
 constexpr int64_t kSlabSmallBlocks = 2048;
+
+// Lanes per node: 4 (8 half-words each) for 5 and 6 inputs, where the masks'
+// reuse matters; 8 (one full 128-byte line per node in each gather
+// instruction) for up to 4 inputs, whose layers are bound by the gathers'
+// L1-miss path rather than the VALU (C5: layer 1 5% faster at k = 2, 2.5%
+// at k = 4; 4% slower at k = 6).
+template <int K>
+constexpr int slab_lanes()
+{
+    return K <= 4 ? 8 : kSlabLanes;
+}
 
 template <int K, int NB>
 hipError_t launch_slab_kn(const uint64_t *in, int32_t w_in, int64_t n_slabs,
@@ -336,11 +346,11 @@ hipError_t launch_slab_kn(const uint64_t *in, int32_t w_in, int64_t n_slabs,
     if (blocks > 0x7fffffff)
         return hipErrorInvalidConfiguration;
     if (fanin)
-        hipLaunchKernelGGL((k_lut_slab<K, kSlabWords, kSlabLanes, NB, true>),
+        hipLaunchKernelGGL((k_lut_slab<K, kSlabWords, slab_lanes<K>(), NB, true>),
                            dim3((unsigned)blocks), dim3(kThreads), 0, stream, in, w_in, conn,
                            tables, w_out, out, n_nblk, (int32_t)n_slabs, fanin);
     else
-        hipLaunchKernelGGL((k_lut_slab<K, kSlabWords, kSlabLanes, NB, false>),
+        hipLaunchKernelGGL((k_lut_slab<K, kSlabWords, slab_lanes<K>(), NB, false>),
                            dim3((unsigned)blocks), dim3(kThreads), 0, stream, in, w_in, conn,
                            tables, w_out, out, n_nblk, (int32_t)n_slabs, fanin);
     return hipGetLastError();
@@ -352,9 +362,9 @@ hipError_t launch_slab_k(const uint64_t *in, int32_t w_in, int64_t n_slabs,
                          uint64_t *out, const uint8_t *fanin, hipStream_t stream)
 {
     const int64_t big = n_slabs * ((w_out + kSlabNB - 1) / kSlabNB);
-    if (big < kSlabSmallBlocks)
-        return launch_slab_kn<K, kSlabNBSmall>(in, w_in, n_slabs, conn, tables, w_out, out,
-                                                fanin, stream);
+    if (big < kSlabSmallBlocks)     // one pass per block
+        return launch_slab_kn<K, kThreads / slab_lanes<K>()>(in, w_in, n_slabs, conn, tables,
+                                                             w_out, out, fanin, stream);
     return launch_slab_kn<K, kSlabNB>(in, w_in, n_slabs, conn, tables, w_out, out, fanin,
                                       stream);
 }
