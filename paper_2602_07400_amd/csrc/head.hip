@@ -11,10 +11,10 @@
 // (v_bitop3 full adders, ~2 ops per word per 32 samples), one lane per column
 // so every row load is a coalesced 512-byte segment.  Long groups are split
 // into row ranges so the launch fills the chip.  Stage 2 runs one lane per
-// sample and one block per column: its waves share the classes, assemble each
-// class score bit by bit from the column's planes (wave-uniform scalar loads)
-// and sum the splits into an LDS score tile, from which the argmax is taken
-// and the scores are written as one contiguous block.
+// sample and one block per column: the column's planes are staged in LDS with
+// coalesced loads, its waves share the classes, assemble each class score bit
+// by bit and sum the splits into an LDS score tile, from which the scores are
+// written as one contiguous block, and take the argmax.
 //
 // Quantized head (Sec. 3 "Encoders and heads"; Sec. 5 "Head", the DSP-backed
 // head): logit i = sum_j Q[i][j] * count[j] with Q a c x c matrix of signed
@@ -128,65 +128,137 @@ __global__ __launch_bounds__(kThreads) void k_head_planes(
     }
 }
 
-constexpr int kFinishClasses = 128;   // classes per LDS score tile
+constexpr int kFinishClasses = 128;                   // classes per chunk
+constexpr int kFinishPerWave = kFinishClasses / kWaves;
+// LDS of the finish: one buffer that first stages plane words (uint64) and
+// then holds the score tile [64][cs] (int32, cs = the odd stride >= the
+// chunk's classes, so the tile has no bank conflicts).  It is sized per launch
+// (finish_lds_words): the larger of the tile and the planes of one chunk, at
+// most the planes of a 129-stride tile's worth of words.
+constexpr int kFinishMaxWords = kWave * (kFinishClasses + 1) / 2;   // uint64 words
 
-// One block (4 waves) per 64-sample column, one lane per sample.  The waves
-// take classes round-robin; a class score is assembled bit by bit from the
-// column's planes (contiguous [class][split][plane], wave-uniform scalar
-// loads) and parked in an LDS tile [64][classes]; then every lane scans its
-// sample's row of the tile for the argmax (lowest index on ties) and the tile
-// is written to scores as one contiguous block.
+int32_t finish_stride(int32_t c)
+{
+    return (c < kFinishClasses ? c : kFinishClasses) | 1;
+}
+
+int64_t finish_lds_words(int32_t c, int32_t S, int32_t P)
+{
+    const int64_t tile = ((int64_t)kWave * finish_stride(c) + 1) / 2;
+    const int64_t stage = (int64_t)(c < kFinishClasses ? c : kFinishClasses) * S * P;
+    const int64_t want = stage < kFinishMaxWords ? stage : kFinishMaxWords;
+    return tile > want ? tile : want;
+}
+
+// One block (4 waves) per 64-sample column, one lane per sample.  Per chunk of
+// up to 128 classes, the block first copies the chunk's planes ([class]
+// [split][plane], contiguous) into LDS with coalesced loads, all in flight at
+// once (a class's planes are otherwise a chain of scalar loads, one latency
+// per class); when a chunk's splits do not fit, it is copied in runs of
+// splits.  Wave w counts classes w, w + 4, ...: bit `lane` of each plane word
+// (a broadcast LDS read of the word's half) goes to bit p of the count, and
+// the splits are summed in registers.  The counts then go to an LDS tile
+// [64][cs] (odd stride), from which the scores leave as one contiguous
+// block.  Each wave keeps its own running argmax in class order; the four
+// are merged at the end (largest count, then lowest class).
 template <int P>
 __global__ __launch_bounds__(kThreads) void k_head_finish(
     const uint64_t *__restrict__ planes, int64_t W, int64_t n, int32_t c, int32_t S,
-    int32_t *__restrict__ scores, int32_t *__restrict__ argmax)
+    int32_t cs, int32_t buf_words, int32_t *__restrict__ scores, int32_t *__restrict__ argmax)
 {
-    extern __shared__ int32_t tile[];     // [64][min(c, kFinishClasses)]
+    extern __shared__ uint64_t buf[];                 // buf_words words
+    __shared__ int32_t part[2][kWaves][kWave];
+    const uint32_t *buf32 = reinterpret_cast<const uint32_t *>(buf);
+    int32_t *tile = reinterpret_cast<int32_t *>(buf);
     const int lane = threadIdx.x % kWave;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int half = lane >> 5, bit = lane & 31;
     const int64_t col = blockIdx.x;
     const int64_t s0 = col * kWave;
     const uint64_t *pc = planes + col * (int64_t)c * S * P;
+    const int32_t sp_words = S * P;                   // one class's plane words
     int32_t best = -1, besti = 0;
-    for (int c0 = 0; c0 < c; c0 += kFinishClasses) {
-        const int cn = min(kFinishClasses, c - c0);
-        for (int ii = wave; ii < cn; ii += kWaves) {
-            const int i = c0 + ii;
-            int32_t cnt = 0;
-            // four splits' loads in flight together (a class's splits are
-            // otherwise a chain of dependent scalar loads)
-#pragma unroll 4
-            for (int q = 0; q < S; ++q) {
-                const uint64_t *pl = pc + ((int64_t)i * S + q) * P;
-                int32_t part = 0;
+    for (int c0 = 0, cn = 0; c0 < c; c0 += cn) {
+        // classes of this chunk, and splits per staged run
+        cn = min(kFinishClasses, c - c0);
+        if ((int64_t)cn * sp_words > buf_words)
+            cn = max(1, buf_words / sp_words);
+        const int run = (int64_t)cn * sp_words <= buf_words ? S : buf_words / P;
+        int32_t cnt[kFinishPerWave];
 #pragma unroll
-                for (int p = 0; p < P; ++p)
-                    part |= (int32_t)((pl[p] >> lane) & 1u) << p;
-                cnt += part;
+        for (int j = 0; j < kFinishPerWave; ++j)
+            cnt[j] = 0;
+        for (int q0 = 0; q0 < S; q0 += run) {
+            const int qn = min(run, S - q0);
+            // contiguous: either whole classes (qn == S) or one class (cn == 1)
+            const uint64_t *src = pc + ((int64_t)c0 * S + q0) * P;
+            const int words = cn * qn * P;
+            for (int e = threadIdx.x; e < words; e += kThreads)
+                buf[e] = src[e];
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < kFinishPerWave; ++j) {
+                const int ii = wave + kWaves * j;
+                if (ii < cn) {
+                    int32_t acc = 0;
+                    for (int q = 0; q < qn; ++q) {
+                        const uint32_t *w = buf32 + 2 * (ii * qn + q) * P + half;
+                        int32_t v = 0;
+#pragma unroll
+                        for (int p = 0; p < P; ++p)
+                            v |= (int32_t)((w[2 * p] >> bit) & 1u) << p;
+                        acc += v;
+                    }
+                    cnt[j] += acc;
+                }
             }
-            tile[lane * cn + ii] = cnt;
+            __syncthreads();
         }
-        __syncthreads();
-        if (wave == 0) {
-            for (int ii = 0; ii < cn; ++ii) {
-                const int32_t v = tile[lane * cn + ii];
-                if (v > best) {
-                    best = v;
+#pragma unroll
+        for (int j = 0; j < kFinishPerWave; ++j) {
+            const int ii = wave + kWaves * j;
+            if (ii < cn) {
+                tile[lane * cs + ii] = cnt[j];
+                if (cnt[j] > best) {             // classes ascend within a wave
+                    best = cnt[j];
                     besti = c0 + ii;
                 }
             }
         }
+        __syncthreads();
         if (scores) {
-            for (int e = threadIdx.x; e < kWave * cn; e += kThreads) {
-                const int64_t ss = s0 + e / cn;
-                if (ss < n)
-                    scores[ss * c + c0 + e % cn] = tile[e];
+            // element e = r * cn + k of the contiguous block, walked without a
+            // division per element
+            const int e0 = threadIdx.x;
+            int r = e0 / cn, k = e0 - r * cn;
+            const int dr = kThreads / cn, dk = kThreads - dr * cn;
+            for (int e = e0; e < kWave * cn; e += kThreads) {
+                if (s0 + r < n)
+                    scores[(s0 + r) * c + c0 + k] = tile[r * cs + k];
+                r += dr;
+                k += dk;
+                if (k >= cn) {
+                    k -= cn;
+                    ++r;
+                }
             }
         }
         __syncthreads();
     }
-    if (wave == 0 && argmax && s0 + lane < n)
-        argmax[s0 + lane] = besti;
+    part[0][wave][lane] = best;
+    part[1][wave][lane] = besti;
+    __syncthreads();
+    if (wave == 0 && argmax && s0 + lane < n) {
+        int32_t b = part[0][0][lane], bi = part[1][0][lane];
+        for (int w = 1; w < kWaves; ++w) {
+            const int32_t v = part[0][w][lane], vi = part[1][w][lane];
+            if (v > b || (v == b && vi < bi)) {
+                b = v;
+                bi = vi;
+            }
+        }
+        argmax[s0 + lane] = bi;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -202,10 +274,12 @@ typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 // the products are in registers; and the argmax partials.
 struct DspLayout {
     int cn, ck, ckp;
-    size_t off_q, off_rs, off_lo, off_hi, off_tile, off_part, bytes;
+    size_t off_q, off_rs, off_lo, off_hi, off_tile, off_part, off_stage, bytes;
 };
 
-__host__ __device__ inline DspLayout dsp_layout(int c)
+// stage_words: room for that many plane words (uint64) after the partials,
+// where the fused finish stages a column's planes (0: none)
+__host__ __device__ inline DspLayout dsp_layout(int c, int stage_words = 0)
 {
     DspLayout L;
     L.cn = (c + 15) / 16 * 16;
@@ -219,7 +293,8 @@ __host__ __device__ inline DspLayout dsp_layout(int c)
     L.off_tile = L.off_lo;
     const size_t tile_end = L.off_tile + (size_t)kWave * c * 4;
     L.off_part = ((planes_end > tile_end ? planes_end : tile_end) + 15) / 16 * 16;
-    L.bytes = L.off_part + 2 * kWaves * kWave * 4;
+    L.off_stage = L.off_part + 2 * kWaves * kWave * 4;
+    L.bytes = L.off_stage + (size_t)stage_words * 8;
     return L;
 }
 
@@ -371,29 +446,48 @@ __device__ __forceinline__ void dsp_emit(uint8_t *smem, const DspLayout &L, int 
 }
 
 // Fused finish of the quantized head: class counts of a 64-sample column from
-// the bit planes (as k_head_finish), then the logits on the matrix cores.
+// the bit planes (as k_head_finish: the column's planes staged in LDS with
+// coalesced loads when they fit in stage_words, else read class by class),
+// then the logits on the matrix cores.
 template <int P>
 __global__ __launch_bounds__(kThreads) void k_head_finish_dsp(
-    const uint64_t *__restrict__ planes, int64_t n, int32_t c, int32_t S,
+    const uint64_t *__restrict__ planes, int64_t n, int32_t c, int32_t S, int32_t stage_words,
     const int8_t *__restrict__ weights, int32_t *__restrict__ logits,
     int32_t *__restrict__ argmax)
 {
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-    const DspLayout L = dsp_layout(c);
+    const DspLayout L = dsp_layout(c, stage_words);
+    uint64_t *stage = reinterpret_cast<uint64_t *>(smem + L.off_stage);
+    const uint32_t *stage32 = reinterpret_cast<const uint32_t *>(stage);
     const int lane = threadIdx.x % kWave;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int half = lane >> 5, bit = lane & 31;
     const int64_t W = (n + kWave - 1) / kWave;
+    const int32_t words = c * S * P;                  // one column's plane words
+    const bool staged = words <= stage_words;
     dsp_stage_q(weights, c, L, smem);
     for (int64_t col = blockIdx.x; col < W; col += gridDim.x) {
         const uint64_t *pc = planes + col * (int64_t)c * S * P;
+        if (staged) {
+            for (int e = threadIdx.x; e < words; e += kThreads)
+                stage[e] = pc[e];
+            __syncthreads();
+        }
         for (int i = wave; i < c; i += kWaves) {
             int32_t cnt = 0;
             for (int q = 0; q < S; ++q) {
-                const uint64_t *pl = pc + ((int64_t)i * S + q) * P;
                 int32_t part = 0;
+                if (staged) {
+                    const uint32_t *w = stage32 + 2 * (i * S + q) * P + half;
 #pragma unroll
-                for (int p = 0; p < P; ++p)
-                    part |= (int32_t)((pl[p] >> lane) & 1u) << p;
+                    for (int p = 0; p < P; ++p)
+                        part |= (int32_t)((w[2 * p] >> bit) & 1u) << p;
+                } else {
+                    const uint64_t *pl = pc + ((int64_t)i * S + q) * P;
+#pragma unroll
+                    for (int p = 0; p < P; ++p)
+                        part |= (int32_t)((pl[p] >> lane) & 1u) << p;
+                }
                 cnt += part;
             }
             dsp_put_count(smem, L, lane, i, cnt);
@@ -601,14 +695,17 @@ hipError_t launch_finish_p(const uint64_t *planes, int64_t n, int32_t c, int32_t
             return hipErrorInvalidValue;
         // Q is staged once per block and reused for a run of columns
         const int64_t blocks = W < kDspFinishBlocks ? W : kDspFinishBlocks;
+        const int64_t want = (int64_t)c * plan.splits * P;
+        const int32_t stage_words = want <= kFinishMaxWords ? (int32_t)want : 0;
         hipLaunchKernelGGL(k_head_finish_dsp<P>, dim3((unsigned)blocks), dim3(kThreads),
-                           dsp_layout(c).bytes, stream, planes, n, c, plan.splits, dsp_weights,
-                           scores, argmax);
+                           dsp_layout(c, stage_words).bytes, stream, planes, n, c, plan.splits,
+                           stage_words, dsp_weights, scores, argmax);
         return hipGetLastError();
     }
-    const size_t lds = (size_t)kWave * (c < kFinishClasses ? c : kFinishClasses) * sizeof(int32_t);
-    hipLaunchKernelGGL(k_head_finish<P>, dim3((unsigned)W), dim3(kThreads), lds, stream,
-                       planes, W, n, c, plan.splits, scores, argmax);
+    const int64_t words = finish_lds_words(c, plan.splits, P);
+    hipLaunchKernelGGL(k_head_finish<P>, dim3((unsigned)W), dim3(kThreads),
+                       (size_t)words * sizeof(uint64_t), stream, planes, W, n, c, plan.splits,
+                       finish_stride(c), (int32_t)words, scores, argmax);
     return hipGetLastError();
 }
 

@@ -185,6 +185,9 @@ HEAD_CASES = [
     (1000, 7, 1000, 1.0),      # all one: ties at g -> argmax 0
     (1500, 10, 3200, 0.5),
     (128, 4, 65535, 0.02),      # the largest group size
+    (200, 129, 40, 0.5),       # a second chunk of one class in the finish
+    (100, 300, 7, 0.5),        # three chunks
+    (70, 1000, 2, 0.5),        # many classes of two nodes
 ]
 
 
