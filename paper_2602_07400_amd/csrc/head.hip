@@ -24,6 +24,7 @@
 // with h, l in [-128, 127], so logit = 256 (Q h) + (Q l) + 32896 rowsum(Q),
 // exact in 32-bit integers for c <= 128.
 #include "bl_internal.h"
+#include "head_finish.h"
 
 namespace bl {
 
@@ -128,137 +129,15 @@ __global__ __launch_bounds__(kThreads) void k_head_planes(
     }
 }
 
-constexpr int kFinishClasses = 128;                   // classes per chunk
-constexpr int kFinishPerWave = kFinishClasses / kWaves;
-// LDS of the finish: one buffer that first stages plane words (uint64) and
-// then holds the score tile [64][cs] (int32, cs = the odd stride >= the
-// chunk's classes, so the tile has no bank conflicts).  It is sized per launch
-// (finish_lds_words): the larger of the tile and the planes of one chunk, at
-// most the planes of a 129-stride tile's worth of words.
-constexpr int kFinishMaxWords = kWave * (kFinishClasses + 1) / 2;   // uint64 words
-
-int32_t finish_stride(int32_t c)
-{
-    return (c < kFinishClasses ? c : kFinishClasses) | 1;
-}
-
-int64_t finish_lds_words(int32_t c, int32_t S, int32_t P)
-{
-    const int64_t tile = ((int64_t)kWave * finish_stride(c) + 1) / 2;
-    const int64_t stage = (int64_t)(c < kFinishClasses ? c : kFinishClasses) * S * P;
-    const int64_t want = stage < kFinishMaxWords ? stage : kFinishMaxWords;
-    return tile > want ? tile : want;
-}
-
-// One block (4 waves) per 64-sample column, one lane per sample.  Per chunk of
-// up to 128 classes, the block first copies the chunk's planes ([class]
-// [split][plane], contiguous) into LDS with coalesced loads, all in flight at
-// once (a class's planes are otherwise a chain of scalar loads, one latency
-// per class); when a chunk's splits do not fit, it is copied in runs of
-// splits.  Wave w counts classes w, w + 4, ...: bit `lane` of each plane word
-// (a broadcast LDS read of the word's half) goes to bit p of the count, and
-// the splits are summed in registers.  The counts then go to an LDS tile
-// [64][cs] (odd stride), from which the scores leave as one contiguous
-// block.  Each wave keeps its own running argmax in class order; the four
-// are merged at the end (largest count, then lowest class).
+// One block (4 waves) per 64-sample column: finish::column (head_finish.h).
 template <int P>
 __global__ __launch_bounds__(kThreads) void k_head_finish(
-    const uint64_t *__restrict__ planes, int64_t W, int64_t n, int32_t c, int32_t S,
-    int32_t cs, int32_t buf_words, int32_t *__restrict__ scores, int32_t *__restrict__ argmax)
+    const uint64_t *__restrict__ planes, int64_t n, int32_t c, int32_t S, int32_t cs,
+    int32_t buf_words, int32_t *__restrict__ scores, int32_t *__restrict__ argmax)
 {
     extern __shared__ uint64_t buf[];                 // buf_words words
-    __shared__ int32_t part[2][kWaves][kWave];
-    const uint32_t *buf32 = reinterpret_cast<const uint32_t *>(buf);
-    int32_t *tile = reinterpret_cast<int32_t *>(buf);
-    const int lane = threadIdx.x % kWave;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int half = lane >> 5, bit = lane & 31;
-    const int64_t col = blockIdx.x;
-    const int64_t s0 = col * kWave;
-    const uint64_t *pc = planes + col * (int64_t)c * S * P;
-    const int32_t sp_words = S * P;                   // one class's plane words
-    int32_t best = -1, besti = 0;
-    for (int c0 = 0, cn = 0; c0 < c; c0 += cn) {
-        // classes of this chunk, and splits per staged run
-        cn = min(kFinishClasses, c - c0);
-        if ((int64_t)cn * sp_words > buf_words)
-            cn = max(1, buf_words / sp_words);
-        const int run = (int64_t)cn * sp_words <= buf_words ? S : buf_words / P;
-        int32_t cnt[kFinishPerWave];
-#pragma unroll
-        for (int j = 0; j < kFinishPerWave; ++j)
-            cnt[j] = 0;
-        for (int q0 = 0; q0 < S; q0 += run) {
-            const int qn = min(run, S - q0);
-            // contiguous: either whole classes (qn == S) or one class (cn == 1)
-            const uint64_t *src = pc + ((int64_t)c0 * S + q0) * P;
-            const int words = cn * qn * P;
-            for (int e = threadIdx.x; e < words; e += kThreads)
-                buf[e] = src[e];
-            __syncthreads();
-#pragma unroll
-            for (int j = 0; j < kFinishPerWave; ++j) {
-                const int ii = wave + kWaves * j;
-                if (ii < cn) {
-                    int32_t acc = 0;
-                    for (int q = 0; q < qn; ++q) {
-                        const uint32_t *w = buf32 + 2 * (ii * qn + q) * P + half;
-                        int32_t v = 0;
-#pragma unroll
-                        for (int p = 0; p < P; ++p)
-                            v |= (int32_t)((w[2 * p] >> bit) & 1u) << p;
-                        acc += v;
-                    }
-                    cnt[j] += acc;
-                }
-            }
-            __syncthreads();
-        }
-#pragma unroll
-        for (int j = 0; j < kFinishPerWave; ++j) {
-            const int ii = wave + kWaves * j;
-            if (ii < cn) {
-                tile[lane * cs + ii] = cnt[j];
-                if (cnt[j] > best) {             // classes ascend within a wave
-                    best = cnt[j];
-                    besti = c0 + ii;
-                }
-            }
-        }
-        __syncthreads();
-        if (scores) {
-            // element e = r * cn + k of the contiguous block, walked without a
-            // division per element
-            const int e0 = threadIdx.x;
-            int r = e0 / cn, k = e0 - r * cn;
-            const int dr = kThreads / cn, dk = kThreads - dr * cn;
-            for (int e = e0; e < kWave * cn; e += kThreads) {
-                if (s0 + r < n)
-                    scores[(s0 + r) * c + c0 + k] = tile[r * cs + k];
-                r += dr;
-                k += dk;
-                if (k >= cn) {
-                    k -= cn;
-                    ++r;
-                }
-            }
-        }
-        __syncthreads();
-    }
-    part[0][wave][lane] = best;
-    part[1][wave][lane] = besti;
-    __syncthreads();
-    if (wave == 0 && argmax && s0 + lane < n) {
-        int32_t b = part[0][0][lane], bi = part[1][0][lane];
-        for (int w = 1; w < kWaves; ++w) {
-            const int32_t v = part[0][w][lane], vi = part[1][w][lane];
-            if (v > b || (v == b && vi < bi)) {
-                b = v;
-                bi = vi;
-            }
-        }
-        argmax[s0 + lane] = bi;
-    }
+    __shared__ int32_t part[2][finish::kWaves][kWave];
+    finish::column<P>(planes, blockIdx.x, n, c, S, cs, buf_words, buf, part, scores, argmax);
 }
 
 // ---------------------------------------------------------------------------
@@ -696,16 +575,16 @@ hipError_t launch_finish_p(const uint64_t *planes, int64_t n, int32_t c, int32_t
         // Q is staged once per block and reused for a run of columns
         const int64_t blocks = W < kDspFinishBlocks ? W : kDspFinishBlocks;
         const int64_t want = (int64_t)c * plan.splits * P;
-        const int32_t stage_words = want <= kFinishMaxWords ? (int32_t)want : 0;
+        const int32_t stage_words = want <= finish::kMaxWords ? (int32_t)want : 0;
         hipLaunchKernelGGL(k_head_finish_dsp<P>, dim3((unsigned)blocks), dim3(kThreads),
                            dsp_layout(c, stage_words).bytes, stream, planes, n, c, plan.splits,
                            stage_words, dsp_weights, scores, argmax);
         return hipGetLastError();
     }
-    const int64_t words = finish_lds_words(c, plan.splits, P);
+    const int64_t words = finish::lds_words(c, plan.splits, P);
     hipLaunchKernelGGL(k_head_finish<P>, dim3((unsigned)W), dim3(kThreads),
-                       (size_t)words * sizeof(uint64_t), stream, planes, W, n, c, plan.splits,
-                       finish_stride(c), (int32_t)words, scores, argmax);
+                       (size_t)words * sizeof(uint64_t), stream, planes, n, c, plan.splits,
+                       finish::stride(c), (int32_t)words, scores, argmax);
     return hipGetLastError();
 }
 
