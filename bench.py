@@ -129,6 +129,9 @@ def measured_traffic(stage):
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f)
+        sources = {n for n in os.listdir(CSRC) if n.endswith((".hip", ".h"))}
+        if sources != set(rec["sources_sha256"]):
+            return None
         for name, digest in rec["sources_sha256"].items():
             with open(os.path.join(CSRC, name), "rb") as f:
                 if hashlib.sha256(f.read()).hexdigest() != digest:
