@@ -64,6 +64,15 @@
  *   1 <= n_thresholds <= 64; every row count fits in int32; the head needs
  *   w % n_classes == 0 and g = w / n_classes <= 65535.
  * - Entry points are thread-safe; calls on one stream run in order.
+ *
+ * ---------------------------------------------------- environment switches
+ * Read at every forward call; they change which kernels run, never results.
+ *   BITLOGIC_UNFUSED_HEAD=1   the forward stores the last layer's bits and
+ *                             runs the separate head kernels instead of the
+ *                             last layer fused with the GroupSum counting.
+ *   BITLOGIC_FUSED_NETWORK=1  GroupSum networks whose activations of 64
+ *                             samples fit in LDS run as one whole-network
+ *                             kernel (bitlogic_forward_info.fused_network).
  */
 #ifndef BITLOGIC_H
 #define BITLOGIC_H
