@@ -359,3 +359,33 @@ def test_forward_fused_head_matches_oracle_and_unfused(g, c, k, n, monkeypatch):
     rs, rp = oracle.forward(x, th, layers, c)
     assert np.array_equal(s_f.cpu().numpy(), rs) and np.array_equal(p_f.cpu().numpy(), rp)
     assert torch.equal(s_f, s_u) and torch.equal(p_f, p_u)
+
+
+@pytest.mark.parametrize("c,g", [(600, 2), (1000, 1)])
+def test_forward_index_space_beyond_int32(c, g):
+    """A 4M-sample batch with 600 or 1000 classes: scores hold n * c > 2^31
+    entries (> 2^32 at 1000 classes), so every score index needs 64-bit
+    arithmetic; the batch has a ragged tail.  The oracle checks sampled rows,
+    the first and last ones included."""
+    n, d, b = (1 << 22) + 37, 16, 2
+    rng = np.random.default_rng(c + g)
+    x = rng.integers(0, 256, size=(n, d), dtype=np.uint8)
+    th = np.sort(rng.integers(0, 256, size=(d, b), dtype=np.uint8), axis=1)
+    layers, w_in = [], d * b
+    for w, k in ((1500, 6), (c * g, 4)):
+        conn = np.stack([rng.choice(w_in, size=k, replace=False) for _ in range(w)]).astype(np.int32)
+        layers.append((conn, rng.integers(0, 1 << 63, size=w, dtype=np.int64).astype(np.uint64)))
+        w_in = w
+    model = bl.BitlogicModel.from_numpy(th, layers, c, device=DEV)
+    scores, argmax = model.forward(torch.from_numpy(x).to(DEV))
+    torch.cuda.synchronize()
+    assert scores.numel() > (1 << 31)
+    idx = np.unique(np.concatenate([np.arange(64), np.arange(n - 101, n),
+                                    rng.choice(n, size=800, replace=False)]))
+    sel = torch.from_numpy(idx).to(DEV)
+    got_s, got_p = scores[sel].cpu().numpy(), argmax[sel].cpu().numpy()
+    ref_s, ref_p = oracle.forward(x[idx], th, layers, c)
+    assert np.array_equal(got_s, ref_s), _report("scores", got_s, ref_s)
+    assert np.array_equal(got_p, ref_p), _report("argmax", got_p, ref_p)
+    del scores, argmax
+    torch.cuda.empty_cache()
