@@ -9,13 +9,17 @@ bitlogic_forward.  Default workload: the CIFAR-100-shaped wide network
 
 Prints ONE JSON line.  Besides the driver's fields it carries
   roofline      the dominant kernel (the stage of the forward with the longest
-                launch; on C4 a k = 6 LUT layer, integer-VALU bound) against
-                the chip's peak for its bound, from per-launch HIP-event times
+                launch; on C4 a k = 6 LUT layer, which the roofline model puts
+                on the integer VALU) against the chip's published peak for its
+                bound, from per-launch HIP-event times
                 that the library records between the stages of the same
                 forward (bitlogic_forward_timed);
   cpu_baseline  the CPU oracle timed on a bounded sample of the same
                 workload on this host (and its agreement with the GPU there);
-  detail        per-stage times, algorithmic bytes/ops and roofline fractions.
+  detail        per-stage times, algorithmic bytes/ops and roofline fractions,
+                and the peaks measured on this device by the library's probes
+                (integer VALU rate, HBM copy rate) with the dominant kernel's
+                fraction of them.
 
 Algorithmic work follows the path the library takes (bitlogic_forward_plan):
 when the last LUT layer is fused with the GroupSum head its output bits are
@@ -35,9 +39,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 # MI355X peaks (published): HBM3E bandwidth; 32-bit VALU lane-ops from
-# 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+# 256 CUs x 4 SIMDs x 32 lanes a clock x 2.4 GHz (the published fp32 vector
+# peak, 157.3 TFLOP/s, counts an FMA as two operations; the integer
+# v_bitop3_b32 of the LUT layers issues at the same 32 lanes a clock)
 PEAK_HBM_GBS = 8000.0
-PEAK_VALU_TOPS = 256 * 64 * 2.4e9 / 1e12      # 39.32 T lane-ops/s
+PEAK_VALU_TOPS = 256 * 4 * 32 * 2.4e9 / 1e12      # 78.64 T lane-ops/s
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "forward_c4_traffic.json")
 
@@ -57,6 +63,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-peaks", action="store_true",
+                    help="skip the on-device peak probes (integer VALU rate, HBM copy rate)")
     ap.add_argument("--stage-steps", type=int, default=None,
                     help="steps of the per-kernel (staged) timing loop; default = --steps")
     ap.add_argument("--batch", type=int, default=None,
@@ -242,6 +250,38 @@ def main():
     stage_ms = dict(zip(names, (sums / ksteps).tolist()))
     plan = model.plan(n)
     whole = plan["fused_network"]
+
+    # ---- on-device peaks, after the timed work: probes with the hot path's
+    # instruction and access types (v_bitop3_b32 chains; 16-byte non-temporal
+    # copies), giving measured roofline denominators beside the published ones
+    peaks = None
+    if not args.no_peaks:
+        def span(fn, reps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            for r in range(2):
+                fn(r)
+            e0.record(stream)
+            for r in range(reps):
+                work = fn(r)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            return work * reps / (e0.elapsed_time(e1) * 1e-3)
+        pblocks = 256 * 256                    # 256 blocks a CU: enough waves to saturate
+        pout = torch.empty(pblocks * bl.PROBE_THREADS, dtype=torch.int32, device=dev)
+        valu = span(lambda r: bl.bitlogic_probe_valu(pout, pblocks, 1024, r, stream), 5) / 1e12
+        cbytes = 1 << 30
+        csrc = torch.ones(cbytes, dtype=torch.uint8, device=dev)
+        cdst = torch.empty_like(csrc)
+        copy = span(lambda r: bl.bitlogic_probe_copy(csrc, cdst, stream), 5) / 1e9
+        del pout, csrc, cdst
+        peaks = {"valu_TOPs": round(valu, 3),
+                 "valu_frac_of_published": round(valu / PEAK_VALU_TOPS, 4),
+                 "copy_GBs": round(copy, 1),
+                 "probes": "bitlogic_probe_valu (65536 x 256 lanes, 1024 rounds of 8 v_bitop3_b32) "
+                           "and bitlogic_probe_copy (1 GiB, read + write counted)"}
+        print(f"[bench] measured peaks: {valu:.2f} T int32 lane-ops/s, copy {copy:.0f} GB/s",
+              file=sys.stderr, flush=True)
     if whole:
         # one kernel runs every stage: a single launch between the first two events
         stage_ms = {"network": float(sum(stage_ms.values()))}
@@ -361,6 +401,11 @@ def main():
         "fit_quantile_thresholds": fit_detail,
         "layer_frac_of_valu_peak": {k: round(alg[k]["ops"] / (stage_ms[k] * 1e-3) / 1e12
                                              / PEAK_VALU_TOPS, 4) for k in layer_names},
+        "measured_peaks": peaks,
+        "dominant_frac_of_measured_peak": (
+            None if peaks is None else
+            round(achieved / (peaks["valu_TOPs"] if a["bound"] == "alu" else peaks["copy_GBs"]),
+                  4)),
         "gpu": torch.cuda.get_device_name(dev),
         "hip": torch.version.hip,
     }

@@ -373,6 +373,26 @@ int bitlogic_network_forward(const bitlogic_network *net, const uint8_t *x, int6
                              size_t workspace_bytes, void *stream, void *const *events,
                              int32_t n_events);
 
+/* ---- Peak probes (measurement, not part of the inference path) ---------- */
+
+/* Integer VALU probe: `blocks` blocks of 256 lanes.  Lane l (global index)
+ * starts from 8 words a[c] = (l + 1) * 0x9E3779B1 ^ (seed + c) * 0x85EBCA77
+ * (32-bit wrap-around), runs `iters` rounds of
+ *     for c = 0..7:  s = a[(c + 1) % 8];  a[c] = (s & a[c]) | (~s & a[(c + 2) % 8])
+ * (each one v_bitop3_b32, the multiplexer of the LUT layers) and writes the XOR of
+ * its 8 words to out[l].  A call performs blocks * 256 * iters * 8 32-bit
+ * lane-ops; timing it on `stream` gives the sustained integer VALU rate.
+ *   out  uint32 [blocks * 256], device memory; blocks >= 1, iters >= 0. */
+int bitlogic_probe_valu(uint32_t *out, int32_t blocks, int32_t iters, uint32_t seed,
+                        void *stream);
+
+/* Streaming copy probe: out[0, n_bytes) = in[0, n_bytes) with 16-byte
+ * non-temporal loads and stores (2 * n_bytes of HBM traffic).  n_bytes >= 0 a
+ * multiple of 16 (0 enqueues nothing, NULL buffers allowed); both buffers
+ * 16-byte aligned device memory that do not overlap (BITLOGIC_ERR_SHAPE
+ * otherwise). */
+int bitlogic_probe_copy(const void *in, void *out, int64_t n_bytes, void *stream);
+
 /* Static description of a status code. */
 const char *bitlogic_status_string(int status);
 

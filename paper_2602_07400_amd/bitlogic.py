@@ -106,6 +106,8 @@ def load_library():
         "bitlogic_specialize_layer": ([P, P, i32, i32, i32, P, P, P], ctypes.c_int),
         "bitlogic_specialize_network": ([i32, P, P, P, P, i32, i32, ctypes.c_double, P, P, P,
                                          P, P, P], ctypes.c_int),
+        "bitlogic_probe_valu": ([P, i32, i32, ctypes.c_uint32, P], ctypes.c_int),
+        "bitlogic_probe_copy": ([P, P, i64, P], ctypes.c_int),
         "bitlogic_status_string": ([ctypes.c_int], ctypes.c_char_p),
         "bitlogic_last_error": ([], ctypes.c_char_p),
         "bitlogic_version": ([], ctypes.c_int),
@@ -622,3 +624,35 @@ def bitlogic_network_forward(model: BitlogicModel, x: torch.Tensor,
         _dev(out, "out", _I32) if out is not None else None, _dev(argmax, "argmax", _I32),
         ws_ptr, ws_bytes, _stream(stream, dev), ev_ptr, n_ev))
     return out, argmax
+
+
+# ---------------------------------------------------------------- peak probes
+
+PROBE_THREADS = 256
+PROBE_CHAINS = 8
+
+
+def bitlogic_probe_valu(out: torch.Tensor, blocks: int, iters: int, seed: int = 0,
+                        stream=None) -> int:
+    """Integer VALU probe into out (int32 [blocks * 256] on the GPU); returns
+    the number of 32-bit lane-ops it performs (blocks * 256 * iters * 8)."""
+    if out.numel() < blocks * PROBE_THREADS:
+        raise ValueError("out needs blocks * 256 words")
+    _check(load_library().bitlogic_probe_valu(_dev(out, "out", _I32), int(blocks), int(iters),
+                                              int(seed) & 0xFFFFFFFF,
+                                              _stream(stream, out.device)))
+    return int(blocks) * PROBE_THREADS * int(iters) * PROBE_CHAINS
+
+
+def bitlogic_probe_copy(src: torch.Tensor, dst: torch.Tensor, stream=None) -> int:
+    """Streaming copy probe of src into dst (same byte size, a multiple of 16);
+    returns the bytes moved (read + written)."""
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != nbytes:
+        raise ValueError("src and dst differ in size")
+    for t, name in ((src, "src"), (dst, "dst")):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous GPU tensor")
+    _check(load_library().bitlogic_probe_copy(src.data_ptr(), dst.data_ptr(), nbytes,
+                                              _stream(stream, src.device)))
+    return 2 * nbytes

@@ -14,7 +14,7 @@ LIB = os.path.join(HERE, "libbitlogic.so")
 OBJ_DIR = os.path.join(HERE, "_build")
 
 SOURCES = ["encode.hip", "lut_layer.hip", "head.hip", "fit.hip", "net_fused.hip", "specialize.hip",
-           "api.hip"]
+           "probes.hip", "api.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -695,4 +695,35 @@ const char *bitlogic_last_error(void) { return g_last_error; }
 
 int bitlogic_version(void) { return BITLOGIC_VERSION; }
 
+int bitlogic_probe_valu(uint32_t *out, int32_t blocks, int32_t iters, uint32_t seed,
+                        void *stream)
+{
+    if (!out)
+        return fail(BITLOGIC_ERR_NULL, "probe_valu: NULL output");
+    if (blocks < 1 || iters < 0)
+        return fail(BITLOGIC_ERR_SHAPE, "probe_valu: need blocks >= 1, iters >= 0");
+    if (!aligned(out, 4))
+        return fail(BITLOGIC_ERR_ALIGN, "probe_valu: output not 4-byte aligned");
+    return hip_status(bl::launch_probe_valu(out, blocks, iters, seed, (hipStream_t)stream),
+                      "probe_valu launch");
+}
+
+int bitlogic_probe_copy(const void *in, void *out, int64_t n_bytes, void *stream)
+{
+    if (n_bytes == 0)
+        return ok();
+    if (!in || !out)
+        return fail(BITLOGIC_ERR_NULL, "probe_copy: NULL buffer");
+    if (n_bytes < 0 || n_bytes % 16 != 0)
+        return fail(BITLOGIC_ERR_SHAPE, "probe_copy: n_bytes %lld not a multiple of 16",
+                    (long long)n_bytes);
+    if (!aligned(in, 16) || !aligned(out, 16))
+        return fail(BITLOGIC_ERR_ALIGN, "probe_copy: buffers not 16-byte aligned");
+    const char *a = static_cast<const char *>(in), *b = static_cast<const char *>(out);
+    if (a < b + n_bytes && b < a + n_bytes)
+        return fail(BITLOGIC_ERR_SHAPE, "probe_copy: buffers overlap");
+    return hip_status(bl::launch_probe_copy(in, out, n_bytes, (hipStream_t)stream),
+                      "probe_copy launch");
+}
+
 }  // extern "C"

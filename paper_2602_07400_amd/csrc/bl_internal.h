@@ -157,4 +157,9 @@ hipError_t launch_net_fused(const uint8_t *x, int64_t n, int32_t d, const uint8_
                             const NetPlan &plan, int32_t *scores, int32_t *argmax,
                             hipStream_t stream);
 
+// Peak probes (probes.hip): kProbeThreads = 256 lanes a block.
+hipError_t launch_probe_valu(uint32_t *out, int32_t blocks, int32_t iters, uint32_t seed,
+                             hipStream_t stream);
+hipError_t launch_probe_copy(const void *in, void *out, int64_t n_bytes, hipStream_t stream);
+
 }  // namespace bl

@@ -363,3 +363,18 @@ def test_pass_fanin_plan(lib, monkeypatch):
     net.pass_fanin = ctypes.cast(arr, ctypes.c_void_p)
     assert lib.bitlogic_network_plan(ctypes.byref(net), 4096, ref) == OK
     assert info.fused_network == 0
+
+
+def test_probe_validation(lib):
+    assert lib.bitlogic_probe_valu(None, 1, 1, 0, None) == ENULL
+    assert lib.bitlogic_probe_valu(FAKE, 0, 1, 0, None) == ESHAPE
+    assert lib.bitlogic_probe_valu(FAKE, 1, -1, 0, None) == ESHAPE
+    assert lib.bitlogic_probe_valu(FAKE + 2, 1, 1, 0, None) == EALIGN
+    assert lib.bitlogic_probe_copy(None, FAKE, 16, None) == ENULL
+    assert lib.bitlogic_probe_copy(FAKE, FAKE * 4, 24, None) == ESHAPE
+    assert lib.bitlogic_probe_copy(FAKE, FAKE * 4, -16, None) == ESHAPE
+    assert lib.bitlogic_probe_copy(FAKE + 8, FAKE * 4, 16, None) == EALIGN
+    assert lib.bitlogic_probe_copy(FAKE, FAKE + 16, 64, None) == ESHAPE      # overlap
+    assert "overlap" in _err(lib)
+    assert lib.bitlogic_probe_copy(FAKE, FAKE * 4, 0, None) == OK
+
