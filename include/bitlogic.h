@@ -402,8 +402,8 @@ const char *bitlogic_last_error(void);
 /* Library version, major * 10000 + minor * 100 + patch.  A caller built
  * against this header can check bitlogic_version() == BITLOGIC_VERSION
  * before using the structs above (0.3.0 added bitlogic_network.pass_fanin and
- * the specialization calls). */
-#define BITLOGIC_VERSION 300
+ * the specialization calls; 0.4.0 the peak probes). */
+#define BITLOGIC_VERSION 400
 int bitlogic_version(void);
 
 #ifdef __cplusplus
