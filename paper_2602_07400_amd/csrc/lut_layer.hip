@@ -265,6 +265,16 @@ __device__ __forceinline__ int pass_fanin(const uint8_t *fanin, int32_t n_fanin,
 #ifndef BL_LUT_MINWAVES
 #define BL_LUT_MINWAVES 1
 #endif
+// Up to 4 inputs, the slab kernel loads the next pass's rows while it
+// evaluates the current pass (two register sets; C5 layer 1: k = 2 0.69 ->
+// 0.665 ms, k = 4 0.84 -> 0.81 ms).  At 5 and 6 inputs the second set would
+// cost occupancy: 4 lanes a node with prefetch need ~170 VGPRs (C4 layer 1
+// 1.23 -> 1.63 ms), 8 lanes with prefetch ran 1.34 ms.
+template <int K>
+constexpr bool slab_prefetch()
+{
+    return K <= 4;
+}
 
 template <int K, int S, int LPN, int NB, bool SPEC>
 __global__ __launch_bounds__(kThreads, BL_LUT_MINWAVES) void k_lut_slab(
@@ -300,6 +310,27 @@ __global__ __launch_bounds__(kThreads, BL_LUT_MINWAVES) void k_lut_slab(
     uint64_t *dst = out + ((int64_t)slab * w_out + node0) * S + sub * R;
     const int npass = (nodes + kPassNodes - 1) / kPassNodes;
 
+    if constexpr (!SPEC && slab_prefetch<K>()) {
+        // two register sets: the next pass's rows are in flight while this
+        // pass is evaluated
+        uint32_t xa[2 * R][K], xb[2 * R][K];
+        if (npass > 0)
+            gather<K, R>(src, &s_conn[lnode * K], S, xa);
+#pragma unroll 1
+        for (int pass = 0; pass < npass; pass += 2) {
+            const int jl = pass * kPassNodes + lnode;
+            const int jl1 = jl + kPassNodes;
+            if (pass + 1 < npass)
+                gather<K, R>(src, &s_conn[jl1 * K], S, xb);
+            eval_store<K, R>(s_tab[jl], xa, dst + (int64_t)jl * S, jl < nodes);
+            if (pass + 1 < npass) {
+                if (pass + 2 < npass)
+                    gather<K, R>(src, &s_conn[(jl1 + kPassNodes) * K], S, xa);
+                eval_store<K, R>(s_tab[jl1], xb, dst + (int64_t)jl1 * S, jl1 < nodes);
+            }
+        }
+        return;
+    }
 #pragma unroll 1
     for (int pass = 0; pass < npass; ++pass) {
         const int jl = pass * kPassNodes + lnode;
