@@ -62,6 +62,8 @@ ENC_CASES = [
     (2048, 3072, 3, "random"),
     (777, 33, 64, "random"),                 # b at its maximum
     (64 * 16 * 2, 64, 8, "zero"),            # the quantile collapse: all thresholds 0
+    (64 * 16 + 3, 96, 7, "random"),          # 32-feature tiles read as 16-byte pieces
+    (64 * 5, 200, 3, "random"),              # 64-feature tiles, ragged last tile
 ]
 
 
@@ -85,6 +87,21 @@ def test_encode_parity(n, d, b, kind):
     ref = oracle.encode(x, th)
     assert np.array_equal(got[:n], ref), _report("encode", got[:n], ref)
     assert not got[n:].any(), "padding bits must be 0"
+
+
+@pytest.mark.parametrize("b", [3, 7, 8])
+def test_encode_dword_aligned_rows(b):
+    """Rows 4-byte but not 16-byte aligned take the dword loads, not the
+    16-byte ones."""
+    rng = np.random.default_rng(50 + b)
+    n, d = 64 * 16 + 9, 128
+    big = rng.integers(0, 256, size=n * d + 16, dtype=np.uint8)
+    xt = to_dev(big)[4:4 + n * d].view(n, d)
+    assert xt.data_ptr() % 4 == 0 and xt.data_ptr() % 16 != 0
+    th = rng.integers(0, 256, size=(d, b), dtype=np.uint8)
+    bits = bl.bitlogic_encode(xt, to_dev(th))
+    ref = oracle.encode(big[4:4 + n * d].reshape(n, d), th)
+    assert np.array_equal(unpack(bits, n), ref)
 
 
 def test_encode_unaligned_rows():
