@@ -419,8 +419,8 @@ hipError_t launch_slab_k(const uint64_t *in, int32_t w_in, int64_t n_slabs,
 // short: its padding nodes get connections 0 and a constant-0 table, so they
 // evaluate to 0 and add nothing to the counters.  A C4 class group of 640
 // nodes is one block, so the finish reads one counter per class.  The kernel
-// is held to 128 VGPRs (4 waves per SIMD; at K = 6 the compiler spills 4
-// dwords).
+// is held to 128 VGPRs (4 waves per SIMD; it takes 126 at K = 6, with no
+// spills).
 #ifndef BL_HEAD_CP
 #define BL_HEAD_CP 4
 #endif
