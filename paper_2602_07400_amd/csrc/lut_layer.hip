@@ -262,9 +262,10 @@ __device__ __forceinline__ int pass_fanin(const uint8_t *fanin, int32_t n_fanin,
     return __builtin_amdgcn_readfirstlane(min(kp, K));
 }
 
-// The next pass's gathers issue at a raised wave priority (as in the fused
-// last layer below): C5 layer 1 at k = 4 0.81 -> 0.79 ms, k = 2 0.665 ->
-// 0.661 ms in alternating runs.
+// The next pass's gathers issue at a raised wave priority, so that they
+// leave ahead of other waves' evaluation: C5 layer 1 at k = 4 0.807 -> 0.786
+// ms, k = 2 0.665 -> 0.660 ms (ABBA runs on one set of buffers).  The
+// memory clobbers keep the loads between the two s_setprio.
 #ifndef BL_PF_SETPRIO
 #define BL_PF_SETPRIO 1
 #endif
@@ -440,9 +441,6 @@ hipError_t launch_slab_k(const uint64_t *in, int32_t w_in, int64_t n_slabs,
 #ifndef BL_HEAD_CP
 #define BL_HEAD_CP 4
 #endif
-#ifndef BL_HEAD_SETPRIO
-#define BL_HEAD_SETPRIO 1
-#endif
 #ifndef BL_HEAD_MINWAVES
 #define BL_HEAD_MINWAVES 4
 #endif
@@ -560,17 +558,8 @@ __global__ __launch_bounds__(kThreads, BL_HEAD_MINWAVES) void k_lut_slab_head(
                                                          node0 + pass * kHeadPassNodes);
             spec_eval<0, K, kHeadR>(kp, src, &s_conn[jl * K], kSlabWords, s_tab[jl], o);
         } else {
-            // The gathers issue at a raised wave priority, so that a wave
-            // starting its pass gets its loads out ahead of the waves that
-            // are evaluating (layer 2 4-8% faster on the k = 6 workloads;
-            // the same bracket made the plain layer kernel slower).  The
-            // memory clobbers keep the loads between the two.
             uint32_t xv[2 * kHeadR][K];
-            if (BL_HEAD_SETPRIO)
-                asm volatile("s_setprio 2" ::: "memory");
             gather<K, kHeadR>(src, &s_conn[jl * K], kSlabWords, xv);
-            if (BL_HEAD_SETPRIO)
-                asm volatile("s_setprio 0" ::: "memory");
             eval_node<K, kHeadR>(s_tab[jl], xv, o);
         }
 #pragma unroll
