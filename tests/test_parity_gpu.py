@@ -6,7 +6,7 @@ counts that are not whole node blocks, repeated connection indices, junk
 table bits above 2^k, threshold edge values, unaligned pixel rows, and head
 groups from 1 node to thousands (split counters).  Whole-network cases run
 every configuration at a reduced batch (several windows plus a ragged tail)
-and at its full batch, where the oracle checks a sample of rows.
+and at its full batch, every sample against the oracle.
 """
 import os
 
@@ -263,17 +263,40 @@ def test_forward_reduced_batch(name):
 
 
 @pytest.mark.parametrize("name", CONFIG_ORDER)
-def test_forward_full_batch_sampled(name):
+def test_forward_full_batch(name):
+    # every sample of the configuration's full batch against the oracle
+    # (App. C.1 "Correctness anchor": the packed path equals the per-sample one)
     cfg = CONFIGS[name]
     wl = make_workload(name, seed=0)
-    rng = np.random.default_rng(99)
-    if cfg.n <= 4096:
-        idx = None                      # the oracle checks every sample
-    else:
-        idx = np.unique(np.concatenate([np.arange(64), np.arange(cfg.n - 64, cfg.n),
-                                        rng.choice(cfg.n, size=1024, replace=False)]))
-    print(f"[full] {name}: n={cfg.n} sampled={None if idx is None else idx.size}", flush=True)
-    _check_forward(wl, idx)
+    assert wl.n == cfg.n
+    print(f"[full] {name}: n={cfg.n}, every sample", flush=True)
+    _check_forward(wl)
+
+
+def test_forward_hidden_layers_with_partial_node_blocks():
+    # hidden layers of up to 4 inputs in the 512-node-block mode (>= 2048
+    # blocks) whose widths are not whole blocks: 8096 nodes at k = 4 leave a
+    # last block of 13 passes (an odd count: the two-register-set loop ends
+    # on its first set); 8100 nodes at k = 2 leave a last block of 14 passes
+    # whose last pass holds 4 nodes and 28 padding lanes
+    rng = np.random.default_rng(31)
+    n, d, b = 1 << 18, 784, 2
+    x = rng.integers(0, 256, size=(n, d), dtype=np.uint8)
+    th = np.sort(rng.integers(0, 256, size=(d, b), dtype=np.uint8), axis=1)
+    layers, w_in = [], d * b
+    for w, k in ((8096, 4), (8100, 2), (8000, 6)):
+        conn = np.stack([rng.choice(w_in, size=k, replace=False) for _ in range(w)]).astype(np.int32)
+        tab = rng.integers(0, 2**64, size=w, dtype=np.uint64)
+        layers.append((conn, tab))
+        w_in = w
+    model = bl.BitlogicModel.from_numpy(th, layers, 10, device=DEV)
+    xd = torch.from_numpy(x).to(DEV)
+    scores, argmax = model.forward(xd)
+    torch.cuda.synchronize()
+    ref_s, ref_p = oracle.forward(x, th, layers, 10)
+    got_s, got_p = scores.cpu().numpy(), argmax.cpu().numpy()
+    assert np.array_equal(got_s, ref_s), _report("scores", got_s, ref_s)
+    assert np.array_equal(got_p, ref_p), _report("argmax", got_p, ref_p)
 
 
 def test_forward_matches_staged_calls_and_is_deterministic():

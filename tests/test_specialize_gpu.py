@@ -141,14 +141,11 @@ def test_specialized_unique_routing_matches_unspecialized():
     assert m.pass_fanin is None
 
 
-def test_collapsed_workload_full_batch_sampled():
+def test_collapsed_workload_full_batch():
     cfg = CONFIGS["c4_collapsed"]
     wl = make_workload("c4_collapsed")
-    rng = np.random.default_rng(5)
-    idx = np.unique(np.concatenate([np.arange(64), np.arange(cfg.n - 64, cfg.n),
-                                    rng.choice(cfg.n, size=512, replace=False)]))
-    print(f"[spec-full] c4_collapsed n={cfg.n} sampled={idx.size}", flush=True)
-    m = _check(wl.x, wl.thresholds, wl.layers, wl.n_classes, True, sample=idx)
+    print(f"[spec-full] c4_collapsed n={cfg.n}, every sample", flush=True)
+    m = _check(wl.x, wl.thresholds, wl.layers, wl.n_classes, True)
     for h in m.fanin_histogram:
         assert h[4:].sum() == 0                      # at most 3 distinct wires per node
     assert all(layer[0].shape[1] == 3 for layer in m.layers)
