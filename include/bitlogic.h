@@ -373,6 +373,33 @@ int bitlogic_network_forward(const bitlogic_network *net, const uint8_t *x, int6
                              size_t workspace_bytes, void *stream, void *const *events,
                              int32_t n_events);
 
+/* ---- Forward without allocation ----------------------------------------
+ * For callers that cannot allocate device memory or hand in a workspace:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Computes exactly what bitlogic_network_forward computes (same
+ * kernels, same results), but its scratch is a static device array inside
+ * the library, BITLOGIC_NOALLOC_SCRATCH_BYTES per GPU, which each GPU the
+ * library runs on holds from load until the process ends.  The call makes no
+ * hipMalloc, hipFree or other allocating call.
+ *   net, x, n_samples, out, argmax, stream: as bitlogic_network_forward
+ *   (out and argmax are the caller's device buffers; no events).
+ * Errors: as bitlogic_network_forward, plus
+ *   BITLOGIC_ERR_WORKSPACE    bitlogic_network_workspace_bytes(net, n_samples)
+ *                             exceeds BITLOGIC_NOALLOC_SCRATCH_BYTES (nothing
+ *                             is enqueued; split the batch or use
+ *                             bitlogic_network_forward);
+ *   BITLOGIC_ERR_UNSUPPORTED  `stream` belongs to another device than the
+ *                             current one.
+ * All calls on one GPU share that GPU's array, which keeps the previous
+ * call's contents (every byte a call reads it has written itself first).
+ * Calls that overlap in time on one GPU -- on different streams, or from
+ * threads that do not order them -- race on the array and their results are
+ * undefined; calls in order on one stream are safe. */
+#define BITLOGIC_NOALLOC_SCRATCH_BYTES (64u << 20)
+int bitlogic_network_forward_noalloc(const bitlogic_network *net, const uint8_t *x,
+                                     int64_t n_samples, int32_t *out, int32_t *argmax,
+                                     void *stream);
+
 /* ---- Peak probes (measurement, not part of the inference path) ---------- */
 
 /* Integer VALU probe: `blocks` blocks of 256 lanes.  Lane l (global index)
@@ -402,8 +429,9 @@ const char *bitlogic_last_error(void);
 /* Library version, major * 10000 + minor * 100 + patch.  A caller built
  * against this header can check bitlogic_version() == BITLOGIC_VERSION
  * before using the structs above (0.3.0 added bitlogic_network.pass_fanin and
- * the specialization calls; 0.4.0 the peak probes). */
-#define BITLOGIC_VERSION 400
+ * the specialization calls; 0.4.0 the peak probes; 0.5.0
+ * bitlogic_network_forward_noalloc). */
+#define BITLOGIC_VERSION 500
 int bitlogic_version(void);
 
 #ifdef __cplusplus

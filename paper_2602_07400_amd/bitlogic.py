@@ -24,6 +24,7 @@ __all__ = [
     "bitlogic_forward", "bitlogic_forward_timed", "bitlogic_forward_workspace_bytes",
     "bitlogic_forward_plan", "bitlogic_grouped_dsp_head", "bitlogic_forward_grouped_dsp",
     "bitlogic_encode_binary", "bitlogic_fit_quantile_thresholds", "bitlogic_network_forward",
+    "bitlogic_network_forward_noalloc", "NOALLOC_SCRATCH_BYTES",
     "bitlogic_groupsum_head_workspace_bytes", "bitlogic_status_string", "bitlogic_version",
     "BitlogicModel", "bitlogic_specialize_layer", "bitlogic_specialize_network", "library_path",
     "load_library", "words",
@@ -98,6 +99,7 @@ def load_library():
         "bitlogic_network_workspace_bytes": ([P, i64], sz),
         "bitlogic_network_plan": ([P, i64, P], ctypes.c_int),
         "bitlogic_network_forward": ([P, P, i64, P, P, P, sz, P, P, i32], ctypes.c_int),
+        "bitlogic_network_forward_noalloc": ([P, P, i64, P, P, P], ctypes.c_int),
         "bitlogic_forward_grouped_dsp": ([P, i64, i32, P, i32, P, i32, i32, P, P, P, P, sz, P],
                                          ctypes.c_int),
         "bitlogic_forward": ([P, i64, i32, P, i32, P, i32, i32, P, P, P, sz, P], ctypes.c_int),
@@ -623,6 +625,28 @@ def bitlogic_network_forward(model: BitlogicModel, x: torch.Tensor,
         ctypes.byref(net), _dev(x, "x", _U8), n,
         _dev(out, "out", _I32) if out is not None else None, _dev(argmax, "argmax", _I32),
         ws_ptr, ws_bytes, _stream(stream, dev), ev_ptr, n_ev))
+    return out, argmax
+
+
+# bitlogic_network_forward_noalloc's static scratch per GPU (the header's
+# BITLOGIC_NOALLOC_SCRATCH_BYTES)
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def bitlogic_network_forward_noalloc(model: BitlogicModel, x: torch.Tensor, out: torch.Tensor,
+                                     argmax: torch.Tensor, stream=None):
+    """Forward of a BitlogicModel through bitlogic_network_forward_noalloc: the
+    library's static scratch replaces the workspace.  out (int32 [N][c] or
+    None) and argmax (int32 [N] or None) are the caller's buffers; nothing is
+    allocated here or in the library."""
+    n, d = x.shape
+    if d != model.n_features:
+        raise ValueError(f"x has {d} features, the model {model.n_features}")
+    net, keep = model._net()
+    _check(load_library().bitlogic_network_forward_noalloc(
+        ctypes.byref(net), _dev(x, "x", _U8), n,
+        _dev(out, "out", _I32) if out is not None else None,
+        _dev(argmax, "argmax", _I32) if argmax is not None else None, _stream(stream, x.device)))
     return out, argmax
 
 

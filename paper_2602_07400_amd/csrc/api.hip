@@ -5,8 +5,17 @@
 #include <stdio.h>
 #include <stdlib.h>
 
+#include <atomic>
+#include <mutex>
+
 #include "bitlogic.h"
 #include "bl_internal.h"
+
+// Scratch of bitlogic_network_forward_noalloc: one copy of this array per GPU
+// the library runs on, held until the process ends.  In host code `scratch`
+// only names the symbol for hipGetSymbolAddress; the array's device address on
+// each GPU is looked up once and kept in g_scratch_ptr below.
+static __device__ __align__(256) unsigned char scratch[BITLOGIC_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -562,6 +571,82 @@ int bitlogic_network_forward(const bitlogic_network *net, const uint8_t *x, int6
 {
     return forward_impl(net, x, n_samples, out, argmax, workspace, workspace_bytes, stream,
                         events, events ? n_events : 0);
+}
+
+}  // extern "C"
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::atomic<void *> g_scratch_ptr[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// Device address of `scratch` on device dev (the current device), looked up
+// on the first call for that device.
+int scratch_address(int dev, void **ptr)
+{
+    void *p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+        if (!p) {
+            hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+            if (e != hipSuccess || !p)
+                return fail(BITLOGIC_ERR_HIP, "forward_noalloc: scratch address on device %d: %s",
+                            dev, hipGetErrorString(e));
+            g_scratch_ptr[dev].store(p, std::memory_order_release);
+        }
+    }
+    *ptr = p;
+    return BITLOGIC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int bitlogic_network_forward_noalloc(const bitlogic_network *net, const uint8_t *x,
+                                     int64_t n_samples, int32_t *out, int32_t *argmax,
+                                     void *stream)
+{
+    // every argument check before the first HIP call
+    ForwardPlan fp;
+    int st = plan_network(net, n_samples, &fp);
+    if (st != BITLOGIC_OK)
+        return st;
+    if (!x || (!out && !argmax))
+        return fail(BITLOGIC_ERR_NULL, "forward_noalloc: NULL pixels or both outputs NULL");
+    if ((out && !aligned(out, 4)) || (argmax && !aligned(argmax, 4)))
+        return fail(BITLOGIC_ERR_ALIGN, "forward_noalloc: misaligned output");
+    if (fp.total > (size_t)BITLOGIC_NOALLOC_SCRATCH_BYTES)
+        return fail(BITLOGIC_ERR_WORKSPACE,
+                    "forward_noalloc: %lld samples need %zu bytes of scratch, the static buffer "
+                    "holds %zu (use bitlogic_network_forward with a workspace)",
+                    (long long)n_samples, fp.total, (size_t)BITLOGIC_NOALLOC_SCRATCH_BYTES);
+    if (n_samples == 0)
+        return ok();
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return hip_status(e, "forward_noalloc: current device");
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(BITLOGIC_ERR_UNSUPPORTED, "forward_noalloc: device %d beyond %d", dev,
+                    kMaxDevices);
+    if (stream) {
+        hipDevice_t sdev = 0;
+        e = hipStreamGetDevice((hipStream_t)stream, &sdev);
+        if (e != hipSuccess)
+            return hip_status(e, "forward_noalloc: stream device");
+        if (sdev != dev)
+            return fail(BITLOGIC_ERR_UNSUPPORTED,
+                        "forward_noalloc: stream of device %d, current device %d", (int)sdev, dev);
+    }
+    void *ws = nullptr;
+    st = scratch_address(dev, &ws);
+    if (st != BITLOGIC_OK)
+        return st;
+    return forward_impl(net, x, n_samples, out, argmax, ws, BITLOGIC_NOALLOC_SCRATCH_BYTES,
+                        stream, nullptr, 0);
 }
 
 int bitlogic_encode_binary(const uint8_t *x, int64_t n_samples, int32_t n_features,

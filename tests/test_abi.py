@@ -312,6 +312,29 @@ def test_network_validation(lib):
     assert info.workspace_bytes == ws(_net(p))
 
 
+def test_network_noalloc_validation(lib):
+    p, keep = _layers([(1000, 6), (1000, 6)])
+    fwd = lambda net, **o: lib.bitlogic_network_forward_noalloc(
+        ctypes.byref(net) if net is not None else None, o.get("x", FAKE), o.get("n", 4096),
+        o.get("out", FAKE), o.get("am", FAKE), None)
+    assert fwd(None) == ENULL
+    assert fwd(_net(p), x=None) == ENULL
+    assert fwd(_net(p), out=None, am=None) == ENULL
+    assert fwd(_net(p), out=FAKE + 2) == EALIGN
+    assert fwd(_net(p, enc=2)) == EUNSUP
+    # the static scratch bounds the batch: rejected before any HIP call
+    cap = bl.NOALLOC_SCRATCH_BYTES
+    ws = lambda n: lib.bitlogic_network_workspace_bytes(ctypes.byref(_net(p)), n)
+    big = 64
+    while ws(big) <= cap:
+        big *= 2
+    assert fwd(_net(p), n=big) == EWS
+    assert "static buffer" in _err(lib)
+    assert fwd(_net(p), n=0) == OK
+    hdr = open(HEADER).read()
+    assert re.search(r"#define BITLOGIC_NOALLOC_SCRATCH_BYTES \(64u << 20\)", hdr)
+
+
 def test_whole_network_plan(lib, monkeypatch):
     info = bl._ForwardInfo()
     ref = ctypes.byref(info)
