@@ -270,17 +270,36 @@ def main():
         pblocks = 256 * 256                    # 256 blocks a CU: enough waves to saturate
         pout = torch.empty(pblocks * bl.PROBE_THREADS, dtype=torch.int32, device=dev)
         valu = span(lambda r: bl.bitlogic_probe_valu(pout, pblocks, 1024, r, stream), 5) / 1e12
-        cbytes = 1 << 30
+        # HBM streams of 4 GiB: read-only, write-only and copy, each at a few
+        # loads-in-flight depths and grid sizes; the best of each is reported
+        cbytes = 4 << 30
         csrc = torch.ones(cbytes, dtype=torch.uint8, device=dev)
         cdst = torch.empty_like(csrc)
-        copy = span(lambda r: bl.bitlogic_probe_copy(csrc, cdst, stream), 5) / 1e9
+        hbm = {}
+        for mode, tag in ((bl.PROBE_HBM_READ, "read"), (bl.PROBE_HBM_WRITE, "write"),
+                          (bl.PROBE_HBM_COPY, "copy")):
+            best = None
+            for unroll, blocks in ((4, 256 * 8), (8, 256 * 4), (8, 256 * 8), (2, 256 * 16)):
+                src = None if mode == bl.PROBE_HBM_WRITE else csrc
+                rate = span(lambda r: bl.bitlogic_probe_hbm(mode, src, cdst, cbytes, unroll,
+                                                            blocks, stream), 5) / 1e9
+                if best is None or rate > best[0]:
+                    best = (rate, unroll, blocks)
+            hbm[tag] = best
         del pout, csrc, cdst
         peaks = {"valu_TOPs": round(valu, 3),
                  "valu_frac_of_published": round(valu / PEAK_VALU_TOPS, 4),
-                 "copy_GBs": round(copy, 1),
-                 "probes": "bitlogic_probe_valu (65536 x 256 lanes, 1024 rounds of 8 v_bitop3_b32) "
-                           "and bitlogic_probe_copy (1 GiB, read + write counted)"}
-        print(f"[bench] measured peaks: {valu:.2f} T int32 lane-ops/s, copy {copy:.0f} GB/s",
+                 "hbm_read_GBs": round(hbm["read"][0], 1),
+                 "hbm_write_GBs": round(hbm["write"][0], 1),
+                 "hbm_copy_GBs": round(hbm["copy"][0], 1),
+                 "hbm_read_frac_of_published": round(hbm["read"][0] / PEAK_HBM_GBS, 4),
+                 "probes": "bitlogic_probe_valu (65536 x 256 lanes, 1024 rounds of 8 v_bitop3_b32); "
+                           "bitlogic_probe_hbm over 4 GiB, best of (unroll, blocks) in "
+                           "(4, 2048), (8, 1024), (8, 2048), (2, 4096): "
+                           + ", ".join(f"{t} unroll {u} blocks {b}" for t, (_, u, b) in hbm.items())
+                           + " (copy counts read + write)"}
+        print(f"[bench] measured peaks: {valu:.2f} T int32 lane-ops/s, HBM read "
+              f"{hbm['read'][0]:.0f} / write {hbm['write'][0]:.0f} / copy {hbm['copy'][0]:.0f} GB/s",
               file=sys.stderr, flush=True)
     if whole:
         # one kernel runs every stage: a single launch between the first two events
@@ -404,8 +423,9 @@ def main():
         "measured_peaks": peaks,
         "dominant_frac_of_measured_peak": (
             None if peaks is None else
-            round(achieved / (peaks["valu_TOPs"] if a["bound"] == "alu" else peaks["copy_GBs"]),
-                  4)),
+            round(achieved / (peaks["valu_TOPs"] if a["bound"] == "alu" else
+                              max(peaks["hbm_read_GBs"], peaks["hbm_write_GBs"],
+                                  peaks["hbm_copy_GBs"])), 4)),
         "gpu": torch.cuda.get_device_name(dev),
         "hip": torch.version.hip,
     }

@@ -413,12 +413,26 @@ int bitlogic_network_forward_noalloc(const bitlogic_network *net, const uint8_t 
 int bitlogic_probe_valu(uint32_t *out, int32_t blocks, int32_t iters, uint32_t seed,
                         void *stream);
 
-/* Streaming copy probe: out[0, n_bytes) = in[0, n_bytes) with 16-byte
- * non-temporal loads and stores (2 * n_bytes of HBM traffic).  n_bytes >= 0 a
- * multiple of 16 (0 enqueues nothing, NULL buffers allowed); both buffers
- * 16-byte aligned device memory that do not overlap (BITLOGIC_ERR_SHAPE
- * otherwise). */
-int bitlogic_probe_copy(const void *in, void *out, int64_t n_bytes, void *stream);
+/* HBM streaming probes over n_bytes (a multiple of 16) in 16-byte pieces,
+ * with non-temporal 16-byte loads and stores; a block of 256 lanes covers
+ * unroll * 256 consecutive pieces per step with its `unroll` loads in
+ * flight before any is used (unroll 1, 2, 4 or 8), over a grid of `blocks`
+ * blocks (0: 8 per CU) that strides over the buffer.  Modes:
+ *   BITLOGIC_PROBE_HBM_COPY   out[0, n_bytes) = in[0, n_bytes)    (2 n_bytes moved)
+ *   BITLOGIC_PROBE_HBM_READ   out[0, 16) = XOR of every 16-byte piece of in
+ *                             (n_bytes read; out is cleared first, so
+ *                             n_bytes = 0 gives 16 zero bytes)
+ *   BITLOGIC_PROBE_HBM_WRITE  piece i of out (bytes 16 i .. 16 i + 15) = the
+ *                             32-bit words (i, i >> 32, ~i, ~(i >> 32)),
+ *                             little-endian; `in` unused (n_bytes written)
+ * in, out: 16-byte aligned device memory; for COPY they must not overlap
+ * (BITLOGIC_ERR_SHAPE).  An unknown mode or unroll is
+ * BITLOGIC_ERR_UNSUPPORTED.  0 bytes enqueue nothing except READ's clear. */
+#define BITLOGIC_PROBE_HBM_COPY 0
+#define BITLOGIC_PROBE_HBM_READ 1
+#define BITLOGIC_PROBE_HBM_WRITE 2
+int bitlogic_probe_hbm(int32_t mode, const void *in, void *out, int64_t n_bytes,
+                       int32_t unroll, int32_t blocks, void *stream);
 
 /* Static description of a status code. */
 const char *bitlogic_status_string(int status);
@@ -430,7 +444,8 @@ const char *bitlogic_last_error(void);
  * against this header can check bitlogic_version() == BITLOGIC_VERSION
  * before using the structs above (0.3.0 added bitlogic_network.pass_fanin and
  * the specialization calls; 0.4.0 the peak probes; 0.5.0
- * bitlogic_network_forward_noalloc). */
+ * bitlogic_network_forward_noalloc, and bitlogic_probe_hbm in
+ * place of the copy-only probe). */
 #define BITLOGIC_VERSION 500
 int bitlogic_version(void);
 

@@ -109,7 +109,7 @@ def load_library():
         "bitlogic_specialize_network": ([i32, P, P, P, P, i32, i32, ctypes.c_double, P, P, P,
                                          P, P, P], ctypes.c_int),
         "bitlogic_probe_valu": ([P, i32, i32, ctypes.c_uint32, P], ctypes.c_int),
-        "bitlogic_probe_copy": ([P, P, i64, P], ctypes.c_int),
+        "bitlogic_probe_hbm": ([i32, P, P, i64, i32, i32, P], ctypes.c_int),
         "bitlogic_status_string": ([ctypes.c_int], ctypes.c_char_p),
         "bitlogic_last_error": ([], ctypes.c_char_p),
         "bitlogic_version": ([], ctypes.c_int),
@@ -668,15 +668,29 @@ def bitlogic_probe_valu(out: torch.Tensor, blocks: int, iters: int, seed: int = 
     return int(blocks) * PROBE_THREADS * int(iters) * PROBE_CHAINS
 
 
-def bitlogic_probe_copy(src: torch.Tensor, dst: torch.Tensor, stream=None) -> int:
-    """Streaming copy probe of src into dst (same byte size, a multiple of 16);
-    returns the bytes moved (read + written)."""
-    nbytes = src.numel() * src.element_size()
-    if dst.numel() * dst.element_size() != nbytes:
-        raise ValueError("src and dst differ in size")
+PROBE_HBM_COPY, PROBE_HBM_READ, PROBE_HBM_WRITE = 0, 1, 2
+
+
+def bitlogic_probe_hbm(mode: int, src: Optional[torch.Tensor], dst: torch.Tensor,
+                       nbytes: Optional[int] = None, unroll: int = 4, blocks: int = 0,
+                       stream=None) -> int:
+    """HBM streaming probe (include/bitlogic.h): copy src into dst, read src
+    (dst[0:16] receives the XOR of its 16-byte pieces) or write dst's
+    pattern; returns the HBM bytes it moves (read + written)."""
     for t, name in ((src, "src"), (dst, "dst")):
-        if not t.is_cuda or not t.is_contiguous():
+        if t is not None and (not t.is_cuda or not t.is_contiguous()):
             raise ValueError(f"{name} must be a contiguous GPU tensor")
-    _check(load_library().bitlogic_probe_copy(src.data_ptr(), dst.data_ptr(), nbytes,
-                                              _stream(stream, src.device)))
-    return 2 * nbytes
+    size = lambda t: t.numel() * t.element_size()
+    if nbytes is None:
+        nbytes = size(dst) if mode == PROBE_HBM_WRITE else size(src)
+    if mode != PROBE_HBM_WRITE and nbytes > size(src):
+        raise ValueError("src is smaller than nbytes")
+    if mode != PROBE_HBM_READ and nbytes > size(dst):
+        raise ValueError("dst is smaller than nbytes")
+    if mode == PROBE_HBM_READ and size(dst) < 16:
+        raise ValueError("the read probe writes 16 bytes")
+    dev = dst.device
+    _check(load_library().bitlogic_probe_hbm(
+        int(mode), src.data_ptr() if src is not None else None, dst.data_ptr(), int(nbytes),
+        int(unroll), int(blocks), _stream(stream, dev)))
+    return (2 if mode == PROBE_HBM_COPY else 1) * int(nbytes)

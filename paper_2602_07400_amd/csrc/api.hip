@@ -793,22 +793,43 @@ int bitlogic_probe_valu(uint32_t *out, int32_t blocks, int32_t iters, uint32_t s
                       "probe_valu launch");
 }
 
-int bitlogic_probe_copy(const void *in, void *out, int64_t n_bytes, void *stream)
+int bitlogic_probe_hbm(int32_t mode, const void *in, void *out, int64_t n_bytes,
+                       int32_t unroll, int32_t blocks, void *stream)
 {
+    if (mode != BITLOGIC_PROBE_HBM_COPY && mode != BITLOGIC_PROBE_HBM_READ &&
+        mode != BITLOGIC_PROBE_HBM_WRITE)
+        return fail(BITLOGIC_ERR_UNSUPPORTED, "probe_hbm: unknown mode %d", mode);
+    if (unroll != 1 && unroll != 2 && unroll != 4 && unroll != 8)
+        return fail(BITLOGIC_ERR_UNSUPPORTED, "probe_hbm: unroll %d not 1, 2, 4 or 8", unroll);
+    if (n_bytes < 0 || n_bytes % 16 != 0 || blocks < 0)
+        return fail(BITLOGIC_ERR_SHAPE, "probe_hbm: n_bytes %lld not a multiple of 16, or "
+                    "blocks < 0", (long long)n_bytes);
+    const bool reads = mode != BITLOGIC_PROBE_HBM_WRITE;
+    if (mode == BITLOGIC_PROBE_HBM_READ) {
+        if (!out || (n_bytes > 0 && !in))
+            return fail(BITLOGIC_ERR_NULL, "probe_hbm: NULL buffer");
+        if ((in && !aligned(in, 16)) || !aligned(out, 16))
+            return fail(BITLOGIC_ERR_ALIGN, "probe_hbm: buffers not 16-byte aligned");
+        return hip_status(bl::launch_probe_hbm(bl::kHbmRead, in, out, n_bytes, unroll, blocks,
+                                               (hipStream_t)stream),
+                          "probe_hbm launch");
+    }
     if (n_bytes == 0)
         return ok();
-    if (!in || !out)
-        return fail(BITLOGIC_ERR_NULL, "probe_copy: NULL buffer");
-    if (n_bytes < 0 || n_bytes % 16 != 0)
-        return fail(BITLOGIC_ERR_SHAPE, "probe_copy: n_bytes %lld not a multiple of 16",
-                    (long long)n_bytes);
-    if (!aligned(in, 16) || !aligned(out, 16))
-        return fail(BITLOGIC_ERR_ALIGN, "probe_copy: buffers not 16-byte aligned");
-    const char *a = static_cast<const char *>(in), *b = static_cast<const char *>(out);
-    if (a < b + n_bytes && b < a + n_bytes)
-        return fail(BITLOGIC_ERR_SHAPE, "probe_copy: buffers overlap");
-    return hip_status(bl::launch_probe_copy(in, out, n_bytes, (hipStream_t)stream),
-                      "probe_copy launch");
+    if (!out || (reads && !in))
+        return fail(BITLOGIC_ERR_NULL, "probe_hbm: NULL buffer");
+    if (!aligned(out, 16) || (reads && !aligned(in, 16)))
+        return fail(BITLOGIC_ERR_ALIGN, "probe_hbm: buffers not 16-byte aligned");
+    if (reads) {
+        const char *a = static_cast<const char *>(in), *b = static_cast<const char *>(out);
+        if (a < b + n_bytes && b < a + n_bytes)
+            return fail(BITLOGIC_ERR_SHAPE, "probe_hbm: buffers overlap");
+    }
+    return hip_status(bl::launch_probe_hbm(mode == BITLOGIC_PROBE_HBM_COPY ? bl::kHbmCopy
+                                                                            : bl::kHbmWrite,
+                                           in, out, n_bytes, unroll, blocks,
+                                           (hipStream_t)stream),
+                      "probe_hbm launch");
 }
 
 }  // extern "C"

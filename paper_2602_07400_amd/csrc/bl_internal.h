@@ -160,6 +160,10 @@ hipError_t launch_net_fused(const uint8_t *x, int64_t n, int32_t d, const uint8_
 // Peak probes (probes.hip): kProbeThreads = 256 lanes a block.
 hipError_t launch_probe_valu(uint32_t *out, int32_t blocks, int32_t iters, uint32_t seed,
                              hipStream_t stream);
-hipError_t launch_probe_copy(const void *in, void *out, int64_t n_bytes, hipStream_t stream);
+constexpr int kHbmCopy = 0;     // bitlogic_probe_hbm modes
+constexpr int kHbmRead = 1;
+constexpr int kHbmWrite = 2;
+hipError_t launch_probe_hbm(int32_t mode, const void *in, void *out, int64_t n_bytes,
+                            int32_t unroll, int32_t blocks, hipStream_t stream);
 
 }  // namespace bl

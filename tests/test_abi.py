@@ -393,11 +393,21 @@ def test_probe_validation(lib):
     assert lib.bitlogic_probe_valu(FAKE, 0, 1, 0, None) == ESHAPE
     assert lib.bitlogic_probe_valu(FAKE, 1, -1, 0, None) == ESHAPE
     assert lib.bitlogic_probe_valu(FAKE + 2, 1, 1, 0, None) == EALIGN
-    assert lib.bitlogic_probe_copy(None, FAKE, 16, None) == ENULL
-    assert lib.bitlogic_probe_copy(FAKE, FAKE * 4, 24, None) == ESHAPE
-    assert lib.bitlogic_probe_copy(FAKE, FAKE * 4, -16, None) == ESHAPE
-    assert lib.bitlogic_probe_copy(FAKE + 8, FAKE * 4, 16, None) == EALIGN
-    assert lib.bitlogic_probe_copy(FAKE, FAKE + 16, 64, None) == ESHAPE      # overlap
+    C, R, Wr = 0, 1, 2
+    hbm = lambda mode, i, o, n, u=4, b=0: lib.bitlogic_probe_hbm(mode, i, o, n, u, b, None)
+    assert hbm(3, FAKE, FAKE * 4, 16) == EUNSUP                # unknown mode
+    assert hbm(C, FAKE, FAKE * 4, 16, u=3) == EUNSUP           # unroll not 1, 2, 4, 8
+    assert hbm(C, None, FAKE, 16) == ENULL
+    assert hbm(C, FAKE, None, 16) == ENULL
+    assert hbm(R, FAKE, None, 16) == ENULL                      # the read probe writes 16 bytes
+    assert hbm(Wr, None, None, 16) == ENULL
+    assert hbm(C, FAKE, FAKE * 4, 24) == ESHAPE
+    assert hbm(C, FAKE, FAKE * 4, -16) == ESHAPE
+    assert hbm(C, FAKE, FAKE * 4, 16, b=-1) == ESHAPE
+    assert hbm(C, FAKE + 8, FAKE * 4, 16) == EALIGN
+    assert hbm(R, FAKE, FAKE * 4 + 4, 16) == EALIGN
+    assert hbm(Wr, None, FAKE + 8, 16) == EALIGN
+    assert hbm(C, FAKE, FAKE + 16, 64) == ESHAPE                # overlap
     assert "overlap" in _err(lib)
-    assert lib.bitlogic_probe_copy(FAKE, FAKE * 4, 0, None) == OK
-
+    assert hbm(C, FAKE, FAKE * 4, 0) == OK
+    assert hbm(Wr, None, FAKE * 4, 0) == OK
