@@ -185,6 +185,37 @@ __device__ __forceinline__ void gather(const uint64_t *src, const int32_t *c, in
     }
 }
 
+// The same gather with each row address formed as a wave-uniform slab base
+// plus a 32-bit byte offset (global loads with an SGPR base: one 32-bit
+// shift-add per input instead of 64-bit address arithmetic).  Used by the
+// fused last layer at 5 and 6 inputs: 3-5% faster there on C3, C4 and C5
+// k = 6 in ABBA runs, but 4% slower at k = 4 and 1% at k = 2; the layer
+// kernel measured slower with it (1.34 against 1.25 ms on C4).
+template <int K, int R>
+__device__ __forceinline__ void gather_off(const char *slab_base, uint32_t lane_off,
+                                           const int32_t *c, int S, uint32_t (&xv)[2 * R][K])
+{
+#pragma unroll
+    for (int i = 0; i < K; ++i) {
+        const uint64_t *p = reinterpret_cast<const uint64_t *>(
+            slab_base + ((uint32_t)c[i] * (uint32_t)(S * 8) + lane_off));
+        if constexpr (R == 1) {
+            const uint2 a = *reinterpret_cast<const uint2 *>(p);
+            xv[0][i] = a.x;
+            xv[1][i] = a.y;
+        } else {
+#pragma unroll
+            for (int r = 0; r < R; r += 2) {
+                const u32x4 a = reinterpret_cast<const u32x4 *>(p)[r / 2];
+                xv[2 * r + 0][i] = a.x;
+                xv[2 * r + 1][i] = a.y;
+                xv[2 * r + 2][i] = a.z;
+                xv[2 * r + 3][i] = a.w;
+            }
+        }
+    }
+}
+
 template <int R>
 __device__ __forceinline__ void store_out(const uint32_t (&o)[2 * R], uint64_t *q, bool ok)
 {
@@ -542,6 +573,10 @@ __global__ __launch_bounds__(kThreads, BL_HEAD_MINWAVES) void k_lut_slab_head(
     const int sub = threadIdx.x % kHeadLPN;
     const int lnode = threadIdx.x / kHeadLPN;
     const uint64_t *src = in + (int64_t)slab * w_in * kSlabWords + sub * kHeadR;
+    const char *slab_base = reinterpret_cast<const char *>(in + (int64_t)slab * w_in * kSlabWords);
+    const uint32_t lane_off = (uint32_t)(sub * kHeadR * 8);
+    // a slab's rows span w_in * 128 bytes: 32-bit offsets while that fits
+    const bool off32 = (int64_t)w_in * kSlabWords * 8 <= 0xFFFFFFFFll;
 
     uint32_t ctr[2 * kHeadR][kHeadCP];
 #pragma unroll
@@ -559,7 +594,10 @@ __global__ __launch_bounds__(kThreads, BL_HEAD_MINWAVES) void k_lut_slab_head(
             spec_eval<0, K, kHeadR>(kp, src, &s_conn[jl * K], kSlabWords, s_tab[jl], o);
         } else {
             uint32_t xv[2 * kHeadR][K];
-            gather<K, kHeadR>(src, &s_conn[jl * K], kSlabWords, xv);
+            if (K >= 5 && off32)
+                gather_off<K, kHeadR>(slab_base, lane_off, &s_conn[jl * K], kSlabWords, xv);
+            else
+                gather<K, kHeadR>(src, &s_conn[jl * K], kSlabWords, xv);
             eval_node<K, kHeadR>(s_tab[jl], xv, o);
         }
 #pragma unroll
