@@ -153,8 +153,7 @@ STAGE_KERNELS = {"encode": "k_encode_t / k_encode_ballot (encoder + bit-pack)",
                  "layer": "k_lut_slab (LUT layer)",
                  "layer_fused": "k_lut_slab_head (last LUT layer fused with GroupSum counting)",
                  "head_fused": "k_head_finish (counts -> scores, argmax)",
-                 "head": "k_head_planes + k_head_finish (GroupSum head, argmax)",
-                 "network": "k_net_fused (encoder, every layer and the head in one kernel)"}
+                 "head": "k_head_planes + k_head_finish (GroupSum head, argmax)"}
 
 
 def main():
@@ -249,7 +248,6 @@ def main():
             sums += [ev[i].elapsed_time(ev[i + 1]) for i in range(len(names))]
     stage_ms = dict(zip(names, (sums / ksteps).tolist()))
     plan = model.plan(n)
-    whole = plan["fused_network"]
 
     # ---- on-device peaks, after the timed work: probes with the hot path's
     # instruction and access types (v_bitop3_b32 chains; 16-byte non-temporal
@@ -301,9 +299,6 @@ def main():
         print(f"[bench] measured peaks: {valu:.2f} T int32 lane-ops/s, HBM read "
               f"{hbm['read'][0]:.0f} / write {hbm['write'][0]:.0f} / copy {hbm['copy'][0]:.0f} GB/s",
               file=sys.stderr, flush=True)
-    if whole:
-        # one kernel runs every stage: a single launch between the first two events
-        stage_ms = {"network": float(sum(stage_ms.values()))}
 
     dsp_detail = None
     if dsp_w is not None:
@@ -361,14 +356,6 @@ def main():
 
     fused = plan["fused_head"]
     alg = algorithmic(cfg, n, fused, binary_bits, model.fanin_histogram)
-    if whole:
-        # compulsory traffic of the single kernel: pixels in, scores and argmax out
-        ops = sum(v["ops"] for v in alg.values())
-        nb = n * cfg.d + 4 * n * cfg.n_classes + 4 * n
-        t_mem, t_alu = nb / (PEAK_HBM_GBS * 1e9), ops / (PEAK_VALU_TOPS * 1e12)
-        alg = {"network": {"bytes": nb, "ops": ops, "roof_ms": max(t_mem, t_alu) * 1e3,
-                           "bound": "hbm" if t_mem >= t_alu else "alu"}}
-        names, layer_names = ["network"], []
     roof_sum = sum(v["roof_ms"] for v in alg.values())
     # dominant kernel: the stage with the longest launch
     dom = max(names, key=lambda k: stage_ms[k])
@@ -379,9 +366,7 @@ def main():
     else:
         achieved = a["bytes"] / (stage_ms[dom] * 1e-3) / 1e9
         peak, unit, per = PEAK_HBM_GBS, "GB/s", f"{a['bytes']} bytes"
-    if dom == "network":
-        kname = STAGE_KERNELS["network"]
-    elif dom == "encode":
+    if dom == "encode":
         kname = STAGE_KERNELS["encode"]
     elif dom == "head":
         kname = STAGE_KERNELS["head_fused" if fused else "head"]
@@ -409,7 +394,6 @@ def main():
         "forward_roofline_frac": round(roof_sum / ms_per_step, 4),
         "staged_sum_ms": round(sum(stage_ms.values()), 4),
         "fused_head": fused,
-        "fused_network": whole,
         "specialized": bool(args.specialize),
         "fanin_histogram": ([None if h is None else [int(v) for v in h]
                              for h in model.fanin_histogram]

@@ -66,13 +66,10 @@
  * - Entry points are thread-safe; calls on one stream run in order.
  *
  * ---------------------------------------------------- environment switches
- * Read at every forward call; they change which kernels run, never results.
+ * Read at every forward call; it changes which kernels run, never results.
  *   BITLOGIC_UNFUSED_HEAD=1   the forward stores the last layer's bits and
  *                             runs the separate head kernels instead of the
  *                             last layer fused with the GroupSum counting.
- *   BITLOGIC_FUSED_NETWORK=1  GroupSum networks whose activations of 64
- *                             samples fit in LDS run as one whole-network
- *                             kernel (bitlogic_forward_info.fused_network).
  */
 #ifndef BITLOGIC_H
 #define BITLOGIC_H
@@ -160,10 +157,6 @@ typedef struct bitlogic_forward_info {
                                  written to memory                                */
     int32_t head_splits;      /* partial counters per (sample word, class)       */
     int32_t head_planes;      /* bit planes per partial counter                  */
-    int32_t fused_network;    /* 1: the whole network runs as one kernel, one
-                                 block per 64 samples with every activation in
-                                 LDS (small networks and batches; the workspace
-                                 is then not used)                              */
 } bitlogic_forward_info;
 
 int bitlogic_forward_plan(int64_t n_samples, int32_t n_features, int32_t n_thresholds,
@@ -445,7 +438,8 @@ const char *bitlogic_last_error(void);
  * before using the structs above (0.3.0 added bitlogic_network.pass_fanin and
  * the specialization calls; 0.4.0 the peak probes; 0.5.0
  * bitlogic_network_forward_noalloc, and bitlogic_probe_hbm in
- * place of the copy-only probe). */
+ * place of the copy-only probe; bitlogic_forward_info lost its
+ * fused_network member with the whole-network kernel). */
 #define BITLOGIC_VERSION 500
 int bitlogic_version(void);
 

@@ -122,26 +122,11 @@ struct ForwardPlan {
     size_t off_enc, off_a, off_b, off_head, total;
     bl::HeadPlan head;
     bool fused;            // last layer + head in one kernel
-    bool whole;            // the whole network in one kernel (net_fused.hip)
-    bl::NetPlan net;
 };
 
-// Whole-network kernel (net_fused.hip): available for GroupSum networks whose
-// activations of 64 samples fit in LDS, on request only
-// (BITLOGIC_FUSED_NETWORK=1).  Measured on MI355X with HIP-graph replays, the
-// layered kernels were faster at every batch from 64 to 4096 samples (C1:
-// 28-29 us against 36 us; 2 x 4000 nodes: 35-37 us against 52-53 us): one
-// block's serial encode -> layers -> head chain has a higher floor than four
-// short kernels that each spread over many CUs.
 bitlogic_network legacy_net(int32_t n_features, const uint8_t *thresholds, int32_t n_thresholds,
                             const bitlogic_layer *layers, int32_t n_layers, int32_t n_classes,
                             const int8_t *dsp_weights);
-
-bool fused_network_requested()
-{
-    const char *e = getenv("BITLOGIC_FUSED_NETWORK");
-    return e && e[0] == '1';
-}
 
 int plan_forward(int64_t n, int32_t d, int32_t b, const bitlogic_layer *layers, int32_t L,
                  int32_t c, ForwardPlan *fp)
@@ -195,8 +180,6 @@ int plan_forward(int64_t n, int32_t d, int32_t b, const bitlogic_layer *layers, 
     fp->off_b = fp->off_a + (need_a ? round_up(act) : 0);
     fp->off_head = fp->off_b + (need_b ? round_up(act) : 0);
     fp->total = fp->off_head + round_up(fp->head.ws_bytes);
-    fp->whole = false;
-    fp->net = bl::NetPlan{};
     return BITLOGIC_OK;
 }
 
@@ -327,17 +310,6 @@ int plan_network(const bitlogic_network *net, int64_t n, ForwardPlan *fp)
                       net->n_classes, fp);
     if (st != BITLOGIC_OK)
         return st;
-    if (fused_network_requested() && net->head == BITLOGIC_HEAD_GROUPSUM &&
-        net->n_layers <= bl::kNetMaxLayers && !net->pass_fanin) {
-        int32_t w_out[bl::kNetMaxLayers];
-        for (int32_t l = 0; l < net->n_layers; ++l)
-            w_out[l] = net->layers[l].w_out;
-        fp->net = bl::plan_net_fused(net->n_features, net->n_bits,
-                                     net->encoder == BITLOGIC_ENCODER_BINARY ? bl::kEncBinary
-                                                                              : bl::kEncThermometer,
-                                     w_out, net->n_layers, net->n_classes);
-        fp->whole = fp->net.ok;
-    }
     return BITLOGIC_OK;
 }
 
@@ -371,28 +343,6 @@ int forward_impl(const bitlogic_network *net, const uint8_t *x, int64_t n_sample
     }
     if (n_samples == 0)
         return ok();
-
-    if (fp.whole) {
-        bl::NetLayers nl{};
-        nl.n = net->n_layers;
-        for (int32_t l = 0; l < net->n_layers; ++l) {
-            nl.conn[l] = net->layers[l].conn;
-            nl.tables[l] = net->layers[l].tables;
-            nl.w_out[l] = net->layers[l].w_out;
-            nl.k[l] = net->layers[l].k;
-        }
-        hipStream_t s = (hipStream_t)stream;
-        // one kernel: every stage boundary event is recorded after it
-        hipError_t e = events ? hipEventRecord((hipEvent_t)events[0], s) : hipSuccess;
-        if (e == hipSuccess)
-            e = bl::launch_net_fused(x, n_samples, net->n_features, net->thresholds, net->n_bits,
-                                     net->encoder == BITLOGIC_ENCODER_BINARY
-                                         ? bl::kEncBinary : bl::kEncThermometer,
-                                     nl, net->n_classes, fp.net, scores, argmax, s);
-        for (int32_t i = 1; events && e == hipSuccess && i < n_events; ++i)
-            e = hipEventRecord((hipEvent_t)events[i], s);
-        return hip_status(e, "forward: whole-network launch");
-    }
 
     const bitlogic_layer *layers = net->layers;
     const int32_t n_classes = net->n_classes;
@@ -560,7 +510,6 @@ int bitlogic_network_plan(const bitlogic_network *net, int64_t n_samples,
     info->fused_head = fp.fused ? 1 : 0;
     info->head_splits = fp.head.splits;
     info->head_planes = fp.head.planes;
-    info->fused_network = fp.whole ? 1 : 0;
     return ok();
 }
 

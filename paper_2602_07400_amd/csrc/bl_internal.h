@@ -134,29 +134,6 @@ hipError_t launch_grouped_dsp(const int32_t *counts, int64_t n, int32_t c,
                               const int8_t *weights, int32_t *logits, int32_t *argmax,
                               hipStream_t stream);
 
-// Whole network in one kernel (net_fused.hip): layer descriptors by value.
-constexpr int kNetMaxLayers = 16;
-constexpr int64_t kNetMaxLds = 64 * 1024;       // dynamic LDS of one block
-struct NetLayers {
-    const int32_t *conn[kNetMaxLayers];
-    const uint64_t *tables[kNetMaxLayers];
-    int32_t w_out[kNetMaxLayers];
-    int32_t k[kNetMaxLayers];
-    int32_t n;
-};
-struct NetPlan {
-    bool ok;               // the network's activations of 64 samples fit in LDS
-    int32_t rows_a, rows_b;
-    bool tile_in_a;
-    size_t lds_bytes;
-};
-NetPlan plan_net_fused(int32_t d, int32_t b, int32_t kind, const int32_t *w_out, int32_t n_layers,
-                       int32_t c);
-hipError_t launch_net_fused(const uint8_t *x, int64_t n, int32_t d, const uint8_t *th, int32_t b,
-                            int32_t kind, const NetLayers &layers, int32_t c,
-                            const NetPlan &plan, int32_t *scores, int32_t *argmax,
-                            hipStream_t stream);
-
 // Peak probes (probes.hip): kProbeThreads = 256 lanes a block.
 hipError_t launch_probe_valu(uint32_t *out, int32_t blocks, int32_t iters, uint32_t seed,
                              hipStream_t stream);

@@ -335,38 +335,8 @@ def test_network_noalloc_validation(lib):
     assert re.search(r"#define BITLOGIC_NOALLOC_SCRATCH_BYTES \(64u << 20\)", hdr)
 
 
-def test_whole_network_plan(lib, monkeypatch):
-    info = bl._ForwardInfo()
-    ref = ctypes.byref(info)
-    p, keep = _layers([(1000, 6), (1000, 6)])
-    # off unless requested
-    monkeypatch.delenv("BITLOGIC_FUSED_NETWORK", raising=False)
-    assert lib.bitlogic_forward_plan(4096, 784, 1, p, 2, 10, ref) == OK
-    assert info.fused_network == 0
-    monkeypatch.setenv("BITLOGIC_FUSED_NETWORK", "1")
-    # C1: 784 wires + 2 x 1000 nodes of 64 samples fit in LDS, at any batch
-    assert lib.bitlogic_forward_plan(4096, 784, 1, p, 2, 10, ref) == OK
-    assert info.fused_network == 1
-    assert lib.bitlogic_forward_plan(1 << 20, 784, 1, p, 2, 10, ref) == OK
-    assert info.fused_network == 1
-    # the paper's deployed network shape (3136 wires, 2 x 4000 nodes) fits
-    pp, keepp = _layers([(4000, 4), (4000, 4)])
-    assert lib.bitlogic_forward_plan(1024, 784, 4, pp, 2, 10, ref) == OK
-    assert info.fused_network == 1
-    # too wide for LDS (C4), more than 8 code bits, or the quantized head: layered
-    p4, keep4 = _layers([(64000, 6), (64000, 6)])
-    assert lib.bitlogic_forward_plan(4096, 3072, 7, p4, 2, 100, ref) == OK
-    assert info.fused_network == 0
-    assert lib.bitlogic_forward_plan(4096, 784, 9, p, 2, 10, ref) == OK
-    assert info.fused_network == 0
-    assert lib.bitlogic_network_plan(ctypes.byref(_net(p, head=1, w=FAKE)), 4096, ref) == OK
-    assert info.fused_network == 0
-
-
-
-def test_pass_fanin_plan(lib, monkeypatch):
-    # a specialized network keeps the fused head and the workspace; the
-    # whole-network kernel is not used for it
+def test_pass_fanin_plan(lib):
+    # a specialized network keeps the fused head and the workspace
     p, keep = _layers([(1280, 6), (1280, 6)])     # g = 128 per class: fused head
     info = bl._ForwardInfo()
     ref = ctypes.byref(info)
@@ -378,14 +348,6 @@ def test_pass_fanin_plan(lib, monkeypatch):
     net.pass_fanin = ctypes.cast(arr, ctypes.c_void_p)
     assert lib.bitlogic_network_plan(ctypes.byref(net), 4096, ref) == OK
     assert info.fused_head == 1 and info.workspace_bytes == plain_ws
-    monkeypatch.setenv("BITLOGIC_FUSED_NETWORK", "1")
-    pc, keepc = _layers([(1000, 6), (1000, 6)])
-    net = _net(pc)
-    assert lib.bitlogic_network_plan(ctypes.byref(net), 4096, ref) == OK
-    assert info.fused_network == 1
-    net.pass_fanin = ctypes.cast(arr, ctypes.c_void_p)
-    assert lib.bitlogic_network_plan(ctypes.byref(net), 4096, ref) == OK
-    assert info.fused_network == 0
 
 
 def test_probe_validation(lib):
