@@ -129,7 +129,7 @@ __global__ __launch_bounds__(kThreads) void k_head_planes(
     }
 }
 
-// One block (4 waves) per 64-sample column: finish::column (head_finish.h).
+// One block (4 waves) per 64-sample column: finish::column_scalar (head_finish.h).
 template <int P>
 __global__ __launch_bounds__(kThreads) void k_head_finish(
     const uint64_t *__restrict__ planes, int64_t n, int32_t c, int32_t S, int32_t cs,
@@ -137,7 +137,8 @@ __global__ __launch_bounds__(kThreads) void k_head_finish(
 {
     extern __shared__ uint64_t buf[];                 // buf_words words
     __shared__ int32_t part[2][finish::kWaves][kWave];
-    finish::column<P>(planes, blockIdx.x, n, c, S, cs, buf_words, buf, part, scores, argmax);
+    (void)buf_words;
+    finish::column_scalar<P>(planes, blockIdx.x, n, c, S, cs, buf, part, scores, argmax);
 }
 
 // ---------------------------------------------------------------------------
@@ -581,7 +582,7 @@ hipError_t launch_finish_p(const uint64_t *planes, int64_t n, int32_t c, int32_t
                            stage_words, dsp_weights, scores, argmax);
         return hipGetLastError();
     }
-    const int64_t words = finish::lds_words(c, plan.splits, P);
+    const int64_t words = finish::tile_words(c);
     hipLaunchKernelGGL(k_head_finish<P>, dim3((unsigned)W), dim3(kThreads),
                        (size_t)words * sizeof(uint64_t), stream, planes, n, c, plan.splits,
                        finish::stride(c), (int32_t)words, scores, argmax);

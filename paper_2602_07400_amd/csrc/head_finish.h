@@ -12,11 +12,9 @@ namespace finish {
 constexpr int kThreads = 256;                    // the block this runs in
 constexpr int kWaves = kThreads / kWave;
 constexpr int kClasses = 128;                    // classes per chunk
-constexpr int kPerWave = kClasses / kWaves;
-// LDS of the finish: one buffer that first stages plane words (uint64) and
-// then holds the score tile [64][cs] (int32, cs = the odd stride >= the
-// chunk's classes, so the tile has no bank conflicts).  Its size is the
-// larger of the tile and the planes of one chunk, at most kMaxWords.
+// LDS of the finish: the score tile [64][cs] (int32, cs = the odd stride >=
+// the chunk's classes, so the tile has no bank conflicts).  kMaxWords bounds
+// the LDS the quantized head's finish stages planes in.
 constexpr int kMaxWords = kWave * (kClasses + 1) / 2;   // uint64 words
 
 __host__ __device__ inline int32_t stride(int32_t c)
@@ -29,104 +27,124 @@ __host__ __device__ inline int64_t tile_words(int32_t c)
     return ((int64_t)kWave * stride(c) + 1) / 2;
 }
 
-__host__ __device__ inline int64_t lds_words(int32_t c, int32_t S, int32_t P)
+
+// 2 v + bit `lane` of the 64-bit word w (wave-uniform, in an SGPR pair): one
+// v_addc_co_u32 whose carry-in is w read as a lane mask.
+__device__ __forceinline__ int32_t twice_plus_bit(int32_t v, uint64_t w)
 {
-    const int64_t stage = (int64_t)(c < kClasses ? c : kClasses) * S * P;
-    const int64_t want = stage < kMaxWords ? stage : kMaxWords;
-    return tile_words(c) > want ? tile_words(c) : want;
+    uint64_t carry_out;
+    asm("v_addc_co_u32_e64 %0, %1, %0, %0, %2" : "+v"(v), "=s"(carry_out) : "s"(w));
+    return v;
 }
 
-// Column `col` of planes [W][c][S][P]: all kThreads threads of the block, one
-// lane per sample.  Per chunk of up to 128 classes, the block first copies
-// the chunk's planes ([class][split][plane], contiguous) into buf with
-// coalesced loads, all in flight at once (a class's planes are otherwise a
-// chain of scalar loads, one latency per class); when a chunk's splits do
-// not fit, it is copied in runs of splits.  Wave w counts classes w, w + 4,
-// ...: bit `lane` of each plane word (a broadcast LDS read of the word's
-// half) goes to bit p of the count, and the splits are summed in registers.
-// The counts then go to the LDS tile [64][cs], from which the scores leave as
-// one contiguous block.  Each wave keeps its own running argmax in class
-// order; the four are merged at the end (largest count, then lowest class)
-// through part.  buf holds buf_words >= tile_words(c) words.  Starts and ends
-// with a barrier, so calls can follow each other.
+// Column `col` of planes [W][c][S][P], one lane per sample.  A class's S * P
+// plane words are wave-uniform, so they are read with scalar loads, and bit `lane` of each word enters the lane's
+// count through the word as a carry-in mask (Horner from the top plane): P
+// VALU instructions per split and class instead of a shift, mask and merge
+// per plane.  Wave w counts classes w, w + 4, ...; the counts go to the LDS
+// tile [64][cs] (buf, tile_words(c) words), from which the scores leave as
+// one contiguous block with 16-byte stores where the block is whole and
+// aligned.  Each wave keeps a running argmax in class order, merged at the
+// end (largest count, then lowest class).  Starts and ends with a barrier.
 template <int P>
-__device__ __forceinline__ void column(const uint64_t *__restrict__ planes, int64_t col, int64_t n,
-                                       int32_t c, int32_t S, int32_t cs, int32_t buf_words,
-                                       uint64_t *buf, int32_t (*part)[kWaves][kWave],
-                                       int32_t *__restrict__ scores, int32_t *__restrict__ argmax)
+__device__ __forceinline__ void column_scalar(const uint64_t *__restrict__ planes, int64_t col,
+                                              int64_t n, int32_t c, int32_t S, int32_t cs,
+                                              uint64_t *buf, int32_t (*part)[kWaves][kWave],
+                                              int32_t *__restrict__ scores,
+                                              int32_t *__restrict__ argmax)
 {
-    const uint32_t *buf32 = reinterpret_cast<const uint32_t *>(buf);
     int32_t *tile = reinterpret_cast<int32_t *>(buf);
     const int lane = threadIdx.x % kWave;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int half = lane >> 5, bit = lane & 31;
     const int64_t s0 = col * kWave;
     const uint64_t *pc = planes + col * (int64_t)c * S * P;
-    const int32_t sp_words = S * P;                   // one class's plane words
     int32_t best = -1, besti = 0;
     __syncthreads();
-    for (int c0 = 0, cn = 0; c0 < c; c0 += cn) {
-        // classes of this chunk, and splits per staged run
-        cn = min(kClasses, c - c0);
-        if ((int64_t)cn * sp_words > buf_words)
-            cn = max(1, buf_words / sp_words);
-        const int run = (int64_t)cn * sp_words <= buf_words ? S : buf_words / P;
-        int32_t cnt[kPerWave];
+    for (int c0 = 0; c0 < c; c0 += kClasses) {
+        const int cn = min(kClasses, c - c0);
+        int ii = wave;
+        if (S == 1) {
+            // kU classes at a time: their plane words are loaded together, so
+            // a wave waits for one scalar-load latency per kU classes
+            constexpr int kU = P <= 8 ? 4 : 2;
+            for (; ii + (kU - 1) * kWaves < cn; ii += kU * kWaves) {
+                uint64_t w[kU][P];
 #pragma unroll
-        for (int j = 0; j < kPerWave; ++j)
-            cnt[j] = 0;
-        for (int q0 = 0; q0 < S; q0 += run) {
-            const int qn = min(run, S - q0);
-            // contiguous: either whole classes (qn == S) or one class (cn == 1)
-            const uint64_t *src = pc + ((int64_t)c0 * S + q0) * P;
-            const int words = cn * qn * P;
-            for (int e = threadIdx.x; e < words; e += kThreads)
-                buf[e] = src[e];
-            __syncthreads();
+                for (int u = 0; u < kU; ++u)
 #pragma unroll
-            for (int j = 0; j < kPerWave; ++j) {
-                const int ii = wave + kWaves * j;
-                if (ii < cn) {
-                    int32_t acc = 0;
-                    for (int q = 0; q < qn; ++q) {
-                        const uint32_t *w = buf32 + 2 * (ii * qn + q) * P + half;
-                        int32_t v = 0;
+                    for (int p = 0; p < P; ++p)
+                        w[u][p] = pc[(int64_t)(c0 + ii + u * kWaves) * P + p];
 #pragma unroll
-                        for (int p = 0; p < P; ++p)
-                            v |= (int32_t)((w[2 * p] >> bit) & 1u) << p;
-                        acc += v;
+                for (int u = 0; u < kU; ++u) {
+                    int32_t v = 0;
+#pragma unroll
+                    for (int p = P - 1; p >= 0; --p)
+                        v = twice_plus_bit(v, w[u][p]);
+                    tile[lane * cs + ii + u * kWaves] = v;
+                    if (v > best) {           // classes ascend within a wave
+                        best = v;
+                        besti = c0 + ii + u * kWaves;
                     }
-                    cnt[j] += acc;
                 }
             }
-            __syncthreads();
         }
+        for (; ii < cn; ii += kWaves) {
+            const uint64_t *pw = pc + (int64_t)(c0 + ii) * S * P;
+            int32_t cnt = 0;
+            for (int q = 0; q < S; ++q) {
+                int32_t v = 0;
 #pragma unroll
-        for (int j = 0; j < kPerWave; ++j) {
-            const int ii = wave + kWaves * j;
-            if (ii < cn) {
-                tile[lane * cs + ii] = cnt[j];
-                if (cnt[j] > best) {             // classes ascend within a wave
-                    best = cnt[j];
-                    besti = c0 + ii;
-                }
+                for (int p = P - 1; p >= 0; --p)
+                    v = twice_plus_bit(v, pw[q * P + p]);
+                cnt += v;
+            }
+            tile[lane * cs + ii] = cnt;
+            if (cnt > best) {
+                best = cnt;
+                besti = c0 + ii;
             }
         }
         __syncthreads();
         if (scores) {
-            // element e = r * cn + k of the contiguous block, walked without a
-            // division per element
-            const int e0 = threadIdx.x;
-            int r = e0 / cn, k = e0 - r * cn;
-            const int dr = kThreads / cn, dk = kThreads - dr * cn;
-            for (int e = e0; e < kWave * cn; e += kThreads) {
-                if (s0 + r < n)
-                    scores[(s0 + r) * c + c0 + k] = tile[r * cs + k];
-                r += dr;
-                k += dk;
-                if (k >= cn) {
-                    k -= cn;
-                    ++r;
+            int32_t *dst = scores + s0 * c + c0;
+            const int total = kWave * cn;
+            if (cn == c && s0 + kWave <= n && ((uintptr_t)dst % 16) == 0) {
+                // the block [64][c] is contiguous: element e = r * c + k,
+                // walked without a division per element
+                const int e0 = 4 * threadIdx.x;
+                int r = e0 / cn, k = e0 - r * cn;
+                const int dr = 4 * kThreads / cn, dk = 4 * kThreads - dr * cn;
+                for (int e = e0; e < total; e += 4 * kThreads) {
+                    int32_t v[4];
+                    int rr = r, kk = k;
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        v[u] = tile[rr * cs + kk];
+                        if (++kk == cn) {
+                            kk = 0;
+                            ++rr;
+                        }
+                    }
+                    *reinterpret_cast<int4 *>(dst + e) = make_int4(v[0], v[1], v[2], v[3]);
+                    r += dr;
+                    k += dk;
+                    if (k >= cn) {
+                        k -= cn;
+                        ++r;
+                    }
+                }
+            } else {
+                int r = threadIdx.x / cn, k = threadIdx.x - r * cn;
+                const int dr = kThreads / cn, dk = kThreads - dr * cn;
+                for (int e = threadIdx.x; e < total; e += kThreads) {
+                    if (s0 + r < n)
+                        dst[(int64_t)r * c + k] = tile[r * cs + k];
+                    r += dr;
+                    k += dk;
+                    if (k >= cn) {
+                        k -= cn;
+                        ++r;
+                    }
                 }
             }
         }
