@@ -284,14 +284,46 @@ def main():
                 if best is None or rate > best[0]:
                     best = (rate, unroll, blocks)
             hbm[tag] = best
-        del pout, csrc, cdst
+        # instruction rates of the multiplexer (three source banks, and two
+        # sources in one bank) and of the table-bit mask extraction, in cycles
+        # per wave instruction per SIMD at the measured engine clock span
+        ops = {}
+        for op, tag in ((bl.PROBE_OP_MUX, "mux_3banks"), (bl.PROBE_OP_MUX_BANK, "mux_2banks"),
+                        (bl.PROBE_OP_BFE, "bfe_mask")):
+            rate = span(lambda r: bl.bitlogic_probe_valu_op(op, pout, pblocks // 4, 64, r,
+                                                            stream), 5)
+            ops[tag] = round(rate * 64 / 1e12, 3)          # T lane-ops/s
+        # the layers' row gathers alone (no multiplexers) and with 512 VALU
+        # instructions per pass, at 4 waves per SIMD as the layer kernels run:
+        # 16 rows per load instruction in two halves (lanes_per_row 4) or whole
+        # lines (8), over an L2-resident 2.75 MB set (C4's layer-1 slab) and an
+        # 8.2 MB set (its layer-2 slab), with and without the output stores
+        gather = {}
+        gblocks, gpasses = 256 * 16, 8
+        gout = torch.empty(gblocks * 256, dtype=torch.int32, device=dev)
+        gsink = torch.empty(gblocks * gpasses * 8192, dtype=torch.uint8, device=dev)
+        for mb, nrow in (("2.75MB", 21504), ("8.2MB", 64000)):
+            grows = torch.ones(nrow * 128, dtype=torch.uint8, device=dev)
+            for lpr, v, sk in ((4, 0, False), (8, 0, False), (4, 512, False), (4, 0, True),
+                               (4, 512, True)):
+                rate = span(lambda r: bl.bitlogic_probe_gather(
+                    grows, lpr, v, gblocks, gpasses, gout, gsink if sk else None,
+                    waves_per_simd=4, seed=r, stream=stream), 5)
+                gather[f"{mb} lanes/row {lpr} valu {v}{' +stores' if sk else ''}"] = round(
+                    rate * 128 / 1e12, 2)                  # TB/s of gathered lines
+            del grows
+        del pout, csrc, cdst, gout, gsink
         peaks = {"valu_TOPs": round(valu, 3),
                  "valu_frac_of_published": round(valu / PEAK_VALU_TOPS, 4),
                  "hbm_read_GBs": round(hbm["read"][0], 1),
                  "hbm_write_GBs": round(hbm["write"][0], 1),
                  "hbm_copy_GBs": round(hbm["copy"][0], 1),
                  "hbm_read_frac_of_published": round(hbm["read"][0] / PEAK_HBM_GBS, 4),
+                 "valu_op_T_lane_ops": ops,
+                 "gather_TBs": gather,
                  "probes": "bitlogic_probe_valu (65536 x 256 lanes, 1024 rounds of 8 v_bitop3_b32); "
+                           "bitlogic_probe_valu_op (16384 x 256 lanes, 64 rounds of 64); "
+                           "bitlogic_probe_gather (4096 blocks x 8 passes, 4 waves per SIMD); "
                            "bitlogic_probe_hbm over 4 GiB, best of (unroll, blocks) in "
                            "(4, 2048), (8, 1024), (8, 2048), (2, 4096): "
                            + ", ".join(f"{t} unroll {u} blocks {b}" for t, (_, u, b) in hbm.items())

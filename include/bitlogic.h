@@ -406,6 +406,55 @@ int bitlogic_network_forward_noalloc(const bitlogic_network *net, const uint8_t 
 int bitlogic_probe_valu(uint32_t *out, int32_t blocks, int32_t iters, uint32_t seed,
                         void *stream);
 
+/* Instruction-rate probe: `blocks` blocks of 256 lanes, each lane running
+ * `iters` rounds of 64 instructions of one form on fixed registers, so that
+ * the VGPR banks of the operands are known (register v[n] is in bank n % 4).
+ * Lane l (global index) starts from c0 = ((l + 1) * 0x9E3779B1) ^ seed,
+ * s = c0 * 0x85EBCA77 and z = ~c0 (32-bit wrap-around) in eight chains
+ * c[0..7] = c0, then every round applies to each chain:
+ *   BITLOGIC_PROBE_OP_MUX       c = (s & c) | (~s & z), one v_bitop3_b32 whose
+ *                               three sources sit in three VGPR banks
+ *   BITLOGIC_PROBE_OP_MUX_BANK  the same with two sources in one bank
+ *   BITLOGIC_PROBE_OP_BFE       c = -((s >> 5) & 1) (v_bfe_i32, the mask of
+ *                               one table bit)
+ * and writes the sum of the eight chains (mod 2^32) to out[l].  A call issues
+ * blocks * 4 * iters * 64 wave instructions.
+ *   out  uint32 [blocks * 256]; blocks >= 1, iters >= 1. */
+#define BITLOGIC_PROBE_OP_MUX 0
+#define BITLOGIC_PROBE_OP_MUX_BANK 1
+#define BITLOGIC_PROBE_OP_BFE 2
+int bitlogic_probe_valu_op(int32_t op, uint32_t *out, int32_t blocks, int32_t iters,
+                           uint32_t seed, void *stream);
+
+/* Gather probe: the LUT layers' random row gathers (App. C.1: every node
+ * reads whole 1024-sample row segments of 128 bytes) without their
+ * multiplexers.  Per pass, wave w of block b gathers, for the 16 nodes
+ * j = (b * passes + pass) * 64 + w * 16 + m (m = 0..15), rows
+ * r(j, i) = h(6 j + i) mod n_rows for i = 0..5, where
+ * h(x) = y ^ (y >> 16), y = (x ^ seed) * 0x9E3779B1 (32-bit).
+ *   lanes_per_row 4: lane t serves node m = t / 4 and loads 16-byte pieces
+ *                    2 q and 2 q + 1 (q = t % 4) of each of its 6 rows (the
+ *                    split of the 5- and 6-input layer kernels: 16 rows per
+ *                    load instruction);
+ *   lanes_per_row 8: lane t serves nodes m = t / 8 and m = 8 + t / 8 and
+ *                    loads piece t % 8 of each of their rows (a whole line
+ *                    per 8 lanes: 8 rows per load instruction).
+ * Each lane then issues valu_per_pass (0, 256, 512 or 768) v_bitop3_b32 on
+ * the loaded words, whose results are dropped (they occupy the VALU as the
+ * multiplexers do), and XORs its 12 pieces into a 16-byte accumulator;
+ * out[b * 256 + t] = the XOR of the accumulator's four words.  With a sink,
+ * wave w of block b also stores, per pass, its lanes' first two pieces to
+ * sink 16-byte pieces ((b * passes + pass) * 4 + w) * 128 + 2 t and + 1,
+ * non-temporally (2 KB per wave and pass, as the layer kernel's output).
+ * waves_per_simd 1..8 limits the resident waves through the block's LDS
+ * size (0: no limit).
+ *   rows  n_rows * 128 bytes (16-byte aligned), 1 <= n_rows < 2^32
+ *   out   uint32 [blocks * 256];  sink  NULL or blocks * passes * 8 KB. */
+int bitlogic_probe_gather(const void *rows, int64_t n_rows, int32_t lanes_per_row,
+                          int32_t valu_per_pass, int32_t blocks, int32_t passes,
+                          int32_t waves_per_simd, uint32_t seed, uint32_t *out, void *sink,
+                          void *stream);
+
 /* HBM streaming probes over n_bytes (a multiple of 16) in 16-byte pieces,
  * with non-temporal 16-byte loads and stores; a block of 256 lanes covers
  * unroll * 256 consecutive pieces per step with its `unroll` loads in
@@ -438,9 +487,10 @@ const char *bitlogic_last_error(void);
  * before using the structs above (0.3.0 added bitlogic_network.pass_fanin and
  * the specialization calls; 0.4.0 the peak probes; 0.5.0
  * bitlogic_network_forward_noalloc, and bitlogic_probe_hbm in
- * place of the copy-only probe; bitlogic_forward_info lost its
- * fused_network member with the whole-network kernel). */
-#define BITLOGIC_VERSION 500
+ * place of the copy-only probe; 0.6.0 bitlogic_forward_info without the
+ * fused_network member (the whole-network kernel was removed), and the
+ * instruction-rate and gather probes). */
+#define BITLOGIC_VERSION 600
 int bitlogic_version(void);
 
 #ifdef __cplusplus

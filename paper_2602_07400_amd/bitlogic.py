@@ -110,6 +110,9 @@ def load_library():
                                          P, P, P], ctypes.c_int),
         "bitlogic_probe_valu": ([P, i32, i32, ctypes.c_uint32, P], ctypes.c_int),
         "bitlogic_probe_hbm": ([i32, P, P, i64, i32, i32, P], ctypes.c_int),
+        "bitlogic_probe_valu_op": ([i32, P, i32, i32, ctypes.c_uint32, P], ctypes.c_int),
+        "bitlogic_probe_gather": ([P, i64, i32, i32, i32, i32, i32, ctypes.c_uint32, P, P, P],
+                                  ctypes.c_int),
         "bitlogic_status_string": ([ctypes.c_int], ctypes.c_char_p),
         "bitlogic_last_error": ([], ctypes.c_char_p),
         "bitlogic_version": ([], ctypes.c_int),
@@ -693,3 +696,38 @@ def bitlogic_probe_hbm(mode: int, src: Optional[torch.Tensor], dst: torch.Tensor
         int(mode), src.data_ptr() if src is not None else None, dst.data_ptr(), int(nbytes),
         int(unroll), int(blocks), _stream(stream, dev)))
     return (2 if mode == PROBE_HBM_COPY else 1) * int(nbytes)
+
+
+PROBE_OP_MUX, PROBE_OP_MUX_BANK, PROBE_OP_BFE = 0, 1, 2
+
+
+def bitlogic_probe_valu_op(op: int, out: torch.Tensor, blocks: int, iters: int, seed: int = 0,
+                           stream=None) -> int:
+    """Instruction-rate probe (include/bitlogic.h) into out (int32 [blocks * 256]
+    on the GPU); returns the wave instructions it issues."""
+    if out.numel() < blocks * PROBE_THREADS:
+        raise ValueError("out needs blocks * 256 words")
+    _check(load_library().bitlogic_probe_valu_op(int(op), _dev(out, "out", _I32), int(blocks),
+                                                 int(iters), int(seed) & 0xFFFFFFFF,
+                                                 _stream(stream, out.device)))
+    return int(blocks) * 4 * int(iters) * 64
+
+
+def bitlogic_probe_gather(rows: torch.Tensor, lanes_per_row: int, valu_per_pass: int,
+                          blocks: int, passes: int, out: torch.Tensor,
+                          sink: Optional[torch.Tensor] = None, waves_per_simd: int = 0,
+                          seed: int = 0, stream=None) -> int:
+    """Gather probe (include/bitlogic.h) over rows (a contiguous GPU tensor of
+    n_rows * 128 bytes); returns the 128-byte rows it gathers."""
+    nbytes = rows.numel() * rows.element_size()
+    if nbytes % 128:
+        raise ValueError("rows must be whole 128-byte rows")
+    if out.numel() < blocks * PROBE_THREADS:
+        raise ValueError("out needs blocks * 256 words")
+    if sink is not None and sink.numel() * sink.element_size() < blocks * passes * 8192:
+        raise ValueError("sink needs blocks * passes * 8 KB")
+    _check(load_library().bitlogic_probe_gather(
+        rows.data_ptr(), nbytes // 128, int(lanes_per_row), int(valu_per_pass), int(blocks),
+        int(passes), int(waves_per_simd), int(seed) & 0xFFFFFFFF, _dev(out, "out", _I32),
+        sink.data_ptr() if sink is not None else None, _stream(stream, out.device)))
+    return int(blocks) * int(passes) * 64 * 6

@@ -742,6 +742,49 @@ int bitlogic_probe_valu(uint32_t *out, int32_t blocks, int32_t iters, uint32_t s
                       "probe_valu launch");
 }
 
+int bitlogic_probe_valu_op(int32_t op, uint32_t *out, int32_t blocks, int32_t iters,
+                           uint32_t seed, void *stream)
+{
+    if (op < BITLOGIC_PROBE_OP_MUX || op > BITLOGIC_PROBE_OP_BFE)
+        return fail(BITLOGIC_ERR_UNSUPPORTED, "probe_valu_op: unknown op %d", op);
+    if (!out)
+        return fail(BITLOGIC_ERR_NULL, "probe_valu_op: NULL output");
+    if (blocks < 1 || iters < 1)
+        return fail(BITLOGIC_ERR_SHAPE, "probe_valu_op: need blocks >= 1, iters >= 1");
+    if (!aligned(out, 4))
+        return fail(BITLOGIC_ERR_ALIGN, "probe_valu_op: output not 4-byte aligned");
+    return hip_status(bl::launch_probe_valu_op(op, out, blocks, iters, seed, (hipStream_t)stream),
+                      "probe_valu_op launch");
+}
+
+int bitlogic_probe_gather(const void *rows, int64_t n_rows, int32_t lanes_per_row,
+                          int32_t valu_per_pass, int32_t blocks, int32_t passes,
+                          int32_t waves_per_simd, uint32_t seed, uint32_t *out, void *sink,
+                          void *stream)
+{
+    if (lanes_per_row != 4 && lanes_per_row != 8)
+        return fail(BITLOGIC_ERR_UNSUPPORTED, "probe_gather: lanes_per_row %d not 4 or 8",
+                    lanes_per_row);
+    if (valu_per_pass != 0 && valu_per_pass != 256 && valu_per_pass != 512 &&
+        valu_per_pass != 768)
+        return fail(BITLOGIC_ERR_UNSUPPORTED, "probe_gather: valu_per_pass %d not 0, 256, 512 "
+                    "or 768", valu_per_pass);
+    if (!rows || !out)
+        return fail(BITLOGIC_ERR_NULL, "probe_gather: NULL rows or output");
+    if (n_rows < 1 || n_rows > 0xFFFFFFFFll || blocks < 1 || passes < 1 || waves_per_simd < 0 ||
+        waves_per_simd > 8)
+        return fail(BITLOGIC_ERR_SHAPE, "probe_gather: need 1 <= n_rows < 2^32, blocks >= 1, "
+                    "passes >= 1, 0 <= waves_per_simd <= 8");
+    if ((int64_t)blocks * passes * 64 * 6 > 0xFFFFFFFFll)
+        return fail(BITLOGIC_ERR_SHAPE, "probe_gather: blocks * passes too large");
+    if (!aligned(rows, 16) || !aligned(out, 4) || (sink && !aligned(sink, 16)))
+        return fail(BITLOGIC_ERR_ALIGN, "probe_gather: rows and sink need 16-byte alignment");
+    return hip_status(bl::launch_probe_gather(rows, n_rows, lanes_per_row, valu_per_pass, blocks,
+                                              passes, waves_per_simd, seed, out, sink,
+                                              (hipStream_t)stream),
+                      "probe_gather launch");
+}
+
 int bitlogic_probe_hbm(int32_t mode, const void *in, void *out, int64_t n_bytes,
                        int32_t unroll, int32_t blocks, void *stream)
 {

@@ -137,6 +137,12 @@ hipError_t launch_grouped_dsp(const int32_t *counts, int64_t n, int32_t c,
 // Peak probes (probes.hip): kProbeThreads = 256 lanes a block.
 hipError_t launch_probe_valu(uint32_t *out, int32_t blocks, int32_t iters, uint32_t seed,
                              hipStream_t stream);
+hipError_t launch_probe_valu_op(int32_t op, uint32_t *out, int32_t blocks, int32_t iters,
+                                uint32_t seed, hipStream_t stream);
+hipError_t launch_probe_gather(const void *rows, int64_t n_rows, int32_t lanes_per_row,
+                               int32_t valu, int32_t blocks, int32_t passes,
+                               int32_t waves_per_simd, uint32_t seed, uint32_t *out, void *sink,
+                               hipStream_t stream);
 constexpr int kHbmCopy = 0;     // bitlogic_probe_hbm modes
 constexpr int kHbmRead = 1;
 constexpr int kHbmWrite = 2;

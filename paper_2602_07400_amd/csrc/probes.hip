@@ -134,6 +134,171 @@ hipError_t launch_hbm_mode(const u32x4 *in, u32x4 *out, int64_t n, int32_t unrol
     return hipGetLastError();
 }
 
+// ---- instruction-rate probe: one VALU instruction form repeated ----------
+// A self-contained asm loop on fixed registers, so that the VGPR banks of
+// the operands are known (v[n] is in bank n % 4): eight chains in v40, v44,
+// ..., v68 (bank 0), the selector in v41 (bank 1) and the zero operand in
+// v42 (bank 2) or v45 (bank 1).  Each round issues 64 instructions:
+//   kOpMux:      v_bitop3_b32 c, v41, c, v42 (table 0xCA: c = (v41 & c) | (~v41 & v42)),
+//                three source banks: the LUT layers' multiplexer at full rate
+//   kOpMuxBank:  the same with v45 in place of v42: two sources in bank 1
+//   kOpBfe:      v_bfe_i32 c, v41, 5, 1 (the mask of one table bit)
+// The lane's result is the sum of the eight chain registers afterwards.
+constexpr int kOpMux = 0, kOpMuxBank = 1, kOpBfe = 2;
+
+#define BL_PV8(INS) INS(40) INS(44) INS(48) INS(52) INS(56) INS(60) INS(64) INS(68)
+#define BL_MUX(R) "v_bitop3_b32 v" #R ", v41, v" #R ", v42 bitop3:0xca\n\t"
+#define BL_MUXB(R) "v_bitop3_b32 v" #R ", v41, v" #R ", v45 bitop3:0xca\n\t"
+#define BL_BFE(R) "v_bfe_i32 v" #R ", v41, 5, 1\n\t"
+#define BL_INIT(R) "v_mov_b32 v" #R ", %[c0]\n\t"
+#define BL_FOLD(R) "v_add_u32 %[r], %[r], v" #R "\n\t"
+#define BL_ROUND(X) BL_PV8(X) BL_PV8(X) BL_PV8(X) BL_PV8(X) BL_PV8(X) BL_PV8(X) BL_PV8(X) BL_PV8(X)
+
+template <int OP>
+__global__ __launch_bounds__(kProbeThreads) void k_probe_valu_op(uint32_t *__restrict__ out,
+                                                                 int32_t iters, uint32_t seed)
+{
+    const uint32_t gid = blockIdx.x * kProbeThreads + threadIdx.x;
+    const uint32_t c0 = (gid + 1u) * 0x9E3779B1u ^ seed;
+    const uint32_t sel = c0 * 0x85EBCA77u, zero = ~c0;
+    uint32_t r = 0;
+    uint32_t cnt = (uint32_t)iters;           // >= 1 (the launcher checks)
+    if constexpr (OP == kOpMux)
+        asm volatile(BL_PV8(BL_INIT) "v_mov_b32 v41, %[s]\n\tv_mov_b32 v42, %[z]\n\t"
+                     "1:\n\t" BL_ROUND(BL_MUX)
+                     "s_sub_u32 %[n], %[n], 1\n\ts_cmp_lg_u32 %[n], 0\n\ts_cbranch_scc1 1b\n\t"
+                     BL_PV8(BL_FOLD)
+                     : [r] "+v"(r), [n] "+s"(cnt)
+                     : [c0] "v"(c0), [s] "v"(sel), [z] "v"(zero)
+                     : "v40", "v41", "v42", "v44", "v48", "v52", "v56", "v60", "v64", "v68",
+                       "scc");
+    else if constexpr (OP == kOpMuxBank)
+        asm volatile(BL_PV8(BL_INIT) "v_mov_b32 v41, %[s]\n\tv_mov_b32 v45, %[z]\n\t"
+                     "1:\n\t" BL_ROUND(BL_MUXB)
+                     "s_sub_u32 %[n], %[n], 1\n\ts_cmp_lg_u32 %[n], 0\n\ts_cbranch_scc1 1b\n\t"
+                     BL_PV8(BL_FOLD)
+                     : [r] "+v"(r), [n] "+s"(cnt)
+                     : [c0] "v"(c0), [s] "v"(sel), [z] "v"(zero)
+                     : "v40", "v41", "v44", "v45", "v48", "v52", "v56", "v60", "v64", "v68",
+                       "scc");
+    else
+        asm volatile(BL_PV8(BL_INIT) "v_mov_b32 v41, %[s]\n\t"
+                     "1:\n\t" BL_ROUND(BL_BFE)
+                     "s_sub_u32 %[n], %[n], 1\n\ts_cmp_lg_u32 %[n], 0\n\ts_cbranch_scc1 1b\n\t"
+                     BL_PV8(BL_FOLD)
+                     : [r] "+v"(r), [n] "+s"(cnt)
+                     : [c0] "v"(c0), [s] "v"(sel)
+                     : "v40", "v41", "v44", "v48", "v52", "v56", "v60", "v64", "v68", "scc");
+    out[gid] = r;
+}
+
+#undef BL_PV8
+#undef BL_MUX
+#undef BL_MUXB
+#undef BL_BFE
+#undef BL_INIT
+#undef BL_FOLD
+#undef BL_ROUND
+
+// ---- gather probe: the LUT layers' row gathers without their arithmetic --
+// Per pass, wave w of block b gathers 6 rows of 128 bytes for each of 16
+// nodes j = (b * passes + pass) * 64 + w * 16 + m, row (j, i) =
+// probe_row(seed, 6 j + i) mod n_rows, with the lane split of the layer
+// kernels: LPR = 4 lanes per node, each loading two 16-byte halves of its
+// 32 bytes of every row (16 rows per load instruction, as at 5 and 6
+// inputs), or LPR = 8 lanes per row, one 16-byte piece each (a whole line
+// per 8 lanes, 8 rows per instruction; a lane then serves nodes m and m + 8).
+// V v_bitop3_b32 per lane and pass then run on the loaded words (their
+// results are dropped: they only occupy the VALU as the multiplexers do);
+// with a sink, each wave also stores 2 KB per pass (the lane's first two
+// pieces, non-temporal), as the layer kernel stores its output.
+__device__ __forceinline__ uint32_t probe_row(uint32_t seed, uint32_t x)
+{
+    uint32_t h = (x ^ seed) * 0x9E3779B1u;
+    return h ^ (h >> 16);
+}
+
+template <int LPR, int V, bool SINK>
+__global__ __launch_bounds__(kProbeThreads) void k_probe_gather(
+    const u32x4 *__restrict__ rows, uint32_t n_rows, uint32_t seed, int32_t passes,
+    uint32_t *__restrict__ out, u32x4 *__restrict__ sink)
+{
+    extern __shared__ uint32_t pad[];            // occupancy limiter only
+    (void)pad;
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int sub = lane % LPR;
+    u32x4 acc = u32x4{0, 0, 0, 0};
+#pragma unroll 1
+    for (int pass = 0; pass < passes; ++pass) {
+        const uint32_t j0 = ((uint32_t)blockIdx.x * (uint32_t)passes + (uint32_t)pass) * 64u +
+                            (uint32_t)wave * 16u;
+        u32x4 v[12];
+#pragma unroll
+        for (int i = 0; i < 6; ++i) {
+            if constexpr (LPR == 4) {
+                const uint32_t j = j0 + (uint32_t)(lane / 4);
+                const uint32_t r = probe_row(seed, 6u * j + (uint32_t)i) % n_rows;
+                v[2 * i] = rows[(size_t)r * 8 + 2 * sub];
+                v[2 * i + 1] = rows[(size_t)r * 8 + 2 * sub + 1];
+            } else {
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const uint32_t j = j0 + (uint32_t)(h * 8 + lane / 8);
+                    const uint32_t r = probe_row(seed, 6u * j + (uint32_t)i) % n_rows;
+                    v[6 * h + i] = rows[(size_t)r * 8 + sub];
+                }
+            }
+        }
+        if constexpr (V > 0) {
+            uint32_t a = v[0].x, b = v[1].y;
+#pragma unroll
+            for (int t = 0; t < V / 2; ++t) {
+                asm volatile("v_bitop3_b32 %0, %1, %0, %2 bitop3:0xca"
+                             : "+v"(a) : "v"(v[t % 12].z), "v"(b));
+                asm volatile("v_bitop3_b32 %0, %1, %0, %2 bitop3:0xca"
+                             : "+v"(b) : "v"(v[(t + 5) % 12].w), "v"(a));
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < 12; ++k)
+            acc ^= v[k];
+        if constexpr (SINK) {
+            u32x4 *q = sink + (((size_t)blockIdx.x * passes + pass) * 4 + wave) * 128 + lane * 2;
+            __builtin_nontemporal_store(v[0], q);
+            __builtin_nontemporal_store(v[1], q + 1);
+        }
+    }
+    out[blockIdx.x * kProbeThreads + threadIdx.x] = acc.x ^ acc.y ^ acc.z ^ acc.w;
+}
+
+template <int LPR, int V>
+hipError_t launch_gather_v(const u32x4 *rows, uint32_t n_rows, uint32_t seed, int32_t passes,
+                           int32_t blocks, size_t lds, uint32_t *out, u32x4 *sink,
+                           hipStream_t stream)
+{
+    if (sink)
+        hipLaunchKernelGGL((k_probe_gather<LPR, V, true>), dim3(blocks), dim3(kProbeThreads), lds,
+                           stream, rows, n_rows, seed, passes, out, sink);
+    else
+        hipLaunchKernelGGL((k_probe_gather<LPR, V, false>), dim3(blocks), dim3(kProbeThreads),
+                           lds, stream, rows, n_rows, seed, passes, out, sink);
+    return hipGetLastError();
+}
+
+template <int LPR>
+hipError_t launch_gather_l(const u32x4 *rows, uint32_t n_rows, uint32_t seed, int32_t passes,
+                           int32_t blocks, size_t lds, int32_t valu, uint32_t *out, u32x4 *sink,
+                           hipStream_t stream)
+{
+    switch (valu) {
+    case 0: return launch_gather_v<LPR, 0>(rows, n_rows, seed, passes, blocks, lds, out, sink, stream);
+    case 256: return launch_gather_v<LPR, 256>(rows, n_rows, seed, passes, blocks, lds, out, sink, stream);
+    case 512: return launch_gather_v<LPR, 512>(rows, n_rows, seed, passes, blocks, lds, out, sink, stream);
+    case 768: return launch_gather_v<LPR, 768>(rows, n_rows, seed, passes, blocks, lds, out, sink, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
 }  // namespace
 
 hipError_t launch_probe_valu(uint32_t *out, int32_t blocks, int32_t iters, uint32_t seed,
@@ -142,6 +307,48 @@ hipError_t launch_probe_valu(uint32_t *out, int32_t blocks, int32_t iters, uint3
     hipLaunchKernelGGL(k_probe_valu, dim3((unsigned)blocks), dim3(kProbeThreads), 0, stream, out,
                        iters, seed);
     return hipGetLastError();
+}
+
+hipError_t launch_probe_valu_op(int32_t op, uint32_t *out, int32_t blocks, int32_t iters,
+                                uint32_t seed, hipStream_t stream)
+{
+    if (iters < 1)
+        return hipErrorInvalidValue;
+    switch (op) {
+    case kOpMux:
+        hipLaunchKernelGGL(k_probe_valu_op<kOpMux>, dim3(blocks), dim3(kProbeThreads), 0, stream,
+                           out, iters, seed);
+        break;
+    case kOpMuxBank:
+        hipLaunchKernelGGL(k_probe_valu_op<kOpMuxBank>, dim3(blocks), dim3(kProbeThreads), 0,
+                           stream, out, iters, seed);
+        break;
+    case kOpBfe:
+        hipLaunchKernelGGL(k_probe_valu_op<kOpBfe>, dim3(blocks), dim3(kProbeThreads), 0, stream,
+                           out, iters, seed);
+        break;
+    default:
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_probe_gather(const void *rows, int64_t n_rows, int32_t lanes_per_row,
+                               int32_t valu, int32_t blocks, int32_t passes,
+                               int32_t waves_per_simd, uint32_t seed, uint32_t *out, void *sink,
+                               hipStream_t stream)
+{
+    // a block is one wave per SIMD: waves_per_simd blocks fit one CU's LDS
+    const size_t lds = waves_per_simd > 0 ? (size_t)(160 * 1024 / waves_per_simd) - 256 : 0;
+    const u32x4 *r = static_cast<const u32x4 *>(rows);
+    u32x4 *k = static_cast<u32x4 *>(sink);
+    if (lanes_per_row == 4)
+        return launch_gather_l<4>(r, (uint32_t)n_rows, seed, passes, blocks, lds, valu, out, k,
+                                  stream);
+    if (lanes_per_row == 8)
+        return launch_gather_l<8>(r, (uint32_t)n_rows, seed, passes, blocks, lds, valu, out, k,
+                                  stream);
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_probe_hbm(int32_t mode, const void *in, void *out, int64_t n_bytes,

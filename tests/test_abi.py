@@ -372,4 +372,23 @@ def test_probe_validation(lib):
     assert hbm(C, FAKE, FAKE + 16, 64) == ESHAPE                # overlap
     assert "overlap" in _err(lib)
     assert hbm(C, FAKE, FAKE * 4, 0) == OK
+    assert lib.bitlogic_probe_valu_op(3, FAKE, 1, 1, 0, None) == EUNSUP
+    assert lib.bitlogic_probe_valu_op(0, None, 1, 1, 0, None) == ENULL
+    assert lib.bitlogic_probe_valu_op(0, FAKE, 0, 1, 0, None) == ESHAPE
+    assert lib.bitlogic_probe_valu_op(2, FAKE, 1, 0, 0, None) == ESHAPE
+    assert lib.bitlogic_probe_valu_op(1, FAKE + 2, 1, 1, 0, None) == EALIGN
+    g = lambda **o: lib.bitlogic_probe_gather(
+        o.get("rows", FAKE), o.get("n", 100), o.get("lpr", 4), o.get("v", 0), o.get("b", 1),
+        o.get("p", 1), o.get("occ", 0), 0, o.get("out", FAKE), o.get("sink", None), None)
+    assert g(lpr=2) == EUNSUP
+    assert g(v=100) == EUNSUP
+    assert g(rows=None) == ENULL
+    assert g(out=None) == ENULL
+    assert g(n=0) == ESHAPE
+    assert g(b=0) == ESHAPE
+    assert g(p=0) == ESHAPE
+    assert g(occ=9) == ESHAPE
+    assert g(b=1 << 20, p=1 << 10) == ESHAPE
+    assert g(rows=FAKE + 8) == EALIGN
+    assert g(sink=FAKE + 8) == EALIGN
     assert hbm(Wr, None, FAKE * 4, 0) == OK
