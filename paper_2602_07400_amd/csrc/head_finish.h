@@ -27,7 +27,6 @@ __host__ __device__ inline int64_t tile_words(int32_t c)
     return ((int64_t)kWave * stride(c) + 1) / 2;
 }
 
-
 // 2 v + bit `lane` of the 64-bit word w (wave-uniform, in an SGPR pair): one
 // v_addc_co_u32 whose carry-in is w read as a lane mask.
 __device__ __forceinline__ int32_t twice_plus_bit(int32_t v, uint64_t w)
@@ -37,15 +36,42 @@ __device__ __forceinline__ int32_t twice_plus_bit(int32_t v, uint64_t w)
     return v;
 }
 
+// Sum over splits q, q + 1, ... (while kQ more remain) of the lane's count
+// from P plane words each, advancing q.  The kQ splits' words are loaded
+// together, so a wave waits for one scalar-load latency per kQ splits.
+template <int P, int kQ>
+__device__ __forceinline__ int32_t add_splits(const uint64_t *__restrict__ pw, int &q, int S)
+{
+    int32_t cnt = 0;
+    for (; q + kQ <= S; q += kQ) {
+        uint64_t w[kQ][P];
+#pragma unroll
+        for (int u = 0; u < kQ; ++u)
+#pragma unroll
+            for (int p = 0; p < P; ++p)
+                w[u][p] = pw[(q + u) * P + p];
+#pragma unroll
+        for (int u = 0; u < kQ; ++u) {
+            int32_t v = 0;
+#pragma unroll
+            for (int p = P - 1; p >= 0; --p)
+                v = twice_plus_bit(v, w[u][p]);
+            cnt += v;
+        }
+    }
+    return cnt;
+}
+
 // Column `col` of planes [W][c][S][P], one lane per sample.  A class's S * P
-// plane words are wave-uniform, so they are read with scalar loads, and bit `lane` of each word enters the lane's
-// count through the word as a carry-in mask (Horner from the top plane): P
-// VALU instructions per split and class instead of a shift, mask and merge
-// per plane.  Wave w counts classes w, w + 4, ...; the counts go to the LDS
-// tile [64][cs] (buf, tile_words(c) words), from which the scores leave as
-// one contiguous block with 16-byte stores where the block is whole and
-// aligned.  Each wave keeps a running argmax in class order, merged at the
-// end (largest count, then lowest class).  Starts and ends with a barrier.
+// plane words are wave-uniform, so they are read with scalar loads (several
+// classes' or splits' words at a time), and bit `lane` of each word enters
+// the lane's count through the word as a carry-in mask (Horner from the top
+// plane): P VALU instructions per split and class instead of a shift, mask
+// and merge per plane.  Wave w counts classes w, w + 4, ...; the counts go
+// to the LDS tile [64][cs] (buf, tile_words(c) words), from which the scores
+// leave as one contiguous block with 16-byte stores where the block is whole
+// and aligned.  Each wave keeps a running argmax in class order, merged at
+// the end (largest count, then lowest class).  Starts and ends with a barrier.
 template <int P>
 __device__ __forceinline__ void column_scalar(const uint64_t *__restrict__ planes, int64_t col,
                                               int64_t n, int32_t c, int32_t S, int32_t cs,
@@ -90,14 +116,9 @@ __device__ __forceinline__ void column_scalar(const uint64_t *__restrict__ plane
         }
         for (; ii < cn; ii += kWaves) {
             const uint64_t *pw = pc + (int64_t)(c0 + ii) * S * P;
-            int32_t cnt = 0;
-            for (int q = 0; q < S; ++q) {
-                int32_t v = 0;
-#pragma unroll
-                for (int p = P - 1; p >= 0; --p)
-                    v = twice_plus_bit(v, pw[q * P + p]);
-                cnt += v;
-            }
+            int q = 0;
+            const int32_t cnt =
+                add_splits<P, (P <= 8 ? 4 : 2)>(pw, q, S) + add_splits<P, 1>(pw, q, S);
             tile[lane * cs + ii] = cnt;
             if (cnt > best) {
                 best = cnt;
