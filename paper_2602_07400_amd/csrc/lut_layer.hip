@@ -6,7 +6,8 @@
 // App. C.1 "Bit-packed inference").  On packed words this is a Shannon
 // expansion: the 2^k table entries become all-0 / all-1 masks and k levels
 // of bitwise multiplexers, level i selected by input word i, fold them to
-// one word -- 2^k - 1 v_bfi_b32 per 32 samples, no per-sample work.
+// one word -- 2^k - 1 v_bitop3_b32 (table 0xCA) per 32 samples, no
+// per-sample work.
 //
 // Mapping (K = fan-in, LPN lanes per node, R words per lane):
 //  * a wave holds 64/LPN nodes; the LPN lanes of a node cover a window of
@@ -20,8 +21,10 @@
 // Locality: input rows are gathered at random (fixed random routing has no
 // spatial locality), so the cache working set of one window is w_in rows x
 // window bytes.  Windows are dealt to the 8 XCDs round-robin and each XCD
-// walks all node blocks of one window before the next, so that slab stays in
-// that XCD's L2 while every node reading it runs.
+// walks all node blocks of one window before the next.  A slab of up to
+// ~32k rows (4 MB at 128 bytes a row) stays in that XCD's L2 while every
+// node reading it runs; a 64000-row slab (8.2 MB) does not, and its rows are
+// fetched about four times from HBM and the MALL.
 #include "bl_device.h"
 
 namespace bl {
