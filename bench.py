@@ -80,6 +80,9 @@ def parse():
     ap.add_argument("--specialize", action="store_true",
                     help="evaluate the network from its specialized tables (tied and "
                          "ignored inputs removed, nodes ordered by effective fan-in)")
+    ap.add_argument("--power-seconds", type=float, default=0.0,
+                    help="also run forwards back to back for this long while amd-smi samples "
+                         "the board's socket power and engine clocks (detail.power)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run a write-only fill and a read-only sum over this many MiB "
                          "(reference kernels for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE)")
@@ -128,6 +131,69 @@ def cpu_model() -> str:
     except OSError:
         pass
     return ""
+
+
+def _smi_sample():
+    """One amd-smi reading: (socket power W, [engine clock MHz per XCD], memory clock MHz)."""
+    import subprocess
+    r = subprocess.run(["amd-smi", "metric", "--power", "--clock", "--json"],
+                       capture_output=True, text=True, timeout=20)
+    g = json.loads(r.stdout)["gpu_data"][0]
+
+    def num(v):
+        v = v.get("value") if isinstance(v, dict) else v
+        return float(v) if isinstance(v, (int, float)) else None
+
+    clk = g["clock"]
+    gfx = [num(clk[k]["clk"]) for k in sorted(clk) if k.startswith("gfx_")]
+    mem = num(clk["mem_0"]["clk"]) if "mem_0" in clk else None
+    return num(g["power"]["socket_power"]), [c for c in gfx if c is not None], mem
+
+
+def power_under_load(step, seconds):
+    """Run step() back to back for `seconds` while a thread samples amd-smi."""
+    import threading
+    samples, errors = [], []
+    stop = threading.Event()
+
+    def sampler():
+        while not stop.is_set():
+            try:
+                samples.append((time.perf_counter(),) + _smi_sample())
+            except Exception as e:            # tool missing or output not understood
+                errors.append(repr(e))
+                return
+            stop.wait(0.2)
+
+    import numpy as np
+    import torch
+    th = threading.Thread(target=sampler, daemon=True)
+    t0 = time.perf_counter()
+    th.start()
+    n = 0
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(50):
+            step()
+        torch.cuda.synchronize()
+        n += 50
+    t1 = time.perf_counter()
+    stop.set()
+    th.join()
+    use = [s for s in samples if t0 + 1.0 <= s[0] <= t1]      # after a second of load
+    if not use:
+        return {"error": errors[0] if errors else "no amd-smi sample under load"}
+    watts = [s[1] for s in use if s[1] is not None]
+    gfx = [c for s in use for c in s[2]]
+    mem = [s[3] for s in use if s[3] is not None]
+    return {"seconds": round(t1 - t0, 2), "forwards": n,
+            "ms_per_forward": round((t1 - t0) / n * 1e3, 4), "samples": len(use),
+            "socket_power_W_median": float(np.median(watts)) if watts else None,
+            "socket_power_W_range": [min(watts), max(watts)] if watts else None,
+            "gfx_clock_MHz_median": float(np.median(gfx)) if gfx else None,
+            "gfx_clock_MHz_range": [min(gfx), max(gfx)] if gfx else None,
+            "mem_clock_MHz_median": float(np.median(mem)) if mem else None,
+            "source": "amd-smi metric --power --clock --json, every ~0.2 s after the first "
+                      "second of back-to-back forwards; engine clocks of all XCDs"}
 
 
 def measured_traffic(stage):
@@ -248,6 +314,12 @@ def main():
             sums += [ev[i].elapsed_time(ev[i + 1]) for i in range(len(names))]
     stage_ms = dict(zip(names, (sums / ksteps).tolist()))
     plan = model.plan(n)
+
+    # ---- board power and engine clocks under a sustained load of the forward
+    power = None
+    if args.power_seconds > 0:
+        power = power_under_load(step, args.power_seconds)
+        print(f"[bench] power under load: {power}", file=sys.stderr, flush=True)
 
     # ---- on-device peaks, after the timed work: probes with the hot path's
     # instruction and access types (v_bitop3_b32 chains; 16-byte non-temporal
@@ -445,6 +517,8 @@ def main():
         "gpu": torch.cuda.get_device_name(dev),
         "hip": torch.version.hip,
     }
+    if power is not None:
+        detail["power"] = power
 
     # ---- CPU oracle on a bounded sample of the same workload
     cpu = None
