@@ -534,8 +534,18 @@ __device__ __forceinline__ void bs_add(uint32_t (&acc)[NP], const uint32_t (&v)[
     }
 }
 
+// The specialized kernel at 6 inputs dispatches over every fan-in up to 6 and
+// does not fit 128 VGPRs: held to 4 waves per SIMD it spilled 80 bytes per
+// lane and its layer ran 2.00 ms on C4 forced through it, against 1.50 ms at
+// 3 waves per SIMD (138 VGPRs, no spills; ABBA runs).
+template <int K, bool SPEC>
+constexpr int head_min_waves()
+{
+    return (SPEC && K == 6) ? 3 : BL_HEAD_MINWAVES;
+}
+
 template <int K, int P, bool SPEC>
-__global__ __launch_bounds__(kThreads, BL_HEAD_MINWAVES) void k_lut_slab_head(
+__global__ __launch_bounds__(kThreads, (head_min_waves<K, SPEC>())) void k_lut_slab_head(
     const uint64_t *__restrict__ in, int32_t w_in, const int32_t *__restrict__ conn,
     const uint64_t *__restrict__ tables, int32_t g, int32_t nb, int32_t n_nblk,
     int32_t n_slabs, int64_t W, int32_t c, int32_t splits, uint64_t *__restrict__ planes,
