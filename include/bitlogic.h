@@ -70,6 +70,13 @@
  *   BITLOGIC_UNFUSED_HEAD=1   the forward stores the last layer's bits and
  *                             runs the separate head kernels instead of the
  *                             last layer fused with the GroupSum counting.
+ *   BITLOGIC_JUMP_LAYER=0     every stored layer runs on the per-lane
+ *                             multiplexer kernel, none on the node-per-wave
+ *                             kernel (bitlogic_forward_info.jump_layers);
+ *                       =1    the node-per-wave kernel runs every stored,
+ *                             unspecialized layer of fan-in 5 or 6 when the
+ *                             batch fills an even number of 1024-sample slabs,
+ *                             also where it is not the faster kernel.
  */
 #ifndef BITLOGIC_H
 #define BITLOGIC_H
@@ -157,6 +164,11 @@ typedef struct bitlogic_forward_info {
                                  written to memory                                */
     int32_t head_splits;      /* partial counters per (sample word, class)       */
     int32_t head_planes;      /* bit planes per partial counter                  */
+    uint32_t jump_layers;     /* bit l (l < 32): layer l is stored by the
+                                 node-per-wave kernel whose table bytes select
+                                 prebuilt 3-input leaves (fan-in 5 or 6, input
+                                 slab pair within the L2); other stored layers
+                                 use the per-lane multiplexer kernel          */
 } bitlogic_forward_info;
 
 int bitlogic_forward_plan(int64_t n_samples, int32_t n_features, int32_t n_thresholds,
@@ -489,8 +501,10 @@ const char *bitlogic_last_error(void);
  * bitlogic_network_forward_noalloc, and bitlogic_probe_hbm in
  * place of the copy-only probe; 0.6.0 bitlogic_forward_info without the
  * fused_network member (the whole-network kernel was removed), and the
- * instruction-rate and gather probes). */
-#define BITLOGIC_VERSION 600
+ * instruction-rate and gather probes; 0.7.0 bitlogic_forward_info.jump_layers
+ * and the node-per-wave layer kernel, whose per-node records enlarge the
+ * forward workspace of networks that use it). */
+#define BITLOGIC_VERSION 700
 int bitlogic_version(void);
 
 #ifdef __cplusplus

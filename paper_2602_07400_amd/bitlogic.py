@@ -46,7 +46,7 @@ class BitlogicError(RuntimeError):
 class _ForwardInfo(ctypes.Structure):
     _fields_ = [("workspace_bytes", ctypes.c_size_t), ("slab_words", ctypes.c_int32),
                 ("fused_head", ctypes.c_int32), ("head_splits", ctypes.c_int32),
-                ("head_planes", ctypes.c_int32)]
+                ("head_planes", ctypes.c_int32), ("jump_layers", ctypes.c_uint32)]
 
 
 class _Layer(ctypes.Structure):
@@ -590,7 +590,9 @@ class BitlogicModel:
                                                     ctypes.byref(info)))
         return {"workspace_bytes": int(info.workspace_bytes), "slab_words": int(info.slab_words),
                 "fused_head": bool(info.fused_head), "head_splits": int(info.head_splits),
-                "head_planes": int(info.head_planes)}
+                "head_planes": int(info.head_planes),
+                "jump_layers": [l for l in range(min(len(self.layers), 32))
+                                if (int(info.jump_layers) >> l) & 1]}
 
     def forward(self, x: torch.Tensor, out: Optional[torch.Tensor] = None,
                 argmax: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,

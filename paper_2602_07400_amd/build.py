@@ -13,7 +13,7 @@ INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 LIB = os.path.join(HERE, "libbitlogic.so")
 OBJ_DIR = os.path.join(HERE, "_build")
 
-SOURCES = ["encode.hip", "lut_layer.hip", "head.hip", "fit.hip", "specialize.hip",
+SOURCES = ["encode.hip", "lut_layer.hip", "lut_jump.hip", "head.hip", "fit.hip", "specialize.hip",
            "probes.hip", "api.hip"]
 
 HIPCC_FLAGS = [

@@ -5,6 +5,7 @@
 #include <stdio.h>
 #include <stdlib.h>
 
+#include <algorithm>
 #include <atomic>
 #include <mutex>
 
@@ -112,6 +113,20 @@ bool fused_head_enabled()
     return !(e && e[0] == '1');
 }
 
+// BITLOGIC_JUMP_LAYER=0 keeps every stored layer on the per-lane slab kernel,
+// =1 runs the node-per-wave kernel wherever it can (also where it is not the
+// faster choice); unset, it runs where it is faster.  Results are identical.
+enum JumpMode { kJumpOff, kJumpAuto, kJumpForced };
+JumpMode jump_mode()
+{
+    const char *e = getenv("BITLOGIC_JUMP_LAYER");
+    if (e && e[0] == '0')
+        return kJumpOff;
+    if (e && e[0] == '1')
+        return kJumpForced;
+    return kJumpAuto;
+}
+
 // bitlogic_forward keeps its encoded and intermediate bit tensors in the slab
 // layout [Wp / S][rows][S] (S = kSlabWords, Wp = W rounded up to whole slabs),
 // which bounds the LUT-layer gathers' per-XCD working set (see lut_layer.hip).
@@ -122,6 +137,8 @@ struct ForwardPlan {
     size_t off_enc, off_a, off_b, off_head, total;
     bl::HeadPlan head;
     bool fused;            // last layer + head in one kernel
+    uint64_t jump_mask;    // bit l: layer l runs on the node-per-wave kernel
+    size_t off_rec;        // its per-node records (shared by those layers)
 };
 
 bitlogic_network legacy_net(int32_t n_features, const uint8_t *thresholds, int32_t n_thresholds,
@@ -129,7 +146,7 @@ bitlogic_network legacy_net(int32_t n_features, const uint8_t *thresholds, int32
                             const int8_t *dsp_weights);
 
 int plan_forward(int64_t n, int32_t d, int32_t b, const bitlogic_layer *layers, int32_t L,
-                 int32_t c, ForwardPlan *fp)
+                 int32_t c, const uint8_t *const *pass_fanin, ForwardPlan *fp)
 {
     if (!layers)
         return fail(BITLOGIC_ERR_NULL, "forward: NULL layer array");
@@ -179,7 +196,26 @@ int plan_forward(int64_t n, int32_t d, int32_t b, const bitlogic_layer *layers, 
     fp->off_a = round_up(enc);
     fp->off_b = fp->off_a + (need_a ? round_up(act) : 0);
     fp->off_head = fp->off_b + (need_b ? round_up(act) : 0);
-    fp->total = fp->off_head + round_up(fp->head.ws_bytes);
+    // stored, unspecialized layers of fan-in 5 or 6 whose input slab pair
+    // fits the L2 run with a node per wave (lut_jump.hip); they share one
+    // record array, sized for the widest of them
+    fp->jump_mask = 0;
+    int32_t rec_w = 0;
+    int32_t w_in = d * b;
+    const JumpMode jm = jump_mode();
+    for (int32_t l = 0; l < L; ++l) {
+        const bool last_fused = fp->fused && l == L - 1;
+        const bool spec = pass_fanin && pass_fanin[l];
+        if (l < 64 && !last_fused && !spec && jm != kJumpOff &&
+            bl::jump_layer_fits(w_in, layers[l].w_out, layers[l].k, fp->n_slabs,
+                                jm == kJumpForced)) {
+            fp->jump_mask |= 1ull << l;
+            rec_w = std::max(rec_w, layers[l].w_out);
+        }
+        w_in = layers[l].w_out;
+    }
+    fp->off_rec = fp->off_head + round_up(fp->head.ws_bytes);
+    fp->total = fp->off_rec + (fp->jump_mask ? round_up(bl::jump_records_bytes(rec_w)) : 0);
     return BITLOGIC_OK;
 }
 
@@ -252,8 +288,8 @@ size_t bitlogic_forward_workspace_bytes(int64_t n_samples, int32_t n_features,
                                         int32_t n_layers, int32_t n_classes)
 {
     ForwardPlan fp;
-    if (plan_forward(n_samples, n_features, n_thresholds, layers, n_layers, n_classes, &fp) !=
-        BITLOGIC_OK)
+    if (plan_forward(n_samples, n_features, n_thresholds, layers, n_layers, n_classes, nullptr,
+                     &fp) != BITLOGIC_OK)
         return 0;
     return fp.total;
 }
@@ -307,7 +343,7 @@ int plan_network(const bitlogic_network *net, int64_t n, ForwardPlan *fp)
     if (st != BITLOGIC_OK)
         return st;
     st = plan_forward(n, net->n_features, net->n_bits, net->layers, net->n_layers,
-                      net->n_classes, fp);
+                      net->n_classes, net->pass_fanin, fp);
     if (st != BITLOGIC_OK)
         return st;
     return BITLOGIC_OK;
@@ -368,6 +404,7 @@ int forward_impl(const bitlogic_network *net, const uint8_t *x, int64_t n_sample
     const uint64_t *cur = enc;
     int32_t w_in = net->n_features * net->n_bits;
     uint64_t *planes = reinterpret_cast<uint64_t *>(ws + fp.off_head);
+    uint32_t *rec = reinterpret_cast<uint32_t *>(ws + fp.off_rec);
     for (int32_t l = 0; l < n_layers; ++l) {
         const bool last_fused = fp.fused && l == n_layers - 1;
         uint64_t *dst = act[l & 1];
@@ -376,6 +413,9 @@ int forward_impl(const bitlogic_network *net, const uint8_t *x, int64_t n_sample
             e = bl::launch_lut_slab_head(cur, w_in, fp.n_slabs, layers[l].conn, layers[l].tables,
                                          layers[l].w_out, layers[l].k, n_classes, fp.W, planes,
                                          fp.head.planes, s, fanin);
+        else if ((fp.jump_mask >> l) & 1)
+            e = bl::launch_jump_layer(cur, w_in, fp.n_slabs, layers[l].conn, layers[l].tables,
+                                      layers[l].w_out, layers[l].k, dst, rec, s);
         else
             e = bl::launch_lut_layer_slab(cur, w_in, fp.n_slabs, layers[l].conn,
                                           layers[l].tables, layers[l].w_out, layers[l].k, dst, s,
@@ -510,6 +550,7 @@ int bitlogic_network_plan(const bitlogic_network *net, int64_t n_samples,
     info->fused_head = fp.fused ? 1 : 0;
     info->head_splits = fp.head.splits;
     info->head_planes = fp.head.planes;
+    info->jump_layers = (uint32_t)(fp.jump_mask & 0xFFFFFFFFu);
     return ok();
 }
 

@@ -99,6 +99,27 @@ void specialize_network(int32_t w_in, int32_t L, const int32_t *w, const int32_t
                         int32_t *const *conn_out, uint64_t *const *tables_out,
                         uint8_t *const *fanin_out, int32_t *const *order_out);
 
+// Node-per-wave LUT layer with jump-table leaves (lut_jump.hip), fan-in 5 or
+// 6, slab layout.  Its prep step writes one kJumpRecBytes record per node
+// (and kJumpPadRecs past the last) into `rec` (jump_records_bytes(w_out)
+// bytes, 128-byte aligned), then the layer runs; both on `stream`.
+// jump_layer_fits: the kernel can run the layer (fan-in 5 or 6, an even slab
+// count, rows within 2^23) and, unless `forced`, is the faster choice (the
+// input slab pair, w_in * 256 bytes, within kJumpMaxPairBytes, and at least
+// kJumpMinBlocks blocks).
+constexpr int kJumpRecBytes = 128;
+constexpr int kJumpPadRecs = 2;
+constexpr int kJumpNodesPerWave = 16;
+constexpr int kJumpNodesPerBlock = 4 * kJumpNodesPerWave;
+constexpr int64_t kJumpMaxPairBytes = 3 << 20;
+constexpr int32_t kJumpMaxRows = 1 << 23;
+constexpr int64_t kJumpMinBlocks = 4096;
+bool jump_layer_fits(int32_t w_in, int32_t w_out, int32_t k, int64_t n_slabs, bool forced);
+size_t jump_records_bytes(int32_t w_out);
+hipError_t launch_jump_layer(const uint64_t *in, int32_t w_in, int64_t n_slabs,
+                             const int32_t *conn, const uint64_t *tables, int32_t w_out,
+                             int32_t k, uint64_t *out, uint32_t *rec, hipStream_t stream);
+
 // Last LUT layer fused with the GroupSum head (slab layout): writes the head's
 // bit planes instead of the layer's bits.  fused_head_nodes(g, c, n_slabs) is the
 // node count nb of one block (a multiple of 64; a class group of g nodes takes
