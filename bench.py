@@ -24,7 +24,10 @@ Prints ONE JSON line.  Besides the driver's fields it carries
 Algorithmic work follows the path the library takes (bitlogic_forward_plan):
 when the last LUT layer is fused with the GroupSum head its output bits are
 never stored, so that stage's compulsory bytes are its input only and the
-head's counting is charged to it.
+head's counting is charged to it; a layer that the node-per-wave kernel runs
+(table-selected 3-input leaves, plan "jump_layers") is charged its 15
+lane-ops per node and 32 samples instead of the 2^k - 1 multiplexers, which
+puts it on its byte roofline.
 """
 from __future__ import annotations
 
@@ -89,10 +92,13 @@ def parse():
     return ap.parse_args()
 
 
-def algorithmic(cfg, n, fused_head, binary_bits=0, fanin_hist=None):
+def algorithmic(cfg, n, fused_head, binary_bits=0, fanin_hist=None, jump_layers=()):
     """Compulsory bytes and algorithmic 32-bit lane-ops per stage of one forward.
     fanin_hist: per layer, None or the node count per effective fan-in 0..6 of
-    a specialized layer (its multiplexers: 2^k' - 1 per node)."""
+    a specialized layer (its multiplexers: 2^k' - 1 per node).
+    jump_layers: layers the node-per-wave kernel evaluates with table-selected
+    3-input leaves: 8 leaves + 7 multiplexers = 15 lane-ops per node and 32
+    samples instead of 2^k - 1, which leaves such a layer bound by its bytes."""
     W = (n + 63) // 64
     D0 = cfg.d * (binary_bits or cfg.b)
     st = {"encode": {"bytes": n * cfg.d + D0 * W * 8, "ops": n * D0}}
@@ -103,6 +109,8 @@ def algorithmic(cfg, n, fused_head, binary_bits=0, fanin_hist=None):
         h = fanin_hist[l] if fanin_hist else None
         muxes = (((1 << cfg.k) - 1) * w if h is None else
                  sum(int(c) * ((1 << q) - 1) for q, c in enumerate(h)))
+        if l in jump_layers:
+            muxes = JUMP_OPS_PER_NODE * w
         st[f"layer{l + 1}"] = {
             # a fused last layer reads its input and hands counts to the head
             "bytes": (w_in + (0 if last_fused else w)) * W * 8,
@@ -215,8 +223,11 @@ def measured_traffic(stage):
         return None
 
 
+JUMP_OPS_PER_NODE = 15      # 8 table-selected v_bitop3_b32 leaves + 7 multiplexers
 STAGE_KERNELS = {"encode": "k_encode_t / k_encode_ballot (encoder + bit-pack)",
                  "layer": "k_lut_slab (LUT layer)",
+                 "layer_jump": "k_jump_prep + k_jump_layer (LUT layer, a node per wave, "
+                               "table-selected bitop3 leaves)",
                  "layer_fused": "k_lut_slab_head (last LUT layer fused with GroupSum counting)",
                  "head_fused": "k_head_finish (counts -> scores, argmax)",
                  "head": "k_head_planes + k_head_finish (GroupSum head, argmax)"}
@@ -459,7 +470,8 @@ def main():
                   "frac_of_hbm_peak": round(n * cfg.d / (fit_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
 
     fused = plan["fused_head"]
-    alg = algorithmic(cfg, n, fused, binary_bits, model.fanin_histogram)
+    jump = plan.get("jump_layers", [])
+    alg = algorithmic(cfg, n, fused, binary_bits, model.fanin_histogram, jump)
     roof_sum = sum(v["roof_ms"] for v in alg.values())
     # dominant kernel: the stage with the longest launch
     dom = max(names, key=lambda k: stage_ms[k])
@@ -476,6 +488,8 @@ def main():
         kname = STAGE_KERNELS["head_fused" if fused else "head"]
     elif dom == layer_names[-1] and fused:
         kname = STAGE_KERNELS["layer_fused"]
+    elif layer_names.index(dom) in jump:
+        kname = STAGE_KERNELS["layer_jump"]
     else:
         kname = STAGE_KERNELS["layer"]
     if model.pass_fanin and dom in layer_names:
@@ -498,6 +512,7 @@ def main():
         "forward_roofline_frac": round(roof_sum / ms_per_step, 4),
         "staged_sum_ms": round(sum(stage_ms.values()), 4),
         "fused_head": fused,
+        "jump_layers": [layer_names[l] for l in jump],
         "specialized": bool(args.specialize),
         "fanin_histogram": ([None if h is None else [int(v) for v in h]
                              for h in model.fanin_histogram]
@@ -508,6 +523,13 @@ def main():
         "fit_quantile_thresholds": fit_detail,
         "layer_frac_of_valu_peak": {k: round(alg[k]["ops"] / (stage_ms[k] * 1e-3) / 1e12
                                              / PEAK_VALU_TOPS, 4) for k in layer_names},
+        # the row segments the layers gather (k per node, each read whole), and
+        # the rate at which each layer moves them from the caches: the path that
+        # binds the k = 6 layers (compare measured_peaks.gather_TBs)
+        "layer_gathered_GB": {k: round(cfg.k * w * n / 8 / 1e9, 3)
+                              for k, w in zip(layer_names, cfg.widths)},
+        "layer_gather_TBs": {k: round(cfg.k * w * n / 8 / (stage_ms[k] * 1e-3) / 1e12, 2)
+                             for k, w in zip(layer_names, cfg.widths)},
         "measured_peaks": peaks,
         "dominant_frac_of_measured_peak": (
             None if peaks is None else
