@@ -138,3 +138,58 @@ def test_default_plan_of_each_configuration(name, expect):
     with jump_switch(None):
         plan = model.plan(CONFIGS[name].n)
     assert plan["jump_layers"] == expect, plan
+
+
+def draw_jump_case(seed):
+    # seeded networks whose hidden layers the node-per-wave kernel takes when
+    # forced: an even number of slabs, hidden fan-ins 5 or 6, and otherwise
+    # mixed widths, depths, encoders, heads, class groups and repeats
+    rng = np.random.default_rng(5000 + seed)
+    n = 1024 * int(rng.choice([2, 4, 6, 8, 18, 64])) - int(rng.choice([0, 0, 1, 63, 500]))
+    d = int(rng.integers(1, 300))
+    binary = bool(rng.random() < 0.3)
+    b = int(rng.integers(1, 9)) if binary else int(rng.choice([1, 2, 3, 7]))
+    depth = int(rng.integers(2, 5))
+    c = int(rng.choice([1, 3, 10, 17, 100]))
+    g = int(rng.choice([1, 7, 64, 100, 333]))
+    while c * g > 12000:
+        g //= 2
+    widths = [int(rng.integers(1, 4000)) for _ in range(depth - 1)] + [c * g]
+    ks = [int(rng.choice([5, 6])) for _ in range(depth - 1)] + [int(rng.integers(1, 7))]
+    return dict(seed=seed, n=n, d=d, binary=binary, b=b, widths=widths, ks=ks, c=c,
+                dsp=bool(rng.random() < 0.25), repeats=bool(rng.random() < 0.3))
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_random_networks_forced_onto_the_node_per_wave_kernel(seed):
+    case = draw_jump_case(seed)
+    print("[case]", case, flush=True)
+    rng = np.random.default_rng(6000 + seed)
+    n, d, b, c = case["n"], case["d"], case["b"], case["c"]
+    x = rng.integers(0, 256, size=(n, d), dtype=np.uint8)
+    th = None if case["binary"] else rng.integers(0, 256, size=(d, b), dtype=np.uint8)
+    layers, w_in = [], d * b
+    for w, k in zip(case["widths"], case["ks"]):
+        if case["repeats"] or k > w_in:
+            conn = rng.integers(0, w_in, size=(w, k))
+        else:
+            conn = np.stack([rng.choice(w_in, size=k, replace=False) for _ in range(w)])
+        tables = rng.integers(0, 1 << 63, size=w, dtype=np.int64).astype(np.uint64)
+        tables |= rng.integers(0, 2, size=w).astype(np.uint64) << np.uint64(63)
+        layers.append((conn.astype(np.int32), tables))
+        w_in = w
+    q = rng.integers(-128, 128, size=(c, c), dtype=np.int16).astype(np.int8) if case["dsp"] else None
+    kw = (dict(encoder="binary", n_features=d, n_bits=b) if case["binary"] else {})
+    model = bl.BitlogicModel.from_numpy(th, layers, c, device=DEV, head_weights=q, **kw)
+    with jump_switch("1"):
+        plan = model.plan(n)
+        s, p = model.forward(torch.from_numpy(x).to(DEV))
+        torch.cuda.synchronize()
+    hidden = list(range(len(layers) - 1)) if plan["fused_head"] else list(range(len(layers)))
+    assert plan["jump_layers"] == [l for l in hidden if case["ks"][l] in (5, 6)], plan
+    rs, rp = oracle.forward(x, th, layers, c, binary_bits=b if case["binary"] else 0)
+    if q is not None:
+        rs, rp = oracle.grouped_dsp(rs, q)
+    s, p = s.cpu().numpy(), p.cpu().numpy()
+    bad = np.nonzero((s != rs).any(axis=1) | (p != rp))[0]
+    assert bad.size == 0, f"{bad.size} of {n} samples differ, first {bad[:8]}"
