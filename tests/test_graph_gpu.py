@@ -85,3 +85,16 @@ def test_graph_replay_specialized():
     assert model.pass_fanin is not None
     _replays(model, wl, lambda xs: oracle.forward(xs, wl.thresholds, wl.layers, wl.n_classes),
              1500)
+
+
+def test_graph_replay_node_per_wave_layer(monkeypatch):
+    # layer 1 on the node-per-wave kernel (forced at this batch): the capture
+    # holds its record kernel, so every replay rebuilds the records it jumps
+    # through, and the eager forwards between replays use the same workspace
+    # layout in their own buffers
+    monkeypatch.setenv("BITLOGIC_JUMP_LAYER", "1")
+    wl = make_workload("c3_cifar10", seed=24, n=4096)
+    model = bl.BitlogicModel.from_numpy(wl.thresholds, wl.layers, wl.n_classes, device=DEV)
+    assert model.plan(4096)["jump_layers"] == [0]
+    _replays(model, wl, lambda xs: oracle.forward(xs, wl.thresholds, wl.layers, wl.n_classes),
+             4096)
