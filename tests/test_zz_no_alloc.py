@@ -52,6 +52,24 @@ def test_noalloc_matches_workspace_forward_twice(name, n1, n2):
         assert np.array_equal(gs, os_) and np.array_equal(gp, op), f"{name} n={n}: oracle"
 
 
+def test_noalloc_with_the_node_per_wave_layer(monkeypatch):
+    # layer 1 forced onto the node-per-wave kernel: its per-node records live
+    # in the static scratch too, and the second, smaller call (4 slabs, then
+    # 2) rebuilds them over what the first call left
+    monkeypatch.setenv("BITLOGIC_JUMP_LAYER", "1")
+    n1, n2 = 64 * 16 * 4, 64 * 16 * 2
+    wl = make_workload("c3_cifar10", seed=7, n=n1)
+    model = _model(wl)
+    x = torch.from_numpy(wl.x).to(DEV)
+    assert model.plan(n1)["jump_layers"] == [0]
+    assert model.workspace_bytes(n1) <= bl.NOALLOC_SCRATCH_BYTES
+    for n in (n1, n2):
+        rs, rp, gs, gp = _both(model, x[:n])
+        assert np.array_equal(gs, rs) and np.array_equal(gp, rp), f"n={n}: noalloc differs"
+        os_, op = oracle.forward(wl.x[:n], wl.thresholds, wl.layers, wl.n_classes)
+        assert np.array_equal(gs, os_) and np.array_equal(gp, op), f"n={n}: oracle"
+
+
 def test_noalloc_quantized_head_and_argmax_only():
     wl = make_workload("c1_mnist_tiny", seed=6, n=3000)
     rng = np.random.default_rng(6)
