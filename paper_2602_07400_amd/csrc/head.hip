@@ -138,7 +138,18 @@ __global__ __launch_bounds__(kThreads) void k_head_finish(
     extern __shared__ uint64_t buf[];                 // buf_words words
     __shared__ int32_t part[2][finish::kWaves][kWave];
     (void)buf_words;
+    // Touch each 128-byte line of the column's planes with one vector load
+    // per thread before the count loop.  The lines then arrive together, and
+    // the loop's scalar loads, issued a few classes at a time, hit the L2
+    // instead of waiting for memory once per batch.  The load is consumed
+    // only after the column (into partials nothing reads any more), so it
+    // stays in flight meanwhile.  Every thread loads (clamped index): under a
+    // divergent branch the compiler reads the planes with vector loads.
+    const int64_t nw = (int64_t)c * S * P;
+    const int64_t e = min((int64_t)threadIdx.x * 16, nw - 1);
+    const uint32_t touch = reinterpret_cast<const uint32_t *>(planes + blockIdx.x * nw + e)[0];
     finish::column_scalar<P>(planes, blockIdx.x, n, c, S, cs, buf, part, scores, argmax);
+    part[0][threadIdx.x / kWave][threadIdx.x % kWave] ^= (int32_t)touch;
 }
 
 // ---------------------------------------------------------------------------
