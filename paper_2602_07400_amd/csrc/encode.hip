@@ -47,7 +47,7 @@ using dev::transpose_consts;
 constexpr int kThreads = 256;
 
 #ifndef BL_ENC_TPB
-#define BL_ENC_TPB 4
+#define BL_ENC_TPB 2
 #endif
 #ifndef BL_ENC_NT_STORE
 #define BL_ENC_NT_STORE 1
@@ -374,7 +374,8 @@ hipError_t launch_t(const uint8_t *x, int64_t n, int32_t d, const uint8_t *th, u
     const int32_t n_ftiles = (d + G::kFT - 1) / G::kFT;
     // enough blocks to fill the chip; at most BL_ENC_TPB column tiles reuse one
     // code table (longer runs let the blocks that share pixel lines drift
-    // apart, and the lines are fetched again)
+    // apart, and the lines are fetched again: 2 tiles a block beat 1, 3, 4
+    // and 8 on 256K-1M samples x 784-3072 features)
     int64_t tpb = n_tiles * n_ftiles / 2048;
     tpb = tpb < 1 ? 1 : (tpb > BL_ENC_TPB ? BL_ENC_TPB : tpb);
     // small batches: split each tile's 16 columns over 2 or 4 blocks (down to
