@@ -11,9 +11,13 @@
 // the group's ladder.
 //
 // k_fit_hist: each block counts a run of rows into an LDS histogram per
-// group (LDS atomics), then adds it into the global 64-bit histogram.  Rows
-// are read as coalesced dwords: a thread keeps its columns (and their
-// groups) and walks the rows, eight rows' loads at a time.  k_fit_select:
+// group (LDS atomics), then adds it into the global 64-bit histogram.  The
+// LDS histogram holds R interleaved copies of every bin (lane l counts into
+// copy l mod R, at word bin * R + l mod R), so that the 64 atomics of a wave
+// spread over the banks and rarely hit the same word; the copies are summed
+// before the global add.  Rows are read as coalesced dwords: a thread keeps
+// its columns (and their groups) and walks the rows, kRowUnroll rows' loads
+// at a time.  k_fit_select:
 // one block per group turns the histogram into the ladder (a block prefix sum,
 // one thread per bin).
 #include "bl_internal.h"
@@ -23,7 +27,15 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kHistBlocks = 1024;
-constexpr int kRowUnroll = 8;
+#ifndef BL_FIT_UNROLL
+#define BL_FIT_UNROLL 32
+#endif
+#ifndef BL_FIT_MAX_REP
+#define BL_FIT_MAX_REP 32
+#endif
+constexpr int kRowUnroll = BL_FIT_UNROLL;
+constexpr int kFitMaxRep = BL_FIT_MAX_REP;        // copies of each histogram bin
+constexpr int kFitHistBytes = 48 << 10;           // LDS of one histogram block
 
 __global__ __launch_bounds__(kThreads) void k_fit_clear(uint64_t *__restrict__ ws, int32_t n)
 {
@@ -34,12 +46,16 @@ __global__ __launch_bounds__(kThreads) void k_fit_clear(uint64_t *__restrict__ w
 
 __global__ __launch_bounds__(kThreads) void k_fit_hist(
     const uint8_t *__restrict__ x, int64_t n, int32_t d, int32_t per, int32_t n_groups,
-    int64_t rows_per_block, int aligned4, uint64_t *__restrict__ ws)
+    int64_t rows_per_block, int aligned4, int32_t rep_log2, uint64_t *__restrict__ ws)
 {
-    extern __shared__ uint32_t hist[];             // [n_groups][256]
-    for (int i = threadIdx.x; i < n_groups * 256; i += kThreads)
+    extern __shared__ uint32_t hist[];             // [n_groups][256][R], R = 2^rep_log2
+    const int nbins = n_groups * 256;
+    for (int i = threadIdx.x; i < nbins << rep_log2; i += kThreads)
         hist[i] = 0;
     __syncthreads();
+    const uint32_t copy = threadIdx.x & ((1u << rep_log2) - 1);
+    // LDS word of bin (g256 + v) in this lane's copy
+    auto slot = [&](int g256, uint32_t v) { return (((uint32_t)g256 + v) << rep_log2) + copy; };
     const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
     const int64_t r1 = min(n, r0 + rows_per_block);
     if (aligned4) {
@@ -61,13 +77,13 @@ __global__ __launch_bounds__(kThreads) void k_fit_hist(
                 for (int q = 0; q < kRowUnroll; ++q)
 #pragma unroll
                     for (int u = 0; u < 4; ++u)
-                        atomicAdd(&hist[g[u] + ((v[q] >> (8 * u)) & 0xFFu)], 1u);
+                        atomicAdd(&hist[slot(g[u], (v[q] >> (8 * u)) & 0xFFu)], 1u);
             }
             for (; r < r1; ++r) {
                 const uint32_t v = x32[r * d4 + fq];
 #pragma unroll
                 for (int u = 0; u < 4; ++u)
-                    atomicAdd(&hist[g[u] + ((v >> (8 * u)) & 0xFFu)], 1u);
+                    atomicAdd(&hist[slot(g[u], (v >> (8 * u)) & 0xFFu)], 1u);
             }
         }
     } else {
@@ -81,17 +97,23 @@ __global__ __launch_bounds__(kThreads) void k_fit_hist(
                     v[q] = x[(r + q) * d + f];
 #pragma unroll
                 for (int q = 0; q < kRowUnroll; ++q)
-                    atomicAdd(&hist[g + v[q]], 1u);
+                    atomicAdd(&hist[slot(g, v[q])], 1u);
             }
             for (; r < r1; ++r)
-                atomicAdd(&hist[g + x[r * d + f]], 1u);
+                atomicAdd(&hist[slot(g, x[r * d + f])], 1u);
         }
     }
     __syncthreads();
-    for (int i = threadIdx.x; i < n_groups * 256; i += kThreads)
-        if (hist[i])
-            atomicAdd(reinterpret_cast<unsigned long long *>(&ws[i]),
-                      (unsigned long long)hist[i]);
+    // sum the copies (each thread starts at another copy, so that the
+    // threads of a wave read different banks), then one global add per bin
+    const int nrep = 1 << rep_log2;
+    for (int i = threadIdx.x; i < nbins; i += kThreads) {
+        uint32_t sum = 0;
+        for (int k = 0; k < nrep; ++k)
+            sum += hist[((uint32_t)i << rep_log2) + ((uint32_t)(k + i) & (uint32_t)(nrep - 1))];
+        if (sum)
+            atomicAdd(reinterpret_cast<unsigned long long *>(&ws[i]), (unsigned long long)sum);
+    }
 }
 
 __global__ __launch_bounds__(kThreads) void k_fit_select(
@@ -154,9 +176,14 @@ hipError_t launch_fit_quantiles(const uint8_t *x, int64_t n, int32_t d, int32_t 
     if (blocks > 0x7fffffff)
         return hipErrorInvalidConfiguration;
     const int aligned4 = (d % 4 == 0) && ((uintptr_t)x % 4 == 0);
+    // as many bin copies as the block's LDS budget allows (at least one)
+    int32_t rep_log2 = 0;
+    while ((2 << rep_log2) <= kFitMaxRep &&
+           (size_t)bins * sizeof(uint32_t) * (2u << rep_log2) <= (size_t)kFitHistBytes)
+        ++rep_log2;
     hipLaunchKernelGGL(k_fit_hist, dim3((unsigned)blocks), dim3(kThreads),
-                       (size_t)bins * sizeof(uint32_t), stream, x, n, d, per, n_groups, rows,
-                       aligned4, ws);
+                       ((size_t)bins << rep_log2) * sizeof(uint32_t), stream, x, n, d, per,
+                       n_groups, rows, aligned4, rep_log2, ws);
     e = hipGetLastError();
     if (e != hipSuccess)
         return e;
