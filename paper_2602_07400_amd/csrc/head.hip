@@ -39,11 +39,7 @@ constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
 constexpr int kMaxPlanes = 16;
 constexpr int kDspMaxClasses = 128;   // logits stay below 2^31; tiles fit in LDS
-#ifndef BL_DSP_FINISH_BLOCKS
-#define BL_DSP_FINISH_BLOCKS 2048
-#endif
 constexpr int64_t kDspBlocks = 1024;  // blocks of the quantized head (4 per CU)
-constexpr int64_t kDspFinishBlocks = BL_DSP_FINISH_BLOCKS;   // measured best on C4: 2048
 
 __device__ __forceinline__ void csa(uint64_t &h, uint64_t &l, uint64_t a, uint64_t b,
                                     uint64_t c)
@@ -165,12 +161,12 @@ typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 // the products are in registers; and the argmax partials.
 struct DspLayout {
     int cn, ck, ckp;
-    size_t off_q, off_rs, off_lo, off_hi, off_tile, off_part, off_stage, bytes;
+    size_t off_q, off_rs, off_lo, off_hi, off_tile, off_part, bytes;
 };
 
-// stage_words: room for that many plane words (uint64) after the partials,
-// where the fused finish stages a column's planes (0: none)
-__host__ __device__ inline DspLayout dsp_layout(int c, int stage_words = 0)
+__host__ __device__ inline int dsp_tile_stride(int c) { return c | 1; }
+
+__host__ __device__ inline DspLayout dsp_layout(int c)
 {
     DspLayout L;
     L.cn = (c + 15) / 16 * 16;
@@ -182,46 +178,59 @@ __host__ __device__ inline DspLayout dsp_layout(int c, int stage_words = 0)
     L.off_hi = L.off_lo + (size_t)kWave * L.ckp;
     const size_t planes_end = L.off_hi + (size_t)kWave * L.ckp;
     L.off_tile = L.off_lo;
-    const size_t tile_end = L.off_tile + (size_t)kWave * c * 4;
+    const size_t tile_end = L.off_tile + (size_t)kWave * dsp_tile_stride(c) * 4;
     L.off_part = ((planes_end > tile_end ? planes_end : tile_end) + 15) / 16 * 16;
-    L.off_stage = L.off_part + 2 * kWaves * kWave * 4;
-    L.bytes = L.off_stage + (size_t)stage_words * 8;
+    L.bytes = L.off_part + 2 * kWaves * kWave * 4;
     return L;
 }
 
-// Stage Q (zero padded) and its row sums in LDS, once per block.  All
-// threads; ends with a barrier.  Q is read as whole dwords when c*c is a
-// multiple of 4 and the matrix is 4-byte aligned.
+// Stage Q (zero padded to [cn][ckp]) and its row sums in LDS.  All threads;
+// ends with a barrier.  Where c is a multiple of 4 and Q is 4-byte aligned,
+// each LDS dword of a row is one dword of Q's row (or zero past it), walked
+// without a division per dword; else byte by byte.
 __device__ __forceinline__ void dsp_stage_q(const int8_t *__restrict__ weights, int c,
                                             const DspLayout &L, uint8_t *smem)
 {
     int8_t *q = reinterpret_cast<int8_t *>(smem + L.off_q);
     int32_t *rs = reinterpret_cast<int32_t *>(smem + L.off_rs);
     uint32_t *q32 = reinterpret_cast<uint32_t *>(smem + L.off_q);
-    for (int e = threadIdx.x; e < L.cn * L.ckp / 4; e += kThreads)
-        q32[e] = 0;
-    __syncthreads();
-    const int cc = c * c;
-    if (cc % 4 == 0 && ((uintptr_t)weights % 4) == 0) {
+    const int rw = L.ckp / 4;                         // LDS dwords per row
+    if (c % 4 == 0 && ((uintptr_t)weights % 4) == 0) {
         const uint32_t *w32 = reinterpret_cast<const uint32_t *>(weights);
-        for (int e = threadIdx.x; e < cc / 4; e += kThreads) {
-            const uint32_t v = w32[e];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int f = 4 * e + u;
-                q[(f / c) * L.ckp + f % c] = (int8_t)(v >> (8 * u));
+        const int cw = c / 4;
+        int i = threadIdx.x / rw, j = threadIdx.x - i * rw;
+        const int di = kThreads / rw, dj = kThreads - di * rw;
+        for (int e = threadIdx.x; e < L.cn * rw; e += kThreads) {
+            q32[e] = (i < c && j < cw) ? w32[i * cw + j] : 0u;
+            i += di;
+            j += dj;
+            if (j >= rw) {
+                j -= rw;
+                ++i;
             }
         }
+        __syncthreads();
+        for (int r = threadIdx.x; r < L.cn; r += kThreads) {
+            int32_t sum = 0;
+            for (int k = 0; k < cw; ++k) {
+                const uint32_t v = q32[r * rw + k];
+                sum += (int8_t)v + (int8_t)(v >> 8) + (int8_t)(v >> 16) + (int8_t)(v >> 24);
+            }
+            rs[r] = sum;
+        }
     } else {
-        for (int f = threadIdx.x; f < cc; f += kThreads)
+        for (int e = threadIdx.x; e < L.cn * rw; e += kThreads)
+            q32[e] = 0;
+        __syncthreads();
+        for (int f = threadIdx.x; f < c * c; f += kThreads)
             q[(f / c) * L.ckp + f % c] = weights[f];
-    }
-    __syncthreads();
-    for (int i = threadIdx.x; i < L.cn; i += kThreads) {
-        int32_t sum = 0;
-        for (int k = 0; k < c; ++k)
-            sum += q[i * L.ckp + k];
-        rs[i] = sum;
+        __syncthreads();
+        for (int r = threadIdx.x; r < L.cn; r += kThreads) {
+            int32_t sum = 0;
+            for (int k = 0; k < c; ++k)
+                sum += q[r * L.ckp + k];
+            rs[r] = sum;
+        }
     }
     __syncthreads();
 }
@@ -234,7 +243,8 @@ __device__ __forceinline__ void dsp_put_count(uint8_t *smem, const DspLayout &L,
     smem[L.off_hi + (size_t)r * L.ckp + k] = (uint8_t)(((cnt >> 8) & 0xFF) ^ 0x80);
 }
 
-// Logit tile [64][c] from the byte planes and Q (after a barrier; ends with
+// Logit tile [64][c] (row stride dsp_tile_stride(c), odd, so that a lane per
+// sample reads it without bank conflicts) from the byte planes and Q (after a barrier; ends with
 // one).  The 4 waves share the (16-sample, 16-class) output tiles, at most
 // kDspTilesPerWave each; v_mfma_i32_16x16x32_i8 takes in lane l the 8
 // K-consecutive bytes of row l % 16 at K offset 8 * (l / 16) of A (counts)
@@ -275,6 +285,7 @@ __device__ __forceinline__ void dsp_logits(uint8_t *smem, const DspLayout &L, in
     }
     __syncthreads();
     int32_t *tile = reinterpret_cast<int32_t *>(smem + L.off_tile);
+    const int cs = dsp_tile_stride(c);
 #pragma unroll
     for (int j = 0; j < kDspTilesPerWave; ++j) {
         const int t = wave + kWaves * j;
@@ -284,15 +295,15 @@ __device__ __forceinline__ void dsp_logits(uint8_t *smem, const DspLayout &L, in
         if (cls < c)
 #pragma unroll
             for (int r = 0; r < 4; ++r)
-                tile[(16 * mt + kq / 2 + r) * c + cls] = res[j][r];   // row 4 * (l / 16) + r
+                tile[(16 * mt + kq / 2 + r) * cs + cls] = res[j][r];   // row 4 * (l / 16) + r
     }
     __syncthreads();
 }
 
-// Argmax (lowest index) and coalesced logit store of the tile; ends with a
-// barrier.  Each wave scans a quarter of the classes of every sample, then
-// wave 0 merges the four partial maxima (in class order, so ties keep the
-// lowest index).
+// Argmax (lowest index) and coalesced logit store of the tile.  Each wave
+// scans a quarter of the classes of every sample; after a barrier, wave 0
+// merges the four partial maxima (in class order, so ties keep the lowest
+// index).  The logits leave as one contiguous block (finish::store_tile).
 __device__ __forceinline__ void dsp_emit(uint8_t *smem, const DspLayout &L, int c, int64_t s0,
                                          int64_t n, int32_t *__restrict__ logits,
                                          int32_t *__restrict__ argmax)
@@ -305,8 +316,9 @@ __device__ __forceinline__ void dsp_emit(uint8_t *smem, const DspLayout &L, int 
         const int per = (c + kWaves - 1) / kWaves;
         const int i0 = wave * per, i1 = min(c, i0 + per);
         int32_t best = INT32_MIN, besti = c;
+        const int cs = dsp_tile_stride(c);
         for (int i = i0; i < i1; ++i) {
-            const int32_t v = tile[lane * c + i];
+            const int32_t v = tile[lane * cs + i];
             if (v > best) {
                 best = v;
                 besti = i;
@@ -316,11 +328,7 @@ __device__ __forceinline__ void dsp_emit(uint8_t *smem, const DspLayout &L, int 
         part[(kWaves + wave) * kWave + lane] = besti;
     }
     if (logits)
-        for (int e = threadIdx.x; e < kWave * c; e += kThreads) {
-            const int64_t ss = s0 + e / c;
-            if (ss < n)
-                logits[ss * c + e % c] = tile[e];
-        }
+        finish::store_tile(tile, dsp_tile_stride(c), logits + s0 * c, c, c, n - s0);
     __syncthreads();
     if (argmax && wave == 0 && s0 + lane < n) {
         int32_t best = part[lane], besti = part[kWaves * kWave + lane];
@@ -336,57 +344,39 @@ __device__ __forceinline__ void dsp_emit(uint8_t *smem, const DspLayout &L, int 
     }
 }
 
-// Fused finish of the quantized head: class counts of a 64-sample column from
-// the bit planes (as k_head_finish: the column's planes staged in LDS with
-// coalesced loads when they fit in stage_words, else read class by class),
-// then the logits on the matrix cores.
+// Fused finish of the quantized head, one block per 64-sample column: class
+// counts from the bit planes as in k_head_finish (the column's lines touched
+// first, then scalar plane loads and one v_addc per plane), written as the two
+// offset byte planes, then the logits on the matrix cores.
 template <int P>
 __global__ __launch_bounds__(kThreads) void k_head_finish_dsp(
-    const uint64_t *__restrict__ planes, int64_t n, int32_t c, int32_t S, int32_t stage_words,
+    const uint64_t *__restrict__ planes, int64_t n, int32_t c, int32_t S,
     const int8_t *__restrict__ weights, int32_t *__restrict__ logits,
     int32_t *__restrict__ argmax)
 {
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-    const DspLayout L = dsp_layout(c, stage_words);
-    uint64_t *stage = reinterpret_cast<uint64_t *>(smem + L.off_stage);
-    const uint32_t *stage32 = reinterpret_cast<const uint32_t *>(stage);
+    const DspLayout L = dsp_layout(c);
     const int lane = threadIdx.x % kWave;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int half = lane >> 5, bit = lane & 31;
-    const int64_t W = (n + kWave - 1) / kWave;
-    const int32_t words = c * S * P;                  // one column's plane words
-    const bool staged = words <= stage_words;
+    const int64_t col = blockIdx.x;
+    const int64_t nw = (int64_t)c * S * P;
+    const int64_t e = min((int64_t)threadIdx.x * 16, nw - 1);
+    const uint32_t touch = reinterpret_cast<const uint32_t *>(planes + col * nw + e)[0];
     dsp_stage_q(weights, c, L, smem);
-    for (int64_t col = blockIdx.x; col < W; col += gridDim.x) {
-        const uint64_t *pc = planes + col * (int64_t)c * S * P;
-        if (staged) {
-            for (int e = threadIdx.x; e < words; e += kThreads)
-                stage[e] = pc[e];
-            __syncthreads();
-        }
-        for (int i = wave; i < c; i += kWaves) {
-            int32_t cnt = 0;
-            for (int q = 0; q < S; ++q) {
-                int32_t part = 0;
-                if (staged) {
-                    const uint32_t *w = stage32 + 2 * (i * S + q) * P + half;
-#pragma unroll
-                    for (int p = 0; p < P; ++p)
-                        part |= (int32_t)((w[2 * p] >> bit) & 1u) << p;
-                } else {
-                    const uint64_t *pl = pc + ((int64_t)i * S + q) * P;
-#pragma unroll
-                    for (int p = 0; p < P; ++p)
-                        part |= (int32_t)((pl[p] >> lane) & 1u) << p;
-                }
-                cnt += part;
-            }
-            dsp_put_count(smem, L, lane, i, cnt);
-        }
-        __syncthreads();
-        dsp_logits(smem, L, c);
-        dsp_emit(smem, L, c, col * kWave, n, logits, argmax);
+    const uint64_t *pc = planes + col * nw;
+    for (int i = wave; i < c; i += kWaves) {
+        const uint64_t *pw = pc + (int64_t)i * S * P;
+        int q = 0;
+        const int32_t cnt = finish::add_splits<P, (P <= 8 ? 4 : 2)>(pw, q, S) +
+                            finish::add_splits<P, 1>(pw, q, S);
+        dsp_put_count(smem, L, lane, i, cnt);
     }
+    __syncthreads();
+    dsp_logits(smem, L, c);
+    dsp_emit(smem, L, c, col * kWave, n, logits, argmax);
+    // the touch is consumed once the argmax partials have been read
+    __syncthreads();
+    reinterpret_cast<int32_t *>(smem + L.off_part)[threadIdx.x] ^= (int32_t)touch;
 }
 
 // Standalone quantized head on counts [n][c] in device memory.  Only Q
@@ -584,13 +574,9 @@ hipError_t launch_finish_p(const uint64_t *planes, int64_t n, int32_t c, int32_t
     if (dsp_weights) {
         if (c > kDspMaxClasses)
             return hipErrorInvalidValue;
-        // Q is staged once per block and reused for a run of columns
-        const int64_t blocks = W < kDspFinishBlocks ? W : kDspFinishBlocks;
-        const int64_t want = (int64_t)c * plan.splits * P;
-        const int32_t stage_words = want <= finish::kMaxWords ? (int32_t)want : 0;
-        hipLaunchKernelGGL(k_head_finish_dsp<P>, dim3((unsigned)blocks), dim3(kThreads),
-                           dsp_layout(c, stage_words).bytes, stream, planes, n, c, plan.splits,
-                           stage_words, dsp_weights, scores, argmax);
+        hipLaunchKernelGGL(k_head_finish_dsp<P>, dim3((unsigned)W), dim3(kThreads),
+                           dsp_layout(c).bytes, stream, planes, n, c, plan.splits, dsp_weights,
+                           scores, argmax);
         return hipGetLastError();
     }
     const int64_t words = finish::tile_words(c);

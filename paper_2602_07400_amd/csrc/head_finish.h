@@ -13,9 +13,7 @@ constexpr int kThreads = 256;                    // the block this runs in
 constexpr int kWaves = kThreads / kWave;
 constexpr int kClasses = 128;                    // classes per chunk
 // LDS of the finish: the score tile [64][cs] (int32, cs = the odd stride >=
-// the chunk's classes, so the tile has no bank conflicts).  kMaxWords bounds
-// the LDS the quantized head's finish stages planes in.
-constexpr int kMaxWords = kWave * (kClasses + 1) / 2;   // uint64 words
+// the chunk's classes, so the tile has no bank conflicts).
 
 __host__ __device__ inline int32_t stride(int32_t c)
 {
@@ -60,6 +58,55 @@ __device__ __forceinline__ int32_t add_splits(const uint64_t *__restrict__ pw, i
         }
     }
     return cnt;
+}
+
+// Store a score tile [64][cn] (LDS, row stride cs) into dst, the [64][c]
+// block of a row-major [n][c] array that starts at the tile's first sample,
+// of which `rows` rows are inside the batch: whole 16-byte stores where the
+// block is contiguous (cn == c), complete and aligned, walking element
+// e = r * c + k without a division per element; else one element at a time.
+// All threads of the block; no barrier.
+__device__ __forceinline__ void store_tile(const int32_t *tile, int32_t cs, int32_t *__restrict__ dst,
+                                           int32_t c, int32_t cn, int64_t rows)
+{
+    const int total = kWave * cn;
+    if (cn == c && rows >= kWave && ((uintptr_t)dst % 16) == 0) {
+        const int e0 = 4 * threadIdx.x;
+        int r = e0 / cn, k = e0 - r * cn;
+        const int dr = 4 * kThreads / cn, dk = 4 * kThreads - dr * cn;
+        for (int e = e0; e < total; e += 4 * kThreads) {
+            int32_t v[4];
+            int rr = r, kk = k;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                v[u] = tile[rr * cs + kk];
+                if (++kk == cn) {
+                    kk = 0;
+                    ++rr;
+                }
+            }
+            *reinterpret_cast<int4 *>(dst + e) = make_int4(v[0], v[1], v[2], v[3]);
+            r += dr;
+            k += dk;
+            if (k >= cn) {
+                k -= cn;
+                ++r;
+            }
+        }
+    } else {
+        int r = threadIdx.x / cn, k = threadIdx.x - r * cn;
+        const int dr = kThreads / cn, dk = kThreads - dr * cn;
+        for (int e = threadIdx.x; e < total; e += kThreads) {
+            if (r < rows)
+                dst[(int64_t)r * c + k] = tile[r * cs + k];
+            r += dr;
+            k += dk;
+            if (k >= cn) {
+                k -= cn;
+                ++r;
+            }
+        }
+    }
 }
 
 // Column `col` of planes [W][c][S][P], one lane per sample.  A class's S * P
@@ -126,49 +173,8 @@ __device__ __forceinline__ void column_scalar(const uint64_t *__restrict__ plane
             }
         }
         __syncthreads();
-        if (scores) {
-            int32_t *dst = scores + s0 * c + c0;
-            const int total = kWave * cn;
-            if (cn == c && s0 + kWave <= n && ((uintptr_t)dst % 16) == 0) {
-                // the block [64][c] is contiguous: element e = r * c + k,
-                // walked without a division per element
-                const int e0 = 4 * threadIdx.x;
-                int r = e0 / cn, k = e0 - r * cn;
-                const int dr = 4 * kThreads / cn, dk = 4 * kThreads - dr * cn;
-                for (int e = e0; e < total; e += 4 * kThreads) {
-                    int32_t v[4];
-                    int rr = r, kk = k;
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) {
-                        v[u] = tile[rr * cs + kk];
-                        if (++kk == cn) {
-                            kk = 0;
-                            ++rr;
-                        }
-                    }
-                    *reinterpret_cast<int4 *>(dst + e) = make_int4(v[0], v[1], v[2], v[3]);
-                    r += dr;
-                    k += dk;
-                    if (k >= cn) {
-                        k -= cn;
-                        ++r;
-                    }
-                }
-            } else {
-                int r = threadIdx.x / cn, k = threadIdx.x - r * cn;
-                const int dr = kThreads / cn, dk = kThreads - dr * cn;
-                for (int e = threadIdx.x; e < total; e += kThreads) {
-                    if (s0 + r < n)
-                        dst[(int64_t)r * c + k] = tile[r * cs + k];
-                    r += dr;
-                    k += dk;
-                    if (k >= cn) {
-                        k -= cn;
-                        ++r;
-                    }
-                }
-            }
-        }
+        if (scores)
+            store_tile(tile, cs, scores + s0 * c + c0, c, cn, n - s0);
         __syncthreads();
     }
     part[0][wave][lane] = best;
