@@ -160,16 +160,12 @@ typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 
 // LDS of the quantized head for c classes: Q padded to [cn][ckp] bytes
 // (cn = c rounded up to 16 output classes, ck = c rounded up to the 32-deep
-// K step, ckp = ck + 8 to spread the banks) and its row sums, kept for the
-// block's whole run of 64-sample tiles; the two offset byte planes of a
-// tile's counts [64][ckp], whose bytes the logit tile [64][c] reuses once
-// the products are in registers; and the argmax partials.
+// K step, ckp = ck + 8 to spread the banks) and its row sums; for the fused
+// finish also the two offset byte planes of a column's counts [64][ckp].
 struct DspLayout {
     int cn, ck, ckp;
-    size_t off_q, off_rs, off_lo, off_hi, off_tile, off_part, bytes;
+    size_t off_q, off_rs, off_lo, off_hi, bytes;
 };
-
-__host__ __device__ inline int dsp_tile_stride(int c) { return c | 1; }
 
 __host__ __device__ inline DspLayout dsp_layout(int c)
 {
@@ -181,11 +177,7 @@ __host__ __device__ inline DspLayout dsp_layout(int c)
     L.off_rs = (size_t)L.cn * L.ckp;
     L.off_lo = L.off_rs + (size_t)L.cn * 4;
     L.off_hi = L.off_lo + (size_t)kWave * L.ckp;
-    const size_t planes_end = L.off_hi + (size_t)kWave * L.ckp;
-    L.off_tile = L.off_lo;
-    const size_t tile_end = L.off_tile + (size_t)kWave * dsp_tile_stride(c) * 4;
-    L.off_part = ((planes_end > tile_end ? planes_end : tile_end) + 15) / 16 * 16;
-    L.bytes = L.off_part + 2 * kWaves * kWave * 4;
+    L.bytes = L.off_hi + (size_t)kWave * L.ckp;
     return L;
 }
 
@@ -248,111 +240,97 @@ __device__ __forceinline__ void dsp_put_count(uint8_t *smem, const DspLayout &L,
     smem[L.off_hi + (size_t)r * L.ckp + k] = (uint8_t)(((cnt >> 8) & 0xFF) ^ 0x80);
 }
 
-// Logit tile [64][c] (row stride dsp_tile_stride(c), odd, so that a lane per
-// sample reads it without bank conflicts) from the byte planes and Q (after a barrier; ends with
-// one).  The 4 waves share the (16-sample, 16-class) output tiles, at most
-// kDspTilesPerWave each; v_mfma_i32_16x16x32_i8 takes in lane l the 8
-// K-consecutive bytes of row l % 16 at K offset 8 * (l / 16) of A (counts)
-// and of B^T (rows of Q), and returns D[4 * (l / 16) + r][l % 16] in
-// accumulator r.  The results wait in registers until every wave is done
-// with the staging bytes, which the tile then overwrites.
-constexpr int kDspTilesPerWave = 4 * (kDspMaxClasses / 16) / kWaves;
+constexpr int kDspMaxK = kDspMaxClasses / 32;      // K steps of 32 classes
 
-__device__ __forceinline__ void dsp_logits(uint8_t *smem, const DspLayout &L, int c)
+// Merge (best, besti) with the lane that the DPP control CTL selects in the
+// same 16-lane row: the larger value wins, the lower class on ties (besti = c
+// marks "none yet").  The order is total, so any merge tree gives the same
+// result.  All lanes of the wave.
+template <int CTL>
+__device__ __forceinline__ void dsp_argmax_step(int32_t &best, int32_t &besti, int c)
 {
-    const int8_t *q = reinterpret_cast<const int8_t *>(smem + L.off_q);
-    const int32_t *rs = reinterpret_cast<const int32_t *>(smem + L.off_rs);
+    const int32_t ov = __builtin_amdgcn_update_dpp(0, best, CTL, 0xF, 0xF, false);
+    const int32_t oi = __builtin_amdgcn_update_dpp(0, besti, CTL, 0xF, 0xF, false);
+    if (oi < c && (besti >= c || ov > best || (ov == best && oi < besti))) {
+        best = ov;
+        besti = oi;
+    }
+}
+
+// One 16-sample M-tile of logits (samples s_first .. s_first + 15) from its
+// A operands (8 K-consecutive counts per lane and K step, as the two offset
+// bytes, in the MFMA layout), with Q and its row sums in LDS: each N tile's
+// product over the K steps, its logits stored from the accumulators, and the
+// argmax of each sample -- spread over the 16 lanes of a row and over the N
+// tiles -- as a running maximum per lane followed by a 16-lane reduction
+// (dsp_argmax_step) that prefers the lower class on ties.  One wave.  v_mfma_i32_16x16x32_i8
+// takes in lane l the 8 K-consecutive bytes of row l % 16 at K offset
+// 8 (l / 16) of A (counts) and of B^T (rows of Q), and returns
+// D[4 (l / 16) + r][l % 16] in accumulator r.
+__device__ __forceinline__ void dsp_mtile(const long (&a_lo)[kDspMaxK], const long (&a_hi)[kDspMaxK],
+                                          int nks, int n_nt, const int8_t *q, int ckp,
+                                          const int32_t *rs, int c, int64_t s_first, int64_t n,
+                                          int32_t *__restrict__ logits,
+                                          int32_t *__restrict__ argmax)
+{
     const int lane = threadIdx.x % kWave;
-    const int wave = threadIdx.x / kWave;
-    const int row = lane % 16, kq = 8 * (lane / 16);
-    const int n_t = 4 * (L.cn / 16);
-    i32x4 res[kDspTilesPerWave];
+    const int row = lane % 16, kg = lane / 16, kq = 8 * kg;
+    int32_t best[4], besti[4];
 #pragma unroll
-    for (int j = 0; j < kDspTilesPerWave; ++j) {
-        const int t = wave + kWaves * j;
-        if (t >= n_t)
-            break;
-        const int mt = t % 4, nt = t / 4;
+    for (int r = 0; r < 4; ++r) {
+        best[r] = INT32_MIN;
+        besti[r] = c;
+    }
+    for (int nt = 0; nt < n_nt; ++nt) {
         i32x4 acc_lo = {0, 0, 0, 0}, acc_hi = {0, 0, 0, 0};
-        for (int k0 = 0; k0 < L.ck; k0 += 32) {
-            const size_t a_off = (size_t)(16 * mt + row) * L.ckp + k0 + kq;
-            const long a_lo = *reinterpret_cast<const long *>(smem + L.off_lo + a_off);
-            const long a_hi = *reinterpret_cast<const long *>(smem + L.off_hi + a_off);
-            const long b = *reinterpret_cast<const long *>(q + (size_t)(16 * nt + row) * L.ckp +
-                                                           k0 + kq);
-            acc_lo = __builtin_amdgcn_mfma_i32_16x16x32_i8(a_lo, b, acc_lo, 0, 0, 0);
-            acc_hi = __builtin_amdgcn_mfma_i32_16x16x32_i8(a_hi, b, acc_hi, 0, 0, 0);
+#pragma unroll
+        for (int ks = 0; ks < kDspMaxK; ++ks) {
+            if (ks >= nks)
+                break;
+            const long b = *reinterpret_cast<const long *>(
+                q + (size_t)(16 * nt + row) * ckp + 32 * ks + kq);
+            acc_lo = __builtin_amdgcn_mfma_i32_16x16x32_i8(a_lo[ks], b, acc_lo, 0, 0, 0);
+            acc_hi = __builtin_amdgcn_mfma_i32_16x16x32_i8(a_hi[ks], b, acc_hi, 0, 0, 0);
         }
-        const uint32_t corr = 32896u * (uint32_t)rs[16 * nt + row];
+        const int cls = 16 * nt + row;               // output column of this lane
+        if (cls < c) {
+            const uint32_t corr = 32896u * (uint32_t)rs[cls];
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-            res[j][r] = (int32_t)(256u * (uint32_t)acc_hi[r] + (uint32_t)acc_lo[r] + corr);
+            for (int r = 0; r < 4; ++r) {
+                const int32_t v =
+                    (int32_t)(256u * (uint32_t)acc_hi[r] + (uint32_t)acc_lo[r] + corr);
+                const int64_t smp = s_first + 4 * kg + r;
+                if (logits && smp < n)
+                    logits[smp * c + cls] = v;
+                if (v > best[r]) {                   // classes ascend with nt
+                    best[r] = v;
+                    besti[r] = cls;
+                }
+            }
+        }
     }
-    __syncthreads();
-    int32_t *tile = reinterpret_cast<int32_t *>(smem + L.off_tile);
-    const int cs = dsp_tile_stride(c);
+    if (argmax) {
 #pragma unroll
-    for (int j = 0; j < kDspTilesPerWave; ++j) {
-        const int t = wave + kWaves * j;
-        if (t >= n_t)
-            break;
-        const int mt = t % 4, cls = 16 * (t / 4) + row;
-        if (cls < c)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-                tile[(16 * mt + kq / 2 + r) * cs + cls] = res[j][r];   // row 4 * (l / 16) + r
+        for (int r = 0; r < 4; ++r) {
+            // the 16 lanes of a row: swap within quads (lane ^ 1, ^ 2), then
+            // rotate the row by 4 and 8; every lane ends with the row's result
+            dsp_argmax_step<0xB1>(best[r], besti[r], c);     // quad_perm [1, 0, 3, 2]
+            dsp_argmax_step<0x4E>(best[r], besti[r], c);     // quad_perm [2, 3, 0, 1]
+            dsp_argmax_step<0x124>(best[r], besti[r], c);    // row_ror:4
+            dsp_argmax_step<0x128>(best[r], besti[r], c);    // row_ror:8
+            const int64_t smp = s_first + 4 * kg + r;
+            if (row == 0 && smp < n)
+                argmax[smp] = besti[r];
+        }
     }
-    __syncthreads();
 }
 
-// Argmax (lowest index) and coalesced logit store of the tile.  Each wave
-// scans a quarter of the classes of every sample; after a barrier, wave 0
-// merges the four partial maxima (in class order, so ties keep the lowest
-// index).  The logits leave as one contiguous block (finish::store_tile).
-__device__ __forceinline__ void dsp_emit(uint8_t *smem, const DspLayout &L, int c, int64_t s0,
-                                         int64_t n, int32_t *__restrict__ logits,
-                                         int32_t *__restrict__ argmax)
-{
-    const int32_t *tile = reinterpret_cast<const int32_t *>(smem + L.off_tile);
-    int32_t *part = reinterpret_cast<int32_t *>(smem + L.off_part);   // [2][kWaves][64]
-    const int lane = threadIdx.x % kWave;
-    const int wave = threadIdx.x / kWave;
-    if (argmax) {
-        const int per = (c + kWaves - 1) / kWaves;
-        const int i0 = wave * per, i1 = min(c, i0 + per);
-        int32_t best = INT32_MIN, besti = c;
-        const int cs = dsp_tile_stride(c);
-        for (int i = i0; i < i1; ++i) {
-            const int32_t v = tile[lane * cs + i];
-            if (v > best) {
-                best = v;
-                besti = i;
-            }
-        }
-        part[wave * kWave + lane] = best;
-        part[(kWaves + wave) * kWave + lane] = besti;
-    }
-    if (logits)
-        finish::store_tile(tile, dsp_tile_stride(c), logits + s0 * c, c, c, n - s0);
-    __syncthreads();
-    if (argmax && wave == 0 && s0 + lane < n) {
-        int32_t best = part[lane], besti = part[kWaves * kWave + lane];
-        for (int w = 1; w < kWaves; ++w) {
-            const int32_t v = part[w * kWave + lane];
-            const int32_t vi = part[(kWaves + w) * kWave + lane];
-            if (vi < c && (besti >= c || v > best)) {
-                best = v;
-                besti = vi;
-            }
-        }
-        argmax[s0 + lane] = besti;
-    }
-}
 
 // Fused finish of the quantized head, one block per 64-sample column: class
 // counts from the bit planes as in k_head_finish (the column's lines touched
 // first, then scalar plane loads and one v_addc per plane), written as the two
-// offset byte planes, then the logits on the matrix cores.
+// offset byte planes, then the logits on the matrix cores, each wave one of
+// the column's four 16-sample M-tiles (dsp_mtile).
 template <int P>
 __global__ __launch_bounds__(kThreads) void k_head_finish_dsp(
     const uint64_t *__restrict__ planes, int64_t n, int32_t c, int32_t S,
@@ -377,22 +355,33 @@ __global__ __launch_bounds__(kThreads) void k_head_finish_dsp(
         dsp_put_count(smem, L, lane, i, cnt);
     }
     __syncthreads();
-    dsp_logits(smem, L, c);
-    dsp_emit(smem, L, c, col * kWave, n, logits, argmax);
-    // the touch is consumed once the argmax partials have been read
-    __syncthreads();
-    reinterpret_cast<int32_t *>(smem + L.off_part)[threadIdx.x] ^= (int32_t)touch;
+    // wave w: samples 16 w .. 16 w + 15 of the column, its A operands from
+    // its 16 rows of the byte planes
+    const int row = lane % 16, kq = 8 * (lane / 16);
+    const int nks = L.ck / 32;
+    long a_lo[kDspMaxK], a_hi[kDspMaxK];
+#pragma unroll
+    for (int ks = 0; ks < kDspMaxK; ++ks) {
+        if (ks >= nks)
+            break;
+        const size_t a_off = (size_t)(16 * wave + row) * L.ckp + 32 * ks + kq;
+        a_lo[ks] = *reinterpret_cast<const long *>(smem + L.off_lo + a_off);
+        a_hi[ks] = *reinterpret_cast<const long *>(smem + L.off_hi + a_off);
+    }
+    dsp_mtile(a_lo, a_hi, nks, L.cn / 16, reinterpret_cast<const int8_t *>(smem + L.off_q), L.ckp,
+              reinterpret_cast<const int32_t *>(smem + L.off_rs), c, col * kWave + 16 * wave, n,
+              logits, argmax);
+    // the touch is consumed after the column, into a padding dword of one of
+    // the wave's own rows (bytes ck .. ckp - 1, which no product reads)
+    atomicXor(reinterpret_cast<uint32_t *>(smem + L.off_lo + (size_t)(16 * wave + row) * L.ckp +
+                                           L.ck) + (lane / 16) % 2,
+              touch);
 }
 
-// Standalone quantized head on counts [n][c] in device memory.  Only Q
-// lives in LDS: each wave takes 16-sample M-tiles and builds its A operands
-// (8 counts per lane and K step, split into the two offset bytes) straight
-// from global memory; each output tile is stored from the accumulators, and
-// the argmax of a sample -- spread over the 16 lanes of a row and over the
-// N tiles -- is a running maximum per lane followed by a 16-lane xor
-// reduction that prefers the lower class on ties.
-constexpr int kDspMaxK = kDspMaxClasses / 32;      // K steps of 32 classes
-
+// Standalone quantized head on counts [n][c] in device memory: only Q lives
+// in LDS, and each wave takes 16-sample M-tiles and builds their A operands
+// straight from the count rows (8 counts per lane and K step, split into the
+// two offset bytes); dsp_mtile does the rest.
 __device__ __forceinline__ uint32_t dsp_byte_pack(const int32_t (&v)[4], int shift)
 {
     uint32_t r = 0;
@@ -444,58 +433,7 @@ __global__ __launch_bounds__(kThreads) void k_grouped_dsp(
             a_lo[ks] = (long)(((uint64_t)dsp_byte_pack(v1, 0) << 32) | dsp_byte_pack(v0, 0));
             a_hi[ks] = (long)(((uint64_t)dsp_byte_pack(v1, 8) << 32) | dsp_byte_pack(v0, 8));
         }
-        int32_t best[4], besti[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            best[r] = INT32_MIN;
-            besti[r] = c;
-        }
-        for (int nt = 0; nt < n_nt; ++nt) {
-            i32x4 acc_lo = {0, 0, 0, 0}, acc_hi = {0, 0, 0, 0};
-#pragma unroll
-            for (int ks = 0; ks < kDspMaxK; ++ks) {
-                if (ks >= nks)
-                    break;
-                const long b = *reinterpret_cast<const long *>(
-                    q + (size_t)(16 * nt + row) * L.ckp + 32 * ks + kq);
-                acc_lo = __builtin_amdgcn_mfma_i32_16x16x32_i8(a_lo[ks], b, acc_lo, 0, 0, 0);
-                acc_hi = __builtin_amdgcn_mfma_i32_16x16x32_i8(a_hi[ks], b, acc_hi, 0, 0, 0);
-            }
-            const int cls = 16 * nt + row;               // output column of this lane
-            if (cls < c) {
-                const uint32_t corr = 32896u * (uint32_t)rs[cls];
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int32_t v =
-                        (int32_t)(256u * (uint32_t)acc_hi[r] + (uint32_t)acc_lo[r] + corr);
-                    const int64_t smp = 16 * mt + 4 * kg + r;
-                    if (logits && smp < n)
-                        logits[smp * c + cls] = v;
-                    if (v > best[r]) {                   // classes ascend with nt
-                        best[r] = v;
-                        besti[r] = cls;
-                    }
-                }
-            }
-        }
-        if (argmax) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-#pragma unroll
-                for (int m = 1; m < 16; m <<= 1) {
-                    const int32_t ov = __shfl_xor(best[r], m);
-                    const int32_t oi = __shfl_xor(besti[r], m);
-                    if (oi < c && (besti[r] >= c || ov > best[r] ||
-                                   (ov == best[r] && oi < besti[r]))) {
-                        best[r] = ov;
-                        besti[r] = oi;
-                    }
-                }
-                const int64_t smp = 16 * mt + 4 * kg + r;
-                if (row == 0 && smp < n)
-                    argmax[smp] = besti[r];
-            }
-        }
+        dsp_mtile(a_lo, a_hi, nks, L.cn / 16, q, L.ckp, rs, c, 16 * mt, n, logits, argmax);
     }
 }
 
