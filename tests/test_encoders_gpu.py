@@ -56,7 +56,11 @@ def _fit_check(x, b, groups):
 
 @pytest.mark.parametrize("n,d,groups,b", [(5000, 3072, 3, 3), (5000, 3072, 1, 4), (1, 12, 3, 7),
                                           (3000, 784, 1, 8), (2000, 30, 3, 64), (4097, 64, 32, 5),
-                                          (700, 15, 5, 1)])
+                                          (700, 15, 5, 1),
+                                          # blocks of 40-69 rows: whole 32-row load batches and
+                                          # a tail, with 32, 16, 1 and 4 copies of each bin
+                                          (70000, 784, 1, 7), (40000, 3072, 3, 7),
+                                          (40000, 64, 32, 5), (40000, 1001, 7, 5)])
 def test_fit_quantiles_parity(n, d, groups, b):
     rng = np.random.default_rng(n + d + groups + b)
     # skewed values: many ties and empty bins
