@@ -10,11 +10,12 @@
 // and adds the group's words into it with a Harley-Seal carry-save tree
 // (v_bitop3 full adders, ~2 ops per word per 32 samples), one lane per column
 // so every row load is a coalesced 512-byte segment.  Long groups are split
-// into row ranges so the launch fills the chip.  Stage 2 runs one lane per
-// sample and one block per column: the column's planes are staged in LDS with
-// coalesced loads, its waves share the classes, assemble each class score bit
-// by bit and sum the splits into an LDS score tile, from which the scores are
-// written as one contiguous block, and take the argmax.
+// into row ranges so the launch fills the chip.  Stage 2 (head_finish.h) runs
+// one lane per sample and one block per column: after one vector load per
+// 128-byte line of the column's planes, its waves share the classes, read
+// each class's plane words with scalar loads, assemble each score bit by bit
+// (one v_addc per plane) and sum the splits into an LDS score tile, from
+// which the scores are written as one contiguous block, and take the argmax.
 //
 // Quantized head (Sec. 3 "Encoders and heads"; Sec. 5 "Head", the DSP-backed
 // head): logit i = sum_j Q[i][j] * count[j] with Q a c x c matrix of signed
