@@ -72,6 +72,26 @@ def test_extremes_and_ties():
         _check(counts, Q)          # all logits equal: argmax 0
 
 
+@pytest.mark.parametrize("c", [17, 37, 100, 128])
+def test_partial_ties_across_lanes_and_tiles(c):
+    # Q = +-identity makes logit i = +-count i; each sample's maximum is
+    # shared by 2-5 classes spread over different lanes (class % 16) and
+    # N tiles (class // 16), so the argmax must merge the lanes' and tiles'
+    # partial maxima and keep the lowest tied class
+    rng = np.random.default_rng(c)
+    n = 64 * 3 + 21
+    for sign in (1, -1):
+        counts = rng.integers(1, 1000, size=(n, c)).astype(np.int32)
+        lowest = np.empty(n, np.int64)
+        for s in range(n):
+            tied = rng.choice(c, size=int(rng.integers(2, 6)), replace=False)
+            counts[s, tied] = 2000 if sign > 0 else 0        # above / below every other count
+            lowest[s] = tied.min()
+        Q = (sign * np.eye(c)).astype(np.int8)
+        assert np.array_equal(oracle.grouped_dsp(counts, Q)[1], lowest)
+        _check(counts, Q)
+
+
 def test_one_output_only():
     rng = np.random.default_rng(8)
     counts = rng.integers(0, 700, size=(300, 100)).astype(np.int32)
