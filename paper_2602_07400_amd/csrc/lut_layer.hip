@@ -296,25 +296,82 @@ __device__ __forceinline__ int pass_fanin(const uint8_t *fanin, int32_t n_fanin,
     return __builtin_amdgcn_readfirstlane(min(kp, K));
 }
 
-// The next pass's gathers issue at a raised wave priority, so that they
-// leave ahead of other waves' evaluation: C5 layer 1 at k = 4 0.807 -> 0.786
-// ms, k = 2 0.665 -> 0.660 ms (ABBA runs on one set of buffers).  The
-// memory clobbers keep the loads between the two s_setprio.
+// In a partial node block (fewer than NB nodes; full blocks take the split
+// phases below) the next pass's gathers issue at a raised wave priority, so
+// that they leave ahead of other waves' evaluation: C5 layer 1 at k = 4 0.807
+// -> 0.786 ms, k = 2 0.665 -> 0.660 ms when every block ran this loop (ABBA
+// runs on one set of buffers).  The memory clobbers keep the loads between
+// the two s_setprio.
 #ifndef BL_PF_SETPRIO
 #define BL_PF_SETPRIO 1
 #endif
 #ifndef BL_LUT_MINWAVES
 #define BL_LUT_MINWAVES 1
 #endif
-// Up to 4 inputs, the slab kernel loads the next pass's rows while it
-// evaluates the current pass (two register sets; C5 layer 1: k = 2 0.69 ->
-// 0.665 ms, k = 4 0.84 -> 0.81 ms).  At 5 and 6 inputs the second set would
+// Up to 4 inputs, the slab kernel loads rows ahead of the evaluation: in
+// full blocks the split phases below, in a partial block the next pass's
+// rows while it evaluates the current pass (two register sets; C5 layer 1,
+// when every block ran that loop: k = 2 0.69 -> 0.665 ms, k = 4 0.84 -> 0.81
+// ms).  At 5 and 6 inputs the second set would
 // cost occupancy: 4 lanes a node with prefetch need ~170 VGPRs (C4 layer 1
 // 1.23 -> 1.63 ms), 8 lanes with prefetch ran 1.34 ms.
 template <int K>
 constexpr bool slab_prefetch()
 {
     return K <= 4;
+}
+
+// A wave's vector-memory counter retires loads and stores in issue order, so
+// a gather issued after a store is seen complete only once that store has
+// been acknowledged, and while the output stream saturates the HBM write path
+// the acknowledgements come late: a loop that stores each pass before the
+// next pass's gather waits on its own stores.  A block whose NB nodes all
+// exist therefore runs in two phases: every pass's rows are gathered
+// (split_depth passes ahead of the evaluation, which takes each pass as its
+// rows arrive) and the outputs are held in registers, then all passes are
+// stored.  No load ever follows a store in the wave.  The depth trades
+// registers for loads in flight: all passes up to 2 inputs, 10 at 3, 4 at 4
+// (C5 layer 1, 2^18 samples into 64000 nodes: k = 2 0.642 -> 0.540 ms, k = 4
+// 0.773 -> 0.669 ms; k = 1 and 3 at that shape 0.585 -> 0.498 and 0.71 ->
+// 0.61 ms).  At 5 and 6 inputs the held outputs would cost occupancy (k = 6
+// holding one pass: 1.21 -> 1.32 ms).  The scheduling barriers keep the
+// compiler from regrouping the gathers, which shortens their distance ahead
+// (k = 2 0.600 ms without them).
+template <int K>
+constexpr int split_depth()
+{
+    return K <= 2 ? 15 : K == 3 ? 10 : 4;
+}
+
+template <int K, int R, int NPASS, int kPassNodes>
+__device__ __forceinline__ void split_passes(const uint64_t *src, const int32_t *s_conn,
+                                             const uint64_t *s_tab, int lnode, int S,
+                                             uint64_t *dst)
+{
+    constexpr int D = split_depth<K>() < NPASS - 1 ? split_depth<K>() : NPASS - 1;
+    uint32_t xs[D + 1][2 * R][K];
+    uint32_t o[NPASS][2 * R];
+#pragma unroll
+    for (int p = 0; p < D; ++p)
+        gather<K, R>(src, &s_conn[(p * kPassNodes + lnode) * K], S, xs[p]);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int p = 0; p < NPASS; ++p) {
+        if (p + D < NPASS)
+            gather<K, R>(src, &s_conn[((p + D) * kPassNodes + lnode) * K], S,
+                         xs[(p + D) % (D + 1)]);
+        __builtin_amdgcn_sched_barrier(0);
+        eval_node<K, R>(s_tab[p * kPassNodes + lnode], xs[p % (D + 1)], o[p]);
+        // pins the evaluation here: without it instruction selection sinks
+        // every pass's evaluation to the stores, after all the gathers
+#pragma unroll
+        for (int w = 0; w < 2 * R; ++w)
+            asm volatile("" : "+v"(o[p][w]));
+        __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int p = 0; p < NPASS; ++p)
+        store_out<R>(o[p], dst + (int64_t)(p * kPassNodes + lnode) * S, true);
 }
 
 template <int K, int S, int LPN, int NB, bool SPEC>
@@ -351,9 +408,16 @@ __global__ __launch_bounds__(kThreads, BL_LUT_MINWAVES) void k_lut_slab(
     uint64_t *dst = out + ((int64_t)slab * w_out + node0) * S + sub * R;
     const int npass = (nodes + kPassNodes - 1) / kPassNodes;
 
+    constexpr int kPasses = NB / kPassNodes;
+    if constexpr (!SPEC && slab_prefetch<K>() && kPasses >= 2) {
+        if (nodes == NB) {
+            split_passes<K, R, kPasses, kPassNodes>(src, s_conn, s_tab, lnode, S, dst);
+            return;
+        }
+    }
     if constexpr (!SPEC && slab_prefetch<K>()) {
-        // two register sets: the next pass's rows are in flight while this
-        // pass is evaluated
+        // a partial block: two register sets, the next pass's rows are in
+        // flight while this pass is evaluated
         uint32_t xa[2 * R][K], xb[2 * R][K];
         if (npass > 0)
             gather<K, R>(src, &s_conn[lnode * K], S, xa);
