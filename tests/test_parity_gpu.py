@@ -275,16 +275,20 @@ def test_forward_full_batch(name):
 
 def test_forward_hidden_layers_with_partial_node_blocks():
     # hidden layers of up to 4 inputs in the 512-node-block mode (>= 2048
-    # blocks) whose widths are not whole blocks: 8096 nodes at k = 4 leave a
-    # last block of 13 passes (an odd count: the two-register-set loop ends
-    # on its first set); 8100 nodes at k = 2 leave a last block of 14 passes
-    # whose last pass holds 4 nodes and 28 padding lanes
+    # blocks) whose widths are not whole blocks, so that every layer runs
+    # both loops: the whole blocks gather all passes before storing any (the
+    # depth ahead differs per fan-in: all passes at k <= 2, 10 at k = 3, 4 at
+    # k = 4), the last block runs the two-register-set loop.  8096 nodes at
+    # k = 4 leave a last block of 13 passes (an odd count: that loop ends on
+    # its first set); 8100 nodes at k = 2 leave 14 passes whose last holds 4
+    # nodes and 28 padding lanes; 4700 at k = 3 and 4300 at k = 1 leave 92
+    # and 204 nodes.
     rng = np.random.default_rng(31)
     n, d, b = 1 << 18, 784, 2
     x = rng.integers(0, 256, size=(n, d), dtype=np.uint8)
     th = np.sort(rng.integers(0, 256, size=(d, b), dtype=np.uint8), axis=1)
     layers, w_in = [], d * b
-    for w, k in ((8096, 4), (8100, 2), (8000, 6)):
+    for w, k in ((8096, 4), (8100, 2), (4700, 3), (4300, 1), (8000, 6)):
         conn = np.stack([rng.choice(w_in, size=k, replace=False) for _ in range(w)]).astype(np.int32)
         tab = rng.integers(0, 2**64, size=w, dtype=np.uint64)
         layers.append((conn, tab))
