@@ -282,7 +282,7 @@ __device__ __forceinline__ void spec_eval(int kp, const uint64_t *src, const int
 }
 
 // evaluated fan-in of the PN nodes from node n0: the largest entry of the
-// runs of kSpecPass nodes they touch (n0 need not start a run)
+// runs of kSpecPass nodes they touch (n0 need not start a run), at most K
 template <int PN, int K>
 __device__ __forceinline__ int pass_fanin(const uint8_t *fanin, int32_t n_fanin, int n0)
 {
@@ -293,7 +293,36 @@ __device__ __forceinline__ int pass_fanin(const uint8_t *fanin, int32_t n_fanin,
     for (int e = 0; e <= PN / kSpecPass; ++e)
         if (e0 + e < n_fanin && (e < PN / kSpecPass || n0 % kSpecPass != 0))
             kp = max(kp, (int)fanin[e0 + e]);
-    return __builtin_amdgcn_readfirstlane(min(kp, K));
+    return min(kp, K);
+}
+
+// A specialized block's fan-ins, staged with its connections (before the
+// block's barrier): s_kp[p] = the fan-in of pass p (PN nodes from n0 + p *
+// PN) for p < npass, s_kp[slot] and s_kp[slot + 1] the smallest and largest
+// of them.  Wave 0 reads the passes' entries at once, a lane a pass, and
+// takes the extremes with ballots; the pass loops then read their fan-in
+// from LDS instead of waiting for a global load before each pass's gathers.
+template <int PN, int K>
+__device__ __forceinline__ void stage_fanin(const uint8_t *fanin, int32_t n_fanin, int n0,
+                                            int npass, int slot, int *s_kp)
+{
+    if (threadIdx.x >= kWave)
+        return;
+    const int p = threadIdx.x;
+    const int kp = p < npass ? pass_fanin<PN, K>(fanin, n_fanin, n0 + p * PN) : -1;
+    if (p < npass)
+        s_kp[p] = kp;
+    int lo = K, hi = 0;
+#pragma unroll
+    for (int v = 0; v <= K; ++v)
+        if (__ballot(kp == v)) {
+            lo = min(lo, v);
+            hi = max(hi, v);
+        }
+    if (p == 0) {
+        s_kp[slot] = lo;
+        s_kp[slot + 1] = hi;
+    }
 }
 
 // In a partial node block (fewer than NB nodes; full blocks take the split
@@ -343,35 +372,64 @@ constexpr int split_depth()
     return K <= 2 ? 15 : K == 3 ? 10 : 4;
 }
 
-template <int K, int R, int NPASS, int kPassNodes>
+// The two phases for nodes of KP inputs whose connections are KS apart in
+// s_conn (KS = KP, or the layer's fan-in for a specialized block of fan-in
+// KP: the first KP slots give each node's output); KP = 0 is a constant node
+// (table bit 0).
+template <int KP, int KS, int R, int NPASS, int kPassNodes>
 __device__ __forceinline__ void split_passes(const uint64_t *src, const int32_t *s_conn,
                                              const uint64_t *s_tab, int lnode, int S,
                                              uint64_t *dst)
 {
-    constexpr int D = split_depth<K>() < NPASS - 1 ? split_depth<K>() : NPASS - 1;
-    uint32_t xs[D + 1][2 * R][K];
     uint32_t o[NPASS][2 * R];
+    if constexpr (KP == 0) {
 #pragma unroll
-    for (int p = 0; p < D; ++p)
-        gather<K, R>(src, &s_conn[(p * kPassNodes + lnode) * K], S, xs[p]);
-    __builtin_amdgcn_sched_barrier(0);
+        for (int p = 0; p < NPASS; ++p) {
+            const uint32_t m = 0u - (uint32_t)(s_tab[p * kPassNodes + lnode] & 1u);
 #pragma unroll
-    for (int p = 0; p < NPASS; ++p) {
-        if (p + D < NPASS)
-            gather<K, R>(src, &s_conn[((p + D) * kPassNodes + lnode) * K], S,
-                         xs[(p + D) % (D + 1)]);
+            for (int h = 0; h < 2 * R; ++h)
+                o[p][h] = m;
+        }
+    } else {
+        constexpr int D = split_depth<KP>() < NPASS - 1 ? split_depth<KP>() : NPASS - 1;
+        uint32_t xs[D + 1][2 * R][KP];
+#pragma unroll
+        for (int p = 0; p < D; ++p)
+            gather<KP, R>(src, &s_conn[(p * kPassNodes + lnode) * KS], S, xs[p]);
         __builtin_amdgcn_sched_barrier(0);
-        eval_node<K, R>(s_tab[p * kPassNodes + lnode], xs[p % (D + 1)], o[p]);
-        // pins the evaluation here: without it instruction selection sinks
-        // every pass's evaluation to the stores, after all the gathers
 #pragma unroll
-        for (int w = 0; w < 2 * R; ++w)
-            asm volatile("" : "+v"(o[p][w]));
-        __builtin_amdgcn_sched_barrier(0);
+        for (int p = 0; p < NPASS; ++p) {
+            if (p + D < NPASS)
+                gather<KP, R>(src, &s_conn[((p + D) * kPassNodes + lnode) * KS], S,
+                              xs[(p + D) % (D + 1)]);
+            __builtin_amdgcn_sched_barrier(0);
+            eval_node<KP, R>(s_tab[p * kPassNodes + lnode], xs[p % (D + 1)], o[p]);
+            // pins the evaluation here: without it instruction selection
+            // sinks every pass's evaluation to the stores, after all the
+            // gathers
+#pragma unroll
+            for (int w = 0; w < 2 * R; ++w)
+                asm volatile("" : "+v"(o[p][w]));
+            __builtin_amdgcn_sched_barrier(0);
+        }
     }
 #pragma unroll
     for (int p = 0; p < NPASS; ++p)
         store_out<R>(o[p], dst + (int64_t)(p * kPassNodes + lnode) * S, true);
+}
+
+// split_passes at the block's fan-in kp (wave-uniform, 0 <= kp <= K).
+template <int KQ, int K, int R, int NPASS, int kPassNodes>
+__device__ __forceinline__ void split_passes_kp(int kp, const uint64_t *src,
+                                                const int32_t *s_conn, const uint64_t *s_tab,
+                                                int lnode, int S, uint64_t *dst)
+{
+    if (kp == KQ) {
+        split_passes<KQ, K, R, NPASS, kPassNodes>(src, s_conn, s_tab, lnode, S, dst);
+        return;
+    }
+    if constexpr (KQ < K)
+        split_passes_kp<KQ + 1, K, R, NPASS, kPassNodes>(kp, src, s_conn, s_tab, lnode, S, dst);
 }
 
 template <int K, int S, int LPN, int NB, bool SPEC>
@@ -384,8 +442,11 @@ __global__ __launch_bounds__(kThreads, BL_LUT_MINWAVES) void k_lut_slab(
     constexpr int kPassNodes = kThreads / LPN;
     static_assert(NB % kPassNodes == 0, "node block must be whole passes");
     static_assert(R == 1 || R % 2 == 0, "R words are loaded as 8- or 16-byte pieces");
+    constexpr int kPasses = NB / kPassNodes;
+    static_assert(kPasses <= kWave, "a lane per pass stages the fan-ins");
     __shared__ int32_t s_conn[NB * K];
     __shared__ uint64_t s_tab[NB];
+    __shared__ int s_kp[SPEC ? kPasses + 2 : 1];
 
     const int bid = blockIdx.x;
     const int loc = local_of(bid);
@@ -395,24 +456,38 @@ __global__ __launch_bounds__(kThreads, BL_LUT_MINWAVES) void k_lut_slab(
         return;
     const int node0 = nblk * NB;
     const int nodes = min(NB, w_out - node0);
+    const int npass = (nodes + kPassNodes - 1) / kPassNodes;
 
     for (int q = threadIdx.x; q < NB * K; q += kThreads)
         s_conn[q] = (q < nodes * K) ? conn[(int64_t)node0 * K + q] : 0;
     for (int q = threadIdx.x; q < NB; q += kThreads)
         s_tab[q] = (q < nodes) ? tables[node0 + q] : 0;
+    if constexpr (SPEC)
+        stage_fanin<kPassNodes, K>(fanin, (w_out + kSpecPass - 1) / kSpecPass, node0, npass,
+                                   kPasses, s_kp);
     __syncthreads();
 
     const int sub = threadIdx.x % LPN;
     const int lnode = threadIdx.x / LPN;
     const uint64_t *src = in + (int64_t)slab * w_in * S + sub * R;
     uint64_t *dst = out + ((int64_t)slab * w_out + node0) * S + sub * R;
-    const int npass = (nodes + kPassNodes - 1) / kPassNodes;
 
-    constexpr int kPasses = NB / kPassNodes;
-    if constexpr (!SPEC && slab_prefetch<K>() && kPasses >= 2) {
+    if constexpr (slab_prefetch<K>() && kPasses >= 2) {
         if (nodes == NB) {
-            split_passes<K, R, kPasses, kPassNodes>(src, s_conn, s_tab, lnode, S, dst);
-            return;
+            if constexpr (SPEC) {
+                // a specialized block of one fan-in runs as a plain block of
+                // that fan-in
+                const int kmin = __builtin_amdgcn_readfirstlane(s_kp[kPasses]);
+                const int kmax = __builtin_amdgcn_readfirstlane(s_kp[kPasses + 1]);
+                if (kmin == kmax) {
+                    split_passes_kp<0, K, R, kPasses, kPassNodes>(kmax, src, s_conn, s_tab, lnode,
+                                                                  S, dst);
+                    return;
+                }
+            } else {
+                split_passes<K, K, R, kPasses, kPassNodes>(src, s_conn, s_tab, lnode, S, dst);
+                return;
+            }
         }
     }
     if constexpr (!SPEC && slab_prefetch<K>()) {
@@ -450,8 +525,7 @@ __global__ __launch_bounds__(kThreads, BL_LUT_MINWAVES) void k_lut_slab(
     for (int pass = 0; pass < npass; ++pass) {
         const int jl = pass * kPassNodes + lnode;
         if constexpr (SPEC) {
-            const int kp = pass_fanin<kPassNodes, K>(fanin, (w_out + kSpecPass - 1) / kSpecPass,
-                                                     node0 + pass * kPassNodes);
+            const int kp = __builtin_amdgcn_readfirstlane(s_kp[pass]);
             uint32_t o[2 * R];
             spec_eval<0, K, R>(kp, src, &s_conn[jl * K], S, s_tab[jl], o);
             store_out<R>(o, dst + (int64_t)jl * S, jl < nodes);
@@ -608,6 +682,56 @@ constexpr int head_min_waves()
     return (SPEC && K == 6) ? 3 : BL_HEAD_MINWAVES;
 }
 
+// The fused layer's pass loop for nodes of KP inputs whose connections are
+// KS apart in s_conn (KS = KP, or the layer's fan-in for a specialized block
+// of fan-in KP); KP = 0 is a constant node (table bit 0).  Each pass's output
+// bits go into the lane's bit-sliced counters.
+template <int KP, int KS>
+__device__ __forceinline__ void head_passes(int passes, const uint64_t *src,
+                                            const char *slab_base, uint32_t lane_off, bool off32,
+                                            const int32_t *s_conn, const uint64_t *s_tab,
+                                            int lnode, uint32_t (&ctr)[2 * kHeadR][kHeadCP])
+{
+#pragma unroll 1
+    for (int pass = 0; pass < passes; ++pass) {
+        const int jl = pass * kHeadPassNodes + lnode;
+        uint32_t o[2 * kHeadR];
+        if constexpr (KP == 0) {
+            const uint32_t m = 0u - (uint32_t)(s_tab[jl] & 1u);
+#pragma unroll
+            for (int h = 0; h < 2 * kHeadR; ++h)
+                o[h] = m;
+        } else {
+            uint32_t xv[2 * kHeadR][KP];
+            if (KP >= 5 && off32)
+                gather_off<KP, kHeadR>(slab_base, lane_off, &s_conn[jl * KS], kSlabWords, xv);
+            else
+                gather<KP, kHeadR>(src, &s_conn[jl * KS], kSlabWords, xv);
+            eval_node<KP, kHeadR>(s_tab[jl], xv, o);
+        }
+#pragma unroll
+        for (int h = 0; h < 2 * kHeadR; ++h)
+            bs_count<kHeadCP>(ctr[h], o[h]);
+    }
+}
+
+// head_passes at fan-in kp (wave-uniform, 0 <= kp <= K).
+template <int KQ, int K>
+__device__ __forceinline__ void head_passes_kp(int kp, int passes, const uint64_t *src,
+                                               const char *slab_base, uint32_t lane_off,
+                                               bool off32, const int32_t *s_conn,
+                                               const uint64_t *s_tab, int lnode,
+                                               uint32_t (&ctr)[2 * kHeadR][kHeadCP])
+{
+    if (kp == KQ) {
+        head_passes<KQ, K>(passes, src, slab_base, lane_off, off32, s_conn, s_tab, lnode, ctr);
+        return;
+    }
+    if constexpr (KQ < K)
+        head_passes_kp<KQ + 1, K>(kp, passes, src, slab_base, lane_off, off32, s_conn, s_tab,
+                                  lnode, ctr);
+}
+
 template <int K, int P, bool SPEC>
 __global__ __launch_bounds__(kThreads, (head_min_waves<K, SPEC>())) void k_lut_slab_head(
     const uint64_t *__restrict__ in, int32_t w_in, const int32_t *__restrict__ conn,
@@ -626,6 +750,8 @@ __global__ __launch_bounds__(kThreads, (head_min_waves<K, SPEC>())) void k_lut_s
     uint64_t *s_tab = reinterpret_cast<uint64_t *>(s_mem);
     int32_t *s_conn = reinterpret_cast<int32_t *>(s_mem + kHeadMaxPasses * kHeadPassNodes * 8);
     auto s_red = reinterpret_cast<uint32_t (*)[kHeadPassNodes][kHeadCP]>(s_mem);
+    static_assert(kHeadMaxPasses <= kWave, "a lane per pass stages the fan-ins");
+    __shared__ int s_kp[SPEC ? kHeadMaxPasses + 2 : 1];
 
     const int bid = blockIdx.x;
     const int loc = local_of(bid);
@@ -645,6 +771,9 @@ __global__ __launch_bounds__(kThreads, (head_min_waves<K, SPEC>())) void k_lut_s
         s_conn[q] = q < nodes * K ? conn[(int64_t)node0 * K + q] : 0;
     for (int q = threadIdx.x; q < staged; q += kThreads)
         s_tab[q] = q < nodes ? tables[node0 + q] : 0;
+    if constexpr (SPEC)
+        stage_fanin<kHeadPassNodes, K>(fanin, (g * c + kSpecPass - 1) / kSpecPass, node0, passes,
+                                       kHeadMaxPasses, s_kp);
     __syncthreads();
 
     const int sub = threadIdx.x % kHeadLPN;
@@ -661,25 +790,26 @@ __global__ __launch_bounds__(kThreads, (head_min_waves<K, SPEC>())) void k_lut_s
 #pragma unroll
         for (int p = 0; p < kHeadCP; ++p)
             ctr[h][p] = 0;
+    int kmin = K, kmax = K;
+    if constexpr (SPEC) {
+        kmin = __builtin_amdgcn_readfirstlane(s_kp[kHeadMaxPasses]);
+        kmax = __builtin_amdgcn_readfirstlane(s_kp[kHeadMaxPasses + 1]);
+    }
+    if (kmin == kmax) {
+        // a plain block, or a specialized block of one fan-in
+        head_passes_kp<0, K>(kmax, passes, src, slab_base, lane_off, off32, s_conn, s_tab, lnode,
+                             ctr);
+    } else {
 #pragma unroll 1
-    for (int pass = 0; pass < passes; ++pass) {
-        const int jl = pass * kHeadPassNodes + lnode;
-        uint32_t o[2 * kHeadR];
-        if constexpr (SPEC) {
-            const int kp = pass_fanin<kHeadPassNodes, K>(fanin, (g * c + kSpecPass - 1) / kSpecPass,
-                                                         node0 + pass * kHeadPassNodes);
+        for (int pass = 0; pass < passes; ++pass) {
+            const int jl = pass * kHeadPassNodes + lnode;
+            uint32_t o[2 * kHeadR];
+            const int kp = __builtin_amdgcn_readfirstlane(s_kp[pass]);
             spec_eval<0, K, kHeadR>(kp, src, &s_conn[jl * K], kSlabWords, s_tab[jl], o);
-        } else {
-            uint32_t xv[2 * kHeadR][K];
-            if (K >= 5 && off32)
-                gather_off<K, kHeadR>(slab_base, lane_off, &s_conn[jl * K], kSlabWords, xv);
-            else
-                gather<K, kHeadR>(src, &s_conn[jl * K], kSlabWords, xv);
-            eval_node<K, kHeadR>(s_tab[jl], xv, o);
-        }
 #pragma unroll
-        for (int h = 0; h < 2 * kHeadR; ++h)
-            bs_count<kHeadCP>(ctr[h], o[h]);
+            for (int h = 0; h < 2 * kHeadR; ++h)
+                bs_count<kHeadCP>(ctr[h], o[h]);
+        }
     }
 
     // lane counters -> LDS (over the staging area), one row of 32 node lanes
