@@ -149,3 +149,24 @@ def test_collapsed_workload_full_batch():
     for h in m.fanin_histogram:
         assert h[4:].sum() == 0                      # at most 3 distinct wires per node
     assert all(layer[0].shape[1] == 3 for layer in m.layers)
+
+
+def test_specialized_large_batch_block_modes():
+    # 2^18 samples: the stored layers run 512-node blocks (>= 2048 a launch),
+    # specialized to fan-in 4, 2 and 1 (slots drawn from 4, 2 and 1 wires);
+    # blocks whose passes share one fan-in run the plain loops of that
+    # fan-in, blocks that mix fan-ins the per-pass loop, and widths that are
+    # not multiples of 512 leave a short last block.  The last layer (fan-in
+    # 3, 256 nodes a class) is fused with the head.
+    rng = np.random.default_rng(2024)
+    n, d, b = 1 << 18, 64, 4
+    x = rng.integers(0, 256, size=(n, d), dtype=np.uint8)
+    th = np.sort(rng.integers(0, 256, size=(d, b)), axis=1).astype(np.uint8)
+    layers, w_in = [], d * b
+    for w, k, pool in ((5000, 6, 4), (4700, 4, 2), (4300, 3, 1), (2560, 6, 3)):
+        layers += _network(rng, w_in, [w], [k], pool)
+        w_in = w
+    print(f"[spec-blocks] n={n}, widths 5000/4700/4300/2560, every sample", flush=True)
+    m = _check(x, th, layers, 10, 0.0)
+    assert [int(conn.shape[1]) for conn, _ in m.layers] == [4, 2, 1, 3]
+    assert m.plan(n)["fused_head"]
