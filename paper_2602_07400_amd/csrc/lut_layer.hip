@@ -456,21 +456,21 @@ __global__ __launch_bounds__(kThreads, BL_LUT_MINWAVES) void k_lut_slab(
         return;
     const int node0 = nblk * NB;
     const int nodes = min(NB, w_out - node0);
-    const int npass = (nodes + kPassNodes - 1) / kPassNodes;
 
     for (int q = threadIdx.x; q < NB * K; q += kThreads)
         s_conn[q] = (q < nodes * K) ? conn[(int64_t)node0 * K + q] : 0;
     for (int q = threadIdx.x; q < NB; q += kThreads)
         s_tab[q] = (q < nodes) ? tables[node0 + q] : 0;
     if constexpr (SPEC)
-        stage_fanin<kPassNodes, K>(fanin, (w_out + kSpecPass - 1) / kSpecPass, node0, npass,
-                                   kPasses, s_kp);
+        stage_fanin<kPassNodes, K>(fanin, (w_out + kSpecPass - 1) / kSpecPass, node0,
+                                   (nodes + kPassNodes - 1) / kPassNodes, kPasses, s_kp);
     __syncthreads();
 
     const int sub = threadIdx.x % LPN;
     const int lnode = threadIdx.x / LPN;
     const uint64_t *src = in + (int64_t)slab * w_in * S + sub * R;
     uint64_t *dst = out + ((int64_t)slab * w_out + node0) * S + sub * R;
+    const int npass = (nodes + kPassNodes - 1) / kPassNodes;
 
     if constexpr (slab_prefetch<K>() && kPasses >= 2) {
         if (nodes == NB) {
@@ -831,8 +831,29 @@ __global__ __launch_bounds__(kThreads, (head_min_waves<K, SPEC>())) void k_lut_s
         kmin = __builtin_amdgcn_readfirstlane(s_kp[kHeadMaxPasses]);
         kmax = __builtin_amdgcn_readfirstlane(s_kp[kHeadMaxPasses + 1]);
     }
-    if (kmin == kmax) {
-        // a plain block, or a specialized block of one fan-in
+    if constexpr (!SPEC && K >= 5) {
+        // the plain loop of 5 and 6 inputs written out here rather than
+        // through head_passes: the same instructions, but the helper's loop
+        // entry moved the register allocation, and C3's fused layer (k = 6)
+        // measured 2% slower with it (ABBA)
+#pragma unroll 1
+        for (int pass = 0; pass < passes; ++pass) {
+            const int jl = pass * kHeadPassNodes + lnode;
+            uint32_t o[2 * kHeadR];
+            uint32_t xv[2 * kHeadR][K];
+            if (off32)
+                gather_off<K, kHeadR>(slab_base, lane_off, &s_conn[jl * K], kSlabWords, xv);
+            else
+                gather<K, kHeadR>(src, &s_conn[jl * K], kSlabWords, xv);
+            eval_node<K, kHeadR>(s_tab[jl], xv, o);
+#pragma unroll
+            for (int h = 0; h < 2 * kHeadR; ++h)
+                bs_count<kHeadCP>(ctr[h], o[h]);
+        }
+    } else if constexpr (!SPEC) {
+        head_passes<K, K>(passes, src, slab_base, lane_off, off32, s_conn, s_tab, lnode, ctr);
+    } else if (kmin == kmax) {
+        // a specialized block of one fan-in runs the plain loop of that fan-in
         head_passes_kp<0, K>(kmax, passes, src, slab_base, lane_off, off32, s_conn, s_tab, lnode,
                              ctr);
     } else {
