@@ -252,11 +252,12 @@ __device__ __forceinline__ void eval_store(uint64_t T, const uint32_t (&xv)[2 * 
 }
 
 // Specialized layers (table specialization, see specialize.hip): the nodes of
-// a pass share one evaluated fan-in kp <= K, read per pass from the layer's
-// fan-in array (one entry per kSpecPass nodes; a pass spanning several
-// entries takes their maximum).  kp is uniform over the block, so the
-// dispatch below is a scalar branch: the pass gathers kp wires and runs the
-// 2^kp - 1 multiplexer tree; kp = 0 is a constant node (table bit 0).
+// a pass share one evaluated fan-in kp <= K, taken from the layer's fan-in
+// array (one entry per kSpecPass nodes; a pass spanning several entries
+// takes their maximum) and staged per pass in LDS (stage_fanin below).  kp
+// is uniform over the block, so the dispatch below is a scalar branch: the
+// pass gathers kp wires and runs the 2^kp - 1 multiplexer tree; kp = 0 is a
+// constant node (table bit 0).
 template <int KQ, int K, int R>
 __device__ __forceinline__ void spec_eval(int kp, const uint64_t *src, const int32_t *c, int S,
                                           uint64_t T, uint32_t (&o)[2 * R])
