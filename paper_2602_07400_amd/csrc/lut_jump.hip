@@ -25,9 +25,12 @@
 // lanes 32-63: slab 2p + 1; one 32-bit half-word, 32 samples, a lane), so
 // every gather is a coalesced 128-byte row segment per half wave and every
 // store two whole lines.  A wave walks kJumpNodesPerWave consecutive nodes;
-// the next node's 6 rows are in flight while the current one is evaluated,
-// and the wait for them leaves the previous node's store in flight (C2's
-// layer 1 0.68 -> 0.64 ms, C3's 0.54 -> 0.52 ms against waiting for it too).
+// the next node's 6 rows are in flight while the current one is evaluated.
+// Each node's output goes to LDS, and the wave stores its nodes' outputs
+// after its last gather: its vector-memory counter retires loads and stores
+// in issue order, so a gather issued after a store would wait for that
+// store's acknowledgement (against a store per node in the loop: C2's layer
+// 1 0.651 -> 0.628 ms, C3's 0.538 -> 0.527 ms, ABBA).
 // The cost is the working set: a slab pair of w_in rows is w_in * 256
 // bytes per XCD, twice the per-lane layout's.  The layer is therefore used
 // only where that fits the 4 MB L2 with room to spare (w_in <= 12288, e.g.
@@ -158,7 +161,8 @@ __device__ __forceinline__ i32x4 buffer_rsrc(const void *base, uint32_t bytes)
 //   s[48:55]  row offsets of the node after next; s[64:79] leaf addresses of
 //             the current node; s[80:81] return address (label L_ret)
 //   s45       byte offset of the current node's record, s46 of its output
-//             row within the slab pair, s44 the end of the wave's rows
+//             row within the slab pair (the loop counter), s44 the end of the
+//             wave's rows; the lds operand: this lane's slot for the node
 // Records are read up to two past the wave's last node, which the caller's
 // record array holds (kJumpPadRecs).
 __global__ __launch_bounds__(kJumpThreads) void k_jump_layer(
@@ -181,9 +185,12 @@ __global__ __launch_bounds__(kJumpThreads) void k_jump_layer(
     const char *ib = reinterpret_cast<const char *>(in) + (int64_t)pair * 2 * w_in * kRow;
     char *ob = reinterpret_cast<char *>(out) + (int64_t)pair * 2 * w_out * kRow;
     const i32x4 rin = buffer_rsrc(ib, (uint32_t)(2 * w_in * kRow));
-    const i32x4 rout = buffer_rsrc(ob, (uint32_t)(2 * w_out * kRow));
     const uint32_t vin = (uint32_t)(lane / 32) * (uint32_t)w_in * kRow + (lane % 32) * 4u;
     const uint32_t vout = (uint32_t)(lane / 32) * (uint32_t)w_out * kRow + (lane % 32) * 4u;
+    // each node's output half-word goes to LDS in the loop (ds_write, counted
+    // by lgkmcnt), and the wave stores its nodes after its last gather
+    __shared__ uint32_t s_out[kJumpThreads / kWave][kJumpNodesPerWave][kWave];
+    uint32_t lds = (uint32_t)reinterpret_cast<uintptr_t>(&s_out[wave][0][lane]);
     const uint32_t roff = __builtin_amdgcn_readfirstlane((uint32_t)n0 * kJumpRecBytes);
     const uint32_t ooff = __builtin_amdgcn_readfirstlane((uint32_t)n0 * kRow);
     const uint32_t oend = __builtin_amdgcn_readfirstlane((uint32_t)(n0 + cnt) * kRow);
@@ -209,12 +216,11 @@ __global__ __launch_bounds__(kJumpThreads) void k_jump_layer(
         "s_load_dwordx16 s[64:79], %[rec], s45\n"
         "s_waitcnt vmcnt(0)\n"
         "s_branch L_first%=\n"
-        // vector memory operations complete in issue order, so with at most
-        // one outstanding, this node's gathers (issued before the previous
-        // node's store) have landed while that store may still be in flight;
-        // the first node, with no store ahead of it, waited for all above
+        // only this node's gathers are outstanding: the outputs go to LDS,
+        // so no store sits ahead of a gather in the wave's vector-memory
+        // counter (it retires in issue order)
         "L_node%=:\n"
-        "s_waitcnt vmcnt(1)\n"
+        "s_waitcnt vmcnt(0)\n"
         "L_first%=:\n"
         "v_mov_b32 v14, v8\n"
         "v_mov_b32 v15, v9\n"
@@ -242,20 +248,27 @@ __global__ __launch_bounds__(kJumpThreads) void k_jump_layer(
         "v_bitop3_b32 v20, v18, v22, v20 bitop3:0xca\n"
         "v_bitop3_b32 v24, v18, v26, v24 bitop3:0xca\n"
         "v_bitop3_b32 v20, v19, v24, v20 bitop3:0xca\n"
-        "buffer_store_dword v20, %[vout], %[rout], s46 offen nt\n"
+        "ds_write_b32 %[lds], v20\n"
+        "v_add_u32_e32 %[lds], 0x100, %[lds]\n"
         "s_add_u32 s46, s46, 0x80\n"
         "s_add_u32 s45, s45, 0x80\n"
         "s_cmp_lg_u32 s46, s44\n"
         "s_cbranch_scc1 L_node%=\n"
         "s_waitcnt vmcnt(0) lgkmcnt(0)\n"
-        :
+        : [lds] "+v"(lds)
         : [roff] "s"(roff), [ooff] "s"(ooff), [oend] "s"(oend), [rec] "s"(rec),
-          [rin] "s"(rin), [rout] "s"(rout), [vin] "v"(vin), [vout] "v"(vout)
+          [rin] "s"(rin), [vin] "v"(vin)
         : "memory", "scc", "s40", "s41", "s44", "s45", "s46", "s48", "s49", "s50", "s51", "s52",
           "s53", "s54", "s55", "s64", "s65", "s66", "s67", "s68", "s69", "s70", "s71", "s72",
           "s73", "s74", "s75", "s76", "s77", "s78", "s79", "s80", "s81", "v8", "v9", "v10",
           "v11", "v12", "v13", "v14", "v15", "v16", "v17", "v18", "v19", "v20", "v21", "v22",
           "v23", "v24", "v25", "v26", "v27");
+    // the wave's outputs, one half-word a lane and node: nodes n0 .. n0 + cnt
+    // are rows of the slab pair's output, 128 bytes apart
+    char *o = ob + vout + (uint32_t)n0 * kRow;
+    for (int i = 0; i < cnt; ++i)
+        __builtin_nontemporal_store(s_out[wave][i][lane],
+                                    reinterpret_cast<uint32_t *>(o + (uint32_t)i * kRow));
 }
 
 }  // namespace
